@@ -1,0 +1,261 @@
+"""CPU oracle for the Sherry 3:4 ternary product -- TEST INFRASTRUCTURE.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never does, and
+this package never imports the product: the two share no code.
+
+The arithmetic lives in ``sherry_oracle.c`` (plain C, built with gcc); this
+module only marshals numpy arrays through ctypes.  Each function names the
+passage of the paper it follows; see the header of ``sherry_oracle.c``.
+
+Parity status of each piece (what pins it, in ``tests/test_oracle.py``):
+
+* code table         -- pinned: hand-derived table (tests/golden), exhaustive
+                         counts (32 of 81 tuples, Sec. 3.1), mirror pairs
+                         (16, Appendix C);
+* pack / unpack      -- pinned: hand-derived byte fixtures (tests/golden),
+                         round trips, 3:4 rejection;
+* act. quantization  -- pinned: absmax -> +-127, exact multiples, RNE ties,
+                         zero rows, clamp;
+* product            -- pinned: numpy int64 matmul, pure-Python brute force,
+                         one-hot / all-ones closed forms;
+* epilogue           -- pinned: exactly representable scale products;
+* ternarizer         -- pinned: brute force over all 32 patterns per block
+                         (Appendix D) and least-squares alpha (Eq. 5);
+* 2-bit codec        -- pinned: hand-derived bytes and round trips.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sherry_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle with gcc (plain -O2, no intrinsics)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call([
+            "gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+            "-fno-fast-math", "-pthread", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        i8p = ctypes.POINTER(ctypes.c_int8)
+        u8p = ctypes.POINTER(ctypes.c_uint8)
+        i64 = ctypes.c_int64
+        L.oracle_code_table.argtypes = [i8p]
+        L.oracle_code_table.restype = ctypes.c_int
+        L.oracle_encode_block.argtypes = [i8p]
+        L.oracle_encode_block.restype = ctypes.c_int
+        L.oracle_decode_code.argtypes = [ctypes.c_int, i8p]
+        L.oracle_decode_code.restype = None
+        L.oracle_packed_bytes.argtypes = [i64, i64]
+        L.oracle_packed_bytes.restype = i64
+        L.oracle_pack.argtypes = [i8p, i64, i64, u8p]
+        L.oracle_pack.restype = i64
+        L.oracle_unpack.argtypes = [u8p, i64, i64, i8p]
+        L.oracle_unpack.restype = ctypes.c_int
+        L.oracle_quantize_act.argtypes = [ctypes.POINTER(ctypes.c_float), i64, i64, i8p,
+                                          ctypes.POINTER(ctypes.c_float)]
+        L.oracle_quantize_act.restype = None
+        L.oracle_gemm_i32.argtypes = [i8p, i8p, i64, i64, i64,
+                                      ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
+        L.oracle_gemm_i32.restype = None
+        L.oracle_dot_i32.argtypes = [i8p, i8p, i64]
+        L.oracle_dot_i32.restype = ctypes.c_int32
+        L.oracle_epilogue.argtypes = [ctypes.POINTER(ctypes.c_int32),
+                                      ctypes.POINTER(ctypes.c_float), ctypes.c_float,
+                                      i64, i64, ctypes.POINTER(ctypes.c_double)]
+        L.oracle_epilogue.restype = None
+        L.oracle_ternarize.argtypes = [ctypes.POINTER(ctypes.c_float), i64, i64, i8p]
+        L.oracle_ternarize.restype = ctypes.c_double
+        L.oracle_packed2_bytes.argtypes = [i64, i64]
+        L.oracle_packed2_bytes.restype = i64
+        L.oracle_pack2.argtypes = [i8p, i64, i64, u8p]
+        L.oracle_pack2.restype = i64
+        L.oracle_unpack2.argtypes = [u8p, i64, i64, i8p]
+        L.oracle_unpack2.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray, ct):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.POINTER(ct))
+
+
+class OracleError(ValueError):
+    pass
+
+
+# ---- (i) code table (Sec. 3.1 point 3) -----------------------------------
+
+def code_table() -> np.ndarray:
+    """int8 [32][4]: weights of each 5-bit code, built by enumeration."""
+    t = np.zeros((32, 4), dtype=np.int8)
+    n = lib().oracle_code_table(_p(t, ctypes.c_int8))
+    if n != 32:
+        raise OracleError("code table enumeration accepted %d tuples" % n)
+    return t
+
+
+def encode_block(w) -> int:
+    a = np.ascontiguousarray(np.asarray(w, dtype=np.int8).reshape(4))
+    return int(lib().oracle_encode_block(_p(a, ctypes.c_int8)))
+
+
+def decode_code(c: int) -> np.ndarray:
+    w = np.zeros(4, dtype=np.int8)
+    lib().oracle_decode_code(int(c), _p(w, ctypes.c_int8))
+    return w
+
+
+# ---- (ii) packed layout (Appendix A, offline packing) --------------------
+
+def packed_bytes(n: int, k: int) -> int:
+    return int(lib().oracle_packed_bytes(n, k))
+
+
+def pack(t: np.ndarray) -> np.ndarray:
+    t = np.ascontiguousarray(t, dtype=np.int8)
+    n, k = t.shape
+    nb = packed_bytes(n, k)
+    if nb == 0:
+        raise OracleError("bad shape %s" % (t.shape,))
+    out = np.zeros(nb, dtype=np.uint8)
+    rc = lib().oracle_pack(_p(t, ctypes.c_int8), n, k, _p(out, ctypes.c_uint8))
+    if rc != 0:
+        raise OracleError("block %d is not 3:4" % (-rc - 1))
+    return out
+
+
+def pack_bad_block(t: np.ndarray):
+    """Flat index of the first non-3:4 block, or None if T packs."""
+    t = np.ascontiguousarray(t, dtype=np.int8)
+    n, k = t.shape
+    out = np.zeros(packed_bytes(n, k), dtype=np.uint8)
+    rc = lib().oracle_pack(_p(t, ctypes.c_int8), n, k, _p(out, ctypes.c_uint8))
+    return None if rc == 0 else int(-rc - 1)
+
+
+def unpack(p: np.ndarray, n: int, k: int) -> np.ndarray:
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    if p.size < packed_bytes(n, k):
+        raise OracleError("packed buffer too small")
+    t = np.zeros((n, k), dtype=np.int8)
+    if lib().oracle_unpack(_p(p, ctypes.c_uint8), n, k, _p(t, ctypes.c_int8)) != 0:
+        raise OracleError("bad shape")
+    return t
+
+
+# ---- (iii) activation quantization ---------------------------------------
+
+def quantize_act(x: np.ndarray):
+    """fp32 [m][k] -> (int8 [m][k], fp32 sx [m]); absmax/127, RNE, clamp."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x[None, :]
+    m, k = x.shape
+    q = np.zeros((m, k), dtype=np.int8)
+    sx = np.zeros(m, dtype=np.float32)
+    lib().oracle_quantize_act(_p(x, ctypes.c_float), m, k, _p(q, ctypes.c_int8),
+                              _p(sx, ctypes.c_float))
+    return q, sx
+
+
+# ---- (iv) product of Eq. 2 on the unpacked T ------------------------------
+
+def gemm_i32(x: np.ndarray, t: np.ndarray, threads: int = 1) -> np.ndarray:
+    """acc [m][n] = x [m][k] . t[n][k]^T in exact integers."""
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    t = np.ascontiguousarray(t, dtype=np.int8)
+    if x.ndim == 1:
+        x = x[None, :]
+    m, k = x.shape
+    n, k2 = t.shape
+    if k != k2:
+        raise OracleError("k mismatch")
+    acc = np.zeros((m, n), dtype=np.int32)
+    lib().oracle_gemm_i32(_p(x, ctypes.c_int8), _p(t, ctypes.c_int8), m, n, k,
+                          _p(acc, ctypes.c_int32), int(threads))
+    return acc
+
+
+def dot_i32(x_row: np.ndarray, t_row: np.ndarray) -> int:
+    x_row = np.ascontiguousarray(x_row, dtype=np.int8)
+    t_row = np.ascontiguousarray(t_row, dtype=np.int8)
+    return int(lib().oracle_dot_i32(_p(x_row, ctypes.c_int8), _p(t_row, ctypes.c_int8),
+                                    x_row.size))
+
+
+# ---- (v) epilogue (Eq. 2 scaling), fp64 -----------------------------------
+
+def epilogue(acc: np.ndarray, sx: np.ndarray, sw: float) -> np.ndarray:
+    acc = np.ascontiguousarray(acc, dtype=np.int32)
+    sx = np.ascontiguousarray(sx, dtype=np.float32)
+    m, n = acc.shape
+    y = np.zeros((m, n), dtype=np.float64)
+    lib().oracle_epilogue(_p(acc, ctypes.c_int32), _p(sx, ctypes.c_float),
+                          ctypes.c_float(sw), m, n, _p(y, ctypes.c_double))
+    return y
+
+
+# ---- (vi) Sparse-AbsMean ternarizer (Eq. 4, Eq. 5) -------------------------
+
+def ternarize(w: np.ndarray):
+    """fp32 [n][k] -> (int8 T [n][k], per-tensor alpha as float)."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    n, k = w.shape
+    t = np.zeros((n, k), dtype=np.int8)
+    alpha = lib().oracle_ternarize(_p(w, ctypes.c_float), n, k, _p(t, ctypes.c_int8))
+    return t, float(alpha)
+
+
+# ---- (vii) 2-bit layout ----------------------------------------------------
+
+def packed2_bytes(n: int, k: int) -> int:
+    return int(lib().oracle_packed2_bytes(n, k))
+
+
+def pack2(t: np.ndarray) -> np.ndarray:
+    t = np.ascontiguousarray(t, dtype=np.int8)
+    n, k = t.shape
+    out = np.zeros(packed2_bytes(n, k), dtype=np.uint8)
+    rc = lib().oracle_pack2(_p(t, ctypes.c_int8), n, k, _p(out, ctypes.c_uint8))
+    if rc != 0:
+        raise OracleError("bad weight at %d" % (-rc - 1))
+    return out
+
+
+def unpack2(p: np.ndarray, n: int, k: int) -> np.ndarray:
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    t = np.zeros((n, k), dtype=np.int8)
+    if lib().oracle_unpack2(_p(p, ctypes.c_uint8), n, k, _p(t, ctypes.c_int8)) != 0:
+        raise OracleError("bad 2-bit stream")
+    return t
+
+
+# ---- convenience: the whole path on the CPU --------------------------------
+
+def linear(x_f32: np.ndarray, t: np.ndarray, sw: float, threads: int = 1):
+    """Quantize x, multiply by T, scale: returns (q, sx, acc, y_fp64)."""
+    q, sx = quantize_act(x_f32)
+    acc = gemm_i32(q, t, threads)
+    return q, sx, acc, epilogue(acc, sx, sw)

@@ -1,0 +1,384 @@
+/*
+ * sherry_oracle.c -- plain, slow, obviously-correct CPU oracle for the Sherry
+ * 3:4 sparse ternary product (arXiv 2601.07892).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library may include, link,
+ * load or call this file.  Only the tests, the smoke check and the CPU-baseline
+ * leg of the benchmark use it.  It shares no code, header, table or constant
+ * with the HIP path; the two meet only at the bytes of the packed format and
+ * at the numbers they compute.
+ *
+ * What it computes, and the passage each part follows:
+ *
+ *  (i)   code table    -- Sec. 3.1, "sweet spot" point (3): a 4-weight block
+ *                         with exactly one zero and three signs has
+ *                         C(4,3)*2^3 = 32 states, one per 5-bit code.  The
+ *                         assignment of bits is this project's reading: low 2
+ *                         bits = position of the zero inside the block, bit
+ *                         2+i = sign of the i-th non-zero in ascending
+ *                         position (1 means -1).  Built by enumerating all 81
+ *                         ternary 4-tuples.
+ *  (ii)  pack/unpack   -- Appendix A (offline packing phase): each 4-block is
+ *                         stored as one 5-bit code in a word-aligned stream.
+ *                         The stream layout is this project's own (the paper
+ *                         gives none); it is written out bit by bit below.
+ *  (iii) act. quant.   -- not in the paper (weight-only, Limitations) yet the
+ *                         engine accumulates in integers (Appendix A, online
+ *                         phase): int8 per-token absmax/127, fp32 decisions.
+ *  (iv)  product       -- Eq. 2, Y = X T alpha, with T in {-1,0,1} satisfying
+ *                         the 3:4 constraint of Eq. 3.  Plain dense integer
+ *                         triple loop on the UNPACKED T; never reads a code.
+ *  (v)   epilogue      -- Eq. 2 scaling, y = acc * sx * sw, in fp64.
+ *  (vi)  ternarizer    -- Eq. 4 (Sparse-AbsMean) and Eq. 5 (alpha), with a
+ *                         per-tensor alpha.
+ *  (vii) 2-bit codec   -- the "2-bit strategy" of Sec. 2.3 (one ternary
+ *                         weight per 2 bits), used only as a bytes-moved
+ *                         comparison; layout is this project's own.
+ *
+ * Build: gcc -O2 -std=c11 -fPIC -shared -ffp-contract=off -pthread.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* (i) code table by enumeration                                            */
+/* ------------------------------------------------------------------------ */
+
+static int8_t g_table[32][4];
+static int g_table_ready = 0;
+
+/* Fills table[c][p] = weight at block position p for code c.  Returns the
+ * number of ternary 4-tuples accepted (must be 32; 81 are enumerated). */
+int oracle_code_table(int8_t table[32][4]) {
+  int accepted = 0;
+  int filled[32];
+  for (int c = 0; c < 32; ++c) filled[c] = 0;
+  const int vals[3] = {-1, 0, 1};
+  for (int a = 0; a < 3; ++a)
+    for (int b = 0; b < 3; ++b)
+      for (int d = 0; d < 3; ++d)
+        for (int e = 0; e < 3; ++e) {
+          int w[4] = {vals[a], vals[b], vals[d], vals[e]};
+          int zeros = 0, zpos = -1;
+          for (int p = 0; p < 4; ++p)
+            if (w[p] == 0) { ++zeros; zpos = p; }
+          if (zeros != 1) continue; /* violates the 3:4 constraint (Eq. 3) */
+          /* signs of the three non-zeros, in ascending position */
+          int code = zpos, i = 0;
+          for (int p = 0; p < 4; ++p) {
+            if (p == zpos) continue;
+            if (w[p] < 0) code += 1 << (2 + i);
+            ++i;
+          }
+          if (filled[code]) return -1; /* two tuples on one code: broken */
+          filled[code] = 1;
+          for (int p = 0; p < 4; ++p) table[code][p] = (int8_t)w[p];
+          ++accepted;
+        }
+  return accepted;
+}
+
+static void ensure_table(void) {
+  if (!g_table_ready) {
+    oracle_code_table(g_table);
+    g_table_ready = 1;
+  }
+}
+
+/* Code of one block by searching the table; -1 if the block is not 3:4. */
+int oracle_encode_block(const int8_t w[4]) {
+  ensure_table();
+  for (int c = 0; c < 32; ++c) {
+    if (g_table[c][0] == w[0] && g_table[c][1] == w[1] &&
+        g_table[c][2] == w[2] && g_table[c][3] == w[3])
+      return c;
+  }
+  return -1;
+}
+
+void oracle_decode_code(int c, int8_t w[4]) {
+  ensure_table();
+  for (int p = 0; p < 4; ++p) w[p] = g_table[c & 31][p];
+}
+
+/* ------------------------------------------------------------------------ */
+/* (ii) the 5-bit tiled layout, bit by bit                                  */
+/*                                                                          */
+/* Rows are padded to Np = ceil(N/64)*64 and the reduction dimension to      */
+/* Kp = ceil(K/512)*512; padding codes are all-zero bits.  The matrix is a   */
+/* grid of units of 64 rows x 512 weights (5120 bytes), unit (r, s) at byte  */
+/* (r*S + s)*5120 with S = Kp/512.  Inside a unit, row i (0..63) holds four  */
+/* containers h (0..3) of 32 consecutive codes, covering weights            */
+/* 512*s + 128*h .. +127.  A container is a 160-bit little-endian stream,    */
+/* code j at stream bits [5j, 5j+5) (code bit q at stream bit 5j+q).  Stream */
+/* bits 0..127 go to the head bytes at 1024*h + 16*i + (0..15); stream bits  */
+/* 128..159 to the tail bytes at 4096 + 16*i + 4*h + (0..3).  Inside a byte, */
+/* stream bit 8*p + t is bit t (LSB first).                                  */
+/* ------------------------------------------------------------------------ */
+
+static int64_t ceil_to(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+int64_t oracle_packed_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1 || k % 4 != 0) return 0;
+  return ceil_to(n, 64) * ceil_to(k, 512) * 5 / 32;
+}
+
+/* Byte offset and bit inside it for stream bit sp of container h, row n,
+ * block-column s (unit column), in a matrix with S unit columns. */
+static void stream_bit_addr(int64_t n, int64_t s, int h, int sp, int64_t S,
+                            int64_t* byte, int* bit) {
+  int64_t r = n / 64;
+  int i = (int)(n % 64);
+  int64_t unit = (r * S + s) * 5120;
+  if (sp < 128) {
+    *byte = unit + 1024 * h + 16 * i + sp / 8;
+    *bit = sp % 8;
+  } else {
+    *byte = unit + 4096 + 16 * i + 4 * h + (sp - 128) / 8;
+    *bit = (sp - 128) % 8;
+  }
+}
+
+/* Packs T (N x K, row-major, values in {-1,0,1}) into out, which must hold
+ * oracle_packed_bytes(n, k) bytes.  Returns 0, or -(b+1) where b is the flat
+ * index (n*K/4 + block) of the first block that is not 3:4. */
+int64_t oracle_pack(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
+  int64_t bytes = oracle_packed_bytes(n, k);
+  if (bytes == 0) return -((int64_t)1 << 62);
+  memset(out, 0, (size_t)bytes);
+  int64_t S = ceil_to(k, 512) / 512;
+  int64_t nb = k / 4;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t b = 0; b < nb; ++b) {
+      int code = oracle_encode_block(t + row * k + 4 * b);
+      if (code < 0) return -(row * nb + b + 1);
+      int64_t kk = 4 * b;             /* first weight of the block      */
+      int64_t s = kk / 512;           /* unit column                    */
+      int h = (int)((kk % 512) / 128);/* container inside the unit      */
+      int j = (int)((kk % 128) / 4);  /* code inside the container      */
+      for (int q = 0; q < 5; ++q) {
+        int64_t byte;
+        int bit;
+        stream_bit_addr(row, s, h, 5 * j + q, S, &byte, &bit);
+        if ((code >> q) & 1) out[byte] |= (uint8_t)(1u << bit);
+      }
+    }
+  }
+  return 0;
+}
+
+/* Inverse of oracle_pack for the first n rows and k weights. */
+int oracle_unpack(const uint8_t* p, int64_t n, int64_t k, int8_t* t) {
+  if (oracle_packed_bytes(n, k) == 0) return -1;
+  int64_t S = ceil_to(k, 512) / 512;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t b = 0; b < k / 4; ++b) {
+      int64_t kk = 4 * b;
+      int64_t s = kk / 512;
+      int h = (int)((kk % 512) / 128);
+      int j = (int)((kk % 128) / 4);
+      int code = 0;
+      for (int q = 0; q < 5; ++q) {
+        int64_t byte;
+        int bit;
+        stream_bit_addr(row, s, h, 5 * j + q, S, &byte, &bit);
+        code |= ((p[byte] >> bit) & 1) << q;
+      }
+      oracle_decode_code(code, t + row * k + kk);
+    }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* (iii) activation quantization: int8 per token, absmax/127                */
+/* Decisions in fp32 (IEEE division, round-half-to-even), as the kernel.    */
+/* ------------------------------------------------------------------------ */
+
+void oracle_quantize_act(const float* x, int64_t m, int64_t k, int8_t* q,
+                         float* sx) {
+  for (int64_t r = 0; r < m; ++r) {
+    const float* xr = x + r * k;
+    float amax = 0.0f;
+    for (int64_t i = 0; i < k; ++i) {
+      float a = fabsf(xr[i]);
+      if (a > amax) amax = a;
+    }
+    if (amax == 0.0f) {
+      sx[r] = 0.0f;
+      for (int64_t i = 0; i < k; ++i) q[r * k + i] = 0;
+      continue;
+    }
+    volatile float s = amax / 127.0f; /* volatile: keep it an fp32 value */
+    sx[r] = s;
+    for (int64_t i = 0; i < k; ++i) {
+      volatile float v = xr[i] / s;
+      float rv = rintf(v); /* default rounding mode: to nearest, ties even */
+      if (rv > 127.0f) rv = 127.0f;
+      if (rv < -127.0f) rv = -127.0f;
+      q[r * k + i] = (int8_t)rv;
+    }
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* (iv) the product of Eq. 2 on the unpacked T, plain triple loop           */
+/* acc[m][n] = sum_k x[m][k] * t[n][k]                                      */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  const int8_t* x;
+  const int8_t* t;
+  int32_t* acc;
+  int64_t m, n, k, n0, n1;
+} gemm_job;
+
+static void* gemm_rows(void* arg) {
+  gemm_job* j = (gemm_job*)arg;
+  for (int64_t mm = 0; mm < j->m; ++mm) {
+    for (int64_t nn = j->n0; nn < j->n1; ++nn) {
+      int64_t sum = 0;
+      for (int64_t kk = 0; kk < j->k; ++kk)
+        sum += (int64_t)j->x[mm * j->k + kk] * (int64_t)j->t[nn * j->k + kk];
+      j->acc[mm * j->n + nn] = (int32_t)sum;
+    }
+  }
+  return 0;
+}
+
+/* threads <= 1 runs on the calling thread; otherwise output rows n are split
+ * into `threads` contiguous ranges. */
+void oracle_gemm_i32(const int8_t* x, const int8_t* t, int64_t m, int64_t n,
+                     int64_t k, int32_t* acc, int threads) {
+  if (threads <= 1 || n < threads) {
+    gemm_job j = {x, t, acc, m, n, k, 0, n};
+    gemm_rows(&j);
+    return;
+  }
+  pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)threads);
+  gemm_job* jobs = (gemm_job*)malloc(sizeof(gemm_job) * (size_t)threads);
+  for (int i = 0; i < threads; ++i) {
+    gemm_job j = {x, t, acc, m, n, k, n * i / threads, n * (i + 1) / threads};
+    jobs[i] = j;
+    pthread_create(&th[i], 0, gemm_rows, &jobs[i]);
+  }
+  for (int i = 0; i < threads; ++i) pthread_join(th[i], 0);
+  free(th);
+  free(jobs);
+}
+
+/* Single output element, for sampled checks at full size. */
+int32_t oracle_dot_i32(const int8_t* x_row, const int8_t* t_row, int64_t k) {
+  int64_t sum = 0;
+  for (int64_t kk = 0; kk < k; ++kk) sum += (int64_t)x_row[kk] * t_row[kk];
+  return (int32_t)sum;
+}
+
+/* ------------------------------------------------------------------------ */
+/* (v) epilogue in fp64: y = acc * sx[m] * sw                               */
+/* ------------------------------------------------------------------------ */
+
+void oracle_epilogue(const int32_t* acc, const float* sx, float sw, int64_t m,
+                     int64_t n, double* y) {
+  for (int64_t mm = 0; mm < m; ++mm)
+    for (int64_t nn = 0; nn < n; ++nn)
+      y[mm * n + nn] = (double)acc[mm * n + nn] * (double)sx[mm] * (double)sw;
+}
+
+/* ------------------------------------------------------------------------ */
+/* (vi) Sparse-AbsMean ternarizer, Eq. 4 and Eq. 5 (per-tensor alpha)       */
+/* Ties for the smallest |W| go to the lowest position; a kept weight equal */
+/* to zero gets +1 so that every block keeps exactly one zero.              */
+/* ------------------------------------------------------------------------ */
+
+double oracle_ternarize(const float* w, int64_t n, int64_t k, int8_t* t) {
+  double kept_abs = 0.0;
+  int64_t kept = 0;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t b = 0; b < k / 4; ++b) {
+      const float* wb = w + row * k + 4 * b;
+      int amin = 0;
+      for (int p = 1; p < 4; ++p)
+        if (fabs((double)wb[p]) < fabs((double)wb[amin])) amin = p;
+      for (int p = 0; p < 4; ++p) {
+        int8_t v;
+        if (p == amin) {
+          v = 0;
+        } else {
+          v = (wb[p] < 0.0f) ? -1 : 1;
+          kept_abs += fabs((double)wb[p]);
+          ++kept;
+        }
+        t[row * k + 4 * b + p] = v;
+      }
+    }
+  }
+  return kept ? kept_abs / (double)kept : 0.0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* (vii) 2-bit layout: value w+1 in {0,1,2}, bit by bit                     */
+/* Rows padded to ceil(N/64)*64, reduction dim to ceil(K/512)*512 (padding   */
+/* value 1, i.e. weight 0).  Unit (r, s) of 64 rows x 512 weights is 8192    */
+/* bytes at (r*S + s)*8192; inside it, plane p (0..7) holds for row i the    */
+/* 16 bytes at 1024*p + 16*i, a 128-bit little-endian word whose bits        */
+/* [2u, 2u+2) carry weight 512*s + 64*p + u.                                 */
+/* ------------------------------------------------------------------------ */
+
+int64_t oracle_packed2_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1 || k % 4 != 0) return 0;
+  return ceil_to(n, 64) * ceil_to(k, 512) / 4;
+}
+
+int64_t oracle_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
+  int64_t bytes = oracle_packed2_bytes(n, k);
+  if (bytes == 0) return -((int64_t)1 << 62);
+  int64_t S = ceil_to(k, 512) / 512;
+  int64_t np = ceil_to(n, 64), kp = ceil_to(k, 512);
+  memset(out, 0, (size_t)bytes);
+  for (int64_t row = 0; row < np; ++row) {
+    for (int64_t kk = 0; kk < kp; ++kk) {
+      int v = 1; /* weight 0 */
+      if (row < n && kk < k) {
+        int8_t w = t[row * k + kk];
+        if (w < -1 || w > 1) return -(row * k + kk + 1);
+        v = w + 1;
+      }
+      int64_t r = row / 64, s = kk / 512;
+      int i = (int)(row % 64);
+      int p = (int)((kk % 512) / 64);
+      int u = (int)(kk % 64);
+      for (int q = 0; q < 2; ++q) {
+        int sb = 2 * u + q;
+        int64_t byte = (r * S + s) * 8192 + 1024 * p + 16 * i + sb / 8;
+        if ((v >> q) & 1) out[byte] |= (uint8_t)(1u << (sb % 8));
+      }
+    }
+  }
+  return 0;
+}
+
+int oracle_unpack2(const uint8_t* pk, int64_t n, int64_t k, int8_t* t) {
+  if (oracle_packed2_bytes(n, k) == 0) return -1;
+  int64_t S = ceil_to(k, 512) / 512;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t kk = 0; kk < k; ++kk) {
+      int64_t r = row / 64, s = kk / 512;
+      int i = (int)(row % 64);
+      int p = (int)((kk % 512) / 64);
+      int u = (int)(kk % 64);
+      int v = 0;
+      for (int q = 0; q < 2; ++q) {
+        int sb = 2 * u + q;
+        int64_t byte = (r * S + s) * 8192 + 1024 * p + 16 * i + sb / 8;
+        v |= ((pk[byte] >> (sb % 8)) & 1) << q;
+      }
+      if (v > 2) return -2;
+      t[row * k + kk] = (int8_t)(v - 1);
+    }
+  }
+  return 0;
+}

@@ -1,0 +1,308 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+None of these re-types the oracle's own formula: each compares it with a
+hand-derived fixture, a count or identity the paper states, a library routine
+(numpy), or brute force on tiny inputs.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+SYM = {"+": 1, "-": -1, "0": 0}
+
+
+def _golden_table():
+    rows = {}
+    with open(os.path.join(GOLDEN, "code_table.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if not line:
+                continue
+            c, w = line.split()
+            rows[int(c)] = [SYM[ch] for ch in w]
+    return rows
+
+
+# ---------------------------------------------------------------- code table
+
+def test_code_table_matches_hand_derived_table():
+    g = _golden_table()
+    assert sorted(g) == list(range(32))
+    t = oracle.code_table()
+    for c in range(32):
+        assert list(t[c]) == g[c], c
+
+
+def test_exactly_32_of_81_ternary_tuples_are_codes():
+    # Sec. 3.1 point 3: C(4,3) * 2^3 = 32 states saturate 5 bits
+    accepted = 0
+    codes = set()
+    for w in itertools.product((-1, 0, 1), repeat=4):
+        c = oracle.encode_block(w)
+        if c >= 0:
+            accepted += 1
+            codes.add(c)
+            assert list(oracle.decode_code(c)) == list(w)
+            assert sum(1 for v in w if v == 0) == 1
+        else:
+            assert sum(1 for v in w if v == 0) != 1
+    assert accepted == 32
+    assert codes == set(range(32))
+
+
+def test_mirror_pairs():
+    # Appendix C: with one shared sign bit, 3:4 has 16 patterns -> code and
+    # its mirror differ only in the sign bits and negate each other.
+    pairs = set()
+    for c in range(32):
+        m = c ^ 0b11100
+        assert list(oracle.decode_code(m)) == list(-oracle.decode_code(c))
+        pairs.add(frozenset((c, m)))
+    assert len(pairs) == 16
+
+
+def test_low_two_bits_are_zero_position():
+    for c in range(32):
+        w = oracle.decode_code(c)
+        assert w[c & 3] == 0
+
+
+# ------------------------------------------------------------ packed layout
+
+def _fixture_t(fx):
+    n, k = fx["n"], fx["k"]
+    t = np.tile(np.array([0, 1, 1, 1], np.int8), (n, k // 4))
+    g = _golden_table()
+    for row, blk, code in fx["blocks"]:
+        t[row, 4 * blk:4 * blk + 4] = g[code]
+    return t
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2])
+def test_pack_hand_derived_bytes(idx):
+    with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
+        fx = json.load(f)["five_bit"][idx]
+    t = _fixture_t(fx)
+    p = oracle.pack(t)
+    assert p.size == fx["total_bytes"] == oracle.packed_bytes(fx["n"], fx["k"])
+    nz = {int(i): int(p[i]) for i in np.nonzero(p)[0]}
+    assert nz == {int(a): b for a, b in fx["nonzero"].items()}
+    assert np.array_equal(oracle.unpack(p, fx["n"], fx["k"]), t)
+
+
+@pytest.mark.parametrize("idx", [0, 1])
+def test_pack2_hand_derived_bytes(idx):
+    with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
+        fx = json.load(f)["two_bit"][idx]
+    t = np.zeros((fx["n"], fx["k"]), np.int8)
+    for row, kk, w in fx["weights"]:
+        t[row, kk] = w
+    p = oracle.pack2(t)
+    assert p.size == fx["total_bytes"]
+    exp = np.full(fx["total_bytes"], fx["fill"], np.uint8)
+    for a, b in fx["bytes"].items():
+        exp[int(a)] = b
+    assert np.array_equal(p, exp)
+    assert np.array_equal(oracle.unpack2(p, fx["n"], fx["k"]), t)
+
+
+def test_packed_sizes_are_1p25_bits():
+    # 5 bits per 4 weights (Sec. 3.1); exact for multiples of 64 x 512
+    for n, k in [(2048, 2048), (512, 2048), (8192, 2048), (2048, 8192),
+                 (3072, 3072), (1024, 3072), (14336, 4096)]:
+        assert oracle.packed_bytes(n, k) * 32 == 5 * n * k
+        assert oracle.packed2_bytes(n, k) * 4 == n * k
+    assert oracle.packed_bytes(0, 4) == 0
+    assert oracle.packed_bytes(4, 6) == 0
+
+
+@pytest.mark.parametrize("k", [4, 8, 12, 124, 128, 132, 516, 2048])
+@pytest.mark.parametrize("n", [1, 63, 65])
+def test_pack_round_trip(n, k):
+    t = synth.ternary_34(n, k, 1, "rt")
+    p = oracle.pack(t)
+    assert np.array_equal(oracle.unpack(p, n, k), t)
+    # 3:4 invariant of Eq. 3: every row keeps exactly 3K/4 non-zeros
+    assert np.all(np.abs(oracle.unpack(p, n, k)).sum(axis=1) == 3 * k // 4)
+    t2 = synth.ternary_any(n, k, 1, "rt2")
+    assert np.array_equal(oracle.unpack2(oracle.pack2(t2), n, k), t2)
+
+
+@pytest.mark.parametrize("zeros", [0, 2, 3, 4])
+def test_pack_rejects_non_34_blocks(zeros):
+    t = synth.ternary_34(3, 64, 2, "bad")
+    blk = np.array([0] * zeros + [1] * (4 - zeros), np.int8)
+    t[2, 20:24] = blk
+    assert oracle.pack_bad_block(t) == 2 * 16 + 5
+    t[1, 4:8] = blk
+    assert oracle.pack_bad_block(t) == 1 * 16 + 1
+
+
+def test_pack_rejects_out_of_set_values():
+    t = synth.ternary_34(1, 8, 3, "oos")
+    t[0, 5] = 2 if t[0, 5] != 0 else t[0, 5]
+    t[0, 4:8] = [0, 2, 1, 1]
+    assert oracle.pack_bad_block(t) == 1
+
+
+# ---------------------------------------------------------------- product
+
+def _brute(x, t):
+    m, k = x.shape
+    n = t.shape[0]
+    out = [[0] * n for _ in range(m)]
+    for i in range(m):
+        for j in range(n):
+            s = 0
+            for kk in range(k):
+                s += int(x[i, kk]) * int(t[j, kk])
+            out[i][j] = s
+    return np.array(out, dtype=np.int64)
+
+
+@pytest.mark.parametrize("m,n,k", [(1, 1, 4), (2, 3, 8), (3, 5, 12)])
+def test_gemm_brute_force_tiny(m, n, k):
+    x = synth.int8_any(m, k, 4, "bf")
+    t = synth.ternary_34(n, k, 4, "bf")
+    assert np.array_equal(oracle.gemm_i32(x, t).astype(np.int64), _brute(x, t))
+
+
+def test_gemm_all_code_pairs():
+    # K=8 and 1024 rows: every ordered pair of the 32 codes appears once
+    g = oracle.code_table()
+    t = np.concatenate([np.concatenate([g[a], g[b]])[None]
+                        for a in range(32) for b in range(32)]).astype(np.int8)
+    x = synth.int8_any(3, 8, 5, "pairs")
+    assert np.array_equal(oracle.gemm_i32(x, t).astype(np.int64), _brute(x, t))
+
+
+@pytest.mark.parametrize("m,n,k", [(1, 257, 2048), (7, 130, 516), (16, 64, 1028)])
+def test_gemm_matches_numpy(m, n, k):
+    x = synth.int8_any(m, k, 6, "np")
+    t = synth.ternary_34(n, k, 6, "np")
+    ref = x.astype(np.int64) @ t.astype(np.int64).T
+    assert np.array_equal(oracle.gemm_i32(x, t), ref)
+    assert np.array_equal(oracle.gemm_i32(x, t, threads=4), ref)
+    for i, j in [(0, 0), (m - 1, n - 1), (m // 2, n // 3)]:
+        assert oracle.dot_i32(x[i], t[j]) == ref[i, j]
+
+
+def test_gemm_closed_forms():
+    n, k = 40, 64
+    t = synth.ternary_34(n, k, 7, "cf")
+    # one-hot activation reads back one column of T
+    for kk in (0, 13, 63):
+        e = np.zeros((1, k), np.int8)
+        e[0, kk] = 1
+        assert np.array_equal(oracle.gemm_i32(e, t)[0], t[:, kk].astype(np.int32))
+    # all-ones activation gives the row sums
+    ones = np.ones((1, k), np.int8)
+    assert np.array_equal(oracle.gemm_i32(ones, t)[0], t.astype(np.int32).sum(1))
+    # extreme magnitudes: |acc| <= 128 * 3K/4
+    xm = np.full((1, k), -128, np.int8)
+    assert np.all(np.abs(oracle.gemm_i32(xm, t)) <= 128 * 3 * k // 4)
+
+
+# ------------------------------------------------------ activation quant
+
+def test_quantize_hand_derived():
+    x = np.array([
+        [127.0, -63.5, 0.5, 1.5, 2.5, -127.0, 0.0, 3.49],
+        [254.0, 1.0, 3.0, -254.0, 5.0, -1.0, 0.0, 0.0],
+        [0.0] * 8,
+    ], np.float32)
+    q, sx = oracle.quantize_act(x)
+    # row 0: absmax 127 -> sx 1; ties go to even (-63.5 -> -64, 0.5 -> 0,
+    # 1.5 -> 2, 2.5 -> 2)
+    assert sx[0] == 1.0
+    assert list(q[0]) == [127, -64, 0, 2, 2, -127, 0, 3]
+    # row 1: absmax 254 -> sx 2; 1/2 -> 0, 3/2 -> 2, 5/2 -> 2, -1/2 -> -0
+    assert sx[1] == 2.0
+    assert list(q[1]) == [127, 0, 2, -127, 2, 0, 0, 0]
+    # all-zero row: scale 0, codes 0
+    assert sx[2] == 0.0 and not q[2].any()
+
+
+def test_quantize_properties():
+    x = synth.activations(9, 1000, 8, "qp", outlier_frac=0.01)
+    q, sx = oracle.quantize_act(x)
+    assert q.dtype == np.int8 and np.all(np.abs(q.astype(int)) <= 127)
+    for r in range(9):
+        amax = np.max(np.abs(x[r]))
+        assert sx[r] == np.float32(amax) / np.float32(127.0)
+        i = int(np.argmax(np.abs(x[r])))
+        assert abs(int(q[r, i])) == 127
+        # dequantization error is at most half a step (plus fp32 slack)
+        err = np.abs(q[r].astype(np.float64) * sx[r] - x[r])
+        assert np.all(err <= 0.5 * sx[r] * (1 + 1e-6))
+    # exact multiples j * sx map back to j
+    s = np.float32(0.25)
+    j = np.arange(-127, 128, dtype=np.float32)
+    q2, sx2 = oracle.quantize_act((j * s)[None, :])
+    assert sx2[0] == s and np.array_equal(q2[0].astype(np.float32), j)
+
+
+# ---------------------------------------------------------------- epilogue
+
+def test_epilogue_exact_products():
+    acc = np.array([[0, 1, -3, 1 << 20], [7, -7, 5, -(1 << 22)]], np.int32)
+    sx = np.array([0.5, 0.125], np.float32)
+    y = oracle.epilogue(acc, sx, 0.25)
+    assert np.array_equal(y, acc * np.array([[0.125], [0.03125]]))
+
+
+def test_linear_path_matches_float_reference():
+    x = synth.activations(3, 256, 9, "lin")
+    t = synth.ternary_34(50, 256, 9, "lin")
+    sw = synth.weight_scale(9, "lin")
+    q, sx, acc, y = oracle.linear(x, t, sw)
+    ref = (q.astype(np.float64) @ t.astype(np.float64).T) * sx[:, None].astype(np.float64) * sw
+    assert np.allclose(y, ref, rtol=1e-12, atol=0)
+    # and the quantized product approximates the fp32 product X T^T sw
+    full = x.astype(np.float64) @ t.astype(np.float64).T * sw
+    assert np.max(np.abs(y - full)) < 0.05 * np.max(np.abs(full))
+
+
+# --------------------------------------------------------------- ternarizer
+
+def test_ternarizer_is_optimal_per_block():
+    # Appendix D: for any alpha > 0 the best 3:4 block maximises sum W*T,
+    # i.e. drop the smallest |W| and keep signs.  Check by brute force over
+    # all 32 patterns.
+    w = synth.dense_weights(6, 64, 10, "tern")
+    t, alpha = oracle.ternarize(w)
+    g = oracle.code_table().astype(np.float64)
+    for row in range(6):
+        for b in range(16):
+            wb = w[row, 4 * b:4 * b + 4].astype(np.float64)
+            best = np.max(g @ wb)
+            assert np.isclose(float(t[row, 4 * b:4 * b + 4].astype(np.float64) @ wb), best)
+            for a in (alpha, 0.3, 2.0):
+                errs = ((wb[None, :] - a * g) ** 2).sum(1)
+                tb = t[row, 4 * b:4 * b + 4].astype(np.float64)
+                assert ((wb - a * tb) ** 2).sum() <= errs.min() + 1e-12
+    # every block keeps exactly one zero
+    assert np.all((t.reshape(6, 16, 4) == 0).sum(-1) == 1)
+
+
+def test_ternarizer_alpha_is_least_squares():
+    # Eq. 5: alpha* = mean |W| over kept weights = <W,T>/<T,T>
+    w = synth.dense_weights(8, 128, 11, "alpha")
+    t, alpha = oracle.ternarize(w)
+    tt = t.astype(np.float64).ravel()
+    sol = np.linalg.lstsq(tt[:, None], w.astype(np.float64).ravel(), rcond=None)[0][0]
+    assert np.isclose(alpha, sol, rtol=1e-12)
+
+
+def test_ternarizer_ties_and_zeros():
+    w = np.array([[0.5, -0.5, 0.5, -0.5, 0.0, 0.0, 1.0, -2.0]], np.float32)
+    t, _ = oracle.ternarize(w)
+    # ties for the smallest |W| go to the lowest position; a kept zero is +1
+    assert list(t[0]) == [0, -1, 1, -1, 0, 1, 1, -1]
