@@ -108,36 +108,35 @@ void oracle_decode_code(int c, int8_t w[4]) {
 /* (ii) the 5-bit tiled layout, bit by bit                                  */
 /*                                                                          */
 /* Rows are padded to Np = ceil(N/64)*64 and the reduction dimension to      */
-/* Kp = ceil(K/512)*512; padding codes are all-zero bits.  The matrix is a   */
-/* grid of units of 64 rows x 512 weights (5120 bytes), unit (r, s) at byte  */
-/* (r*S + s)*5120 with S = Kp/512.  Inside a unit, row i (0..63) holds four  */
-/* containers h (0..3) of 32 consecutive codes, covering weights            */
-/* 512*s + 128*h .. +127.  A container is a 160-bit little-endian stream,    */
-/* code j at stream bits [5j, 5j+5) (code bit q at stream bit 5j+q).  Stream */
-/* bits 0..127 go to the head bytes at 1024*h + 16*i + (0..15); stream bits  */
-/* 128..159 to the tail bytes at 4096 + 16*i + 4*h + (0..3).  Inside a byte, */
-/* stream bit 8*p + t is bit t (LSB first).                                  */
+/* Kp = ceil(K/128)*128; padding codes are all-zero bits.  The matrix is a   */
+/* grid of units of 64 rows x 128 weights (1280 bytes), unit (r, c) at byte  */
+/* (r*C + c)*1280 with C = Kp/128.  Inside a unit, row i (0..63) holds one   */
+/* container of 32 consecutive codes for weights 128*c .. 128*c+127: a       */
+/* 160-bit little-endian stream, code j at stream bits [5j, 5j+5) (code bit  */
+/* q at stream bit 5j+q).  Stream bits 0..127 go to the head bytes at        */
+/* 16*i + (0..15); stream bits 128..159 to the tail bytes at 1024 + 4*i +    */
+/* (0..3).  Inside a byte, stream bit 8*p + t is bit t (LSB first).          */
 /* ------------------------------------------------------------------------ */
 
 static int64_t ceil_to(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
 int64_t oracle_packed_bytes(int64_t n, int64_t k) {
   if (n < 1 || k < 1 || k % 4 != 0) return 0;
-  return ceil_to(n, 64) * ceil_to(k, 512) * 5 / 32;
+  return ceil_to(n, 64) * ceil_to(k, 128) * 5 / 32;
 }
 
-/* Byte offset and bit inside it for stream bit sp of container h, row n,
- * block-column s (unit column), in a matrix with S unit columns. */
-static void stream_bit_addr(int64_t n, int64_t s, int h, int sp, int64_t S,
+/* Byte offset and bit inside it for stream bit sp of the container of row n
+ * and container column c, in a matrix with C container columns. */
+static void stream_bit_addr(int64_t n, int64_t c, int sp, int64_t C,
                             int64_t* byte, int* bit) {
   int64_t r = n / 64;
   int i = (int)(n % 64);
-  int64_t unit = (r * S + s) * 5120;
+  int64_t unit = (r * C + c) * 1280;
   if (sp < 128) {
-    *byte = unit + 1024 * h + 16 * i + sp / 8;
+    *byte = unit + 16 * i + sp / 8;
     *bit = sp % 8;
   } else {
-    *byte = unit + 4096 + 16 * i + 4 * h + (sp - 128) / 8;
+    *byte = unit + 1024 + 4 * i + (sp - 128) / 8;
     *bit = (sp - 128) % 8;
   }
 }
@@ -149,20 +148,19 @@ int64_t oracle_pack(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
   int64_t bytes = oracle_packed_bytes(n, k);
   if (bytes == 0) return -((int64_t)1 << 62);
   memset(out, 0, (size_t)bytes);
-  int64_t S = ceil_to(k, 512) / 512;
+  int64_t C = ceil_to(k, 128) / 128;
   int64_t nb = k / 4;
   for (int64_t row = 0; row < n; ++row) {
     for (int64_t b = 0; b < nb; ++b) {
       int code = oracle_encode_block(t + row * k + 4 * b);
       if (code < 0) return -(row * nb + b + 1);
-      int64_t kk = 4 * b;             /* first weight of the block      */
-      int64_t s = kk / 512;           /* unit column                    */
-      int h = (int)((kk % 512) / 128);/* container inside the unit      */
-      int j = (int)((kk % 128) / 4);  /* code inside the container      */
+      int64_t kk = 4 * b;            /* first weight of the block      */
+      int64_t c = kk / 128;          /* container column               */
+      int j = (int)((kk % 128) / 4); /* code inside the container      */
       for (int q = 0; q < 5; ++q) {
         int64_t byte;
         int bit;
-        stream_bit_addr(row, s, h, 5 * j + q, S, &byte, &bit);
+        stream_bit_addr(row, c, 5 * j + q, C, &byte, &bit);
         if ((code >> q) & 1) out[byte] |= (uint8_t)(1u << bit);
       }
     }
@@ -173,18 +171,17 @@ int64_t oracle_pack(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
 /* Inverse of oracle_pack for the first n rows and k weights. */
 int oracle_unpack(const uint8_t* p, int64_t n, int64_t k, int8_t* t) {
   if (oracle_packed_bytes(n, k) == 0) return -1;
-  int64_t S = ceil_to(k, 512) / 512;
+  int64_t C = ceil_to(k, 128) / 128;
   for (int64_t row = 0; row < n; ++row) {
     for (int64_t b = 0; b < k / 4; ++b) {
       int64_t kk = 4 * b;
-      int64_t s = kk / 512;
-      int h = (int)((kk % 512) / 128);
+      int64_t c = kk / 128;
       int j = (int)((kk % 128) / 4);
       int code = 0;
       for (int q = 0; q < 5; ++q) {
         int64_t byte;
         int bit;
-        stream_bit_addr(row, s, h, 5 * j + q, S, &byte, &bit);
+        stream_bit_addr(row, c, 5 * j + q, C, &byte, &bit);
         code |= ((p[byte] >> bit) & 1) << q;
       }
       oracle_decode_code(code, t + row * k + kk);
@@ -321,23 +318,31 @@ double oracle_ternarize(const float* w, int64_t n, int64_t k, int8_t* t) {
 
 /* ------------------------------------------------------------------------ */
 /* (vii) 2-bit layout: value w+1 in {0,1,2}, bit by bit                     */
-/* Rows padded to ceil(N/64)*64, reduction dim to ceil(K/512)*512 (padding   */
-/* value 1, i.e. weight 0).  Unit (r, s) of 64 rows x 512 weights is 8192    */
-/* bytes at (r*S + s)*8192; inside it, plane p (0..7) holds for row i the    */
-/* 16 bytes at 1024*p + 16*i, a 128-bit little-endian word whose bits        */
-/* [2u, 2u+2) carry weight 512*s + 64*p + u.                                 */
+/* Rows padded to ceil(N/64)*64, reduction dim to ceil(K/64)*64 (padding     */
+/* value 1, i.e. weight 0).  Unit (r, c) of 64 rows x 64 weights is 1024     */
+/* bytes at (r*C + c)*1024 with C = Kp/64; row i holds the 16 bytes at       */
+/* 16*i, a 128-bit little-endian word whose bits [2u, 2u+2) carry weight     */
+/* 64*c + u.                                                                 */
 /* ------------------------------------------------------------------------ */
 
 int64_t oracle_packed2_bytes(int64_t n, int64_t k) {
   if (n < 1 || k < 1 || k % 4 != 0) return 0;
-  return ceil_to(n, 64) * ceil_to(k, 512) / 4;
+  return ceil_to(n, 64) * ceil_to(k, 64) / 4;
+}
+
+static int64_t two_bit_byte(int64_t row, int64_t kk, int q, int64_t C, int* bit) {
+  int64_t r = row / 64, c = kk / 64;
+  int i = (int)(row % 64);
+  int sb = 2 * (int)(kk % 64) + q;
+  *bit = sb % 8;
+  return (r * C + c) * 1024 + 16 * i + sb / 8;
 }
 
 int64_t oracle_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
   int64_t bytes = oracle_packed2_bytes(n, k);
   if (bytes == 0) return -((int64_t)1 << 62);
-  int64_t S = ceil_to(k, 512) / 512;
-  int64_t np = ceil_to(n, 64), kp = ceil_to(k, 512);
+  int64_t C = ceil_to(k, 64) / 64;
+  int64_t np = ceil_to(n, 64), kp = ceil_to(k, 64);
   memset(out, 0, (size_t)bytes);
   for (int64_t row = 0; row < np; ++row) {
     for (int64_t kk = 0; kk < kp; ++kk) {
@@ -347,14 +352,10 @@ int64_t oracle_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
         if (w < -1 || w > 1) return -(row * k + kk + 1);
         v = w + 1;
       }
-      int64_t r = row / 64, s = kk / 512;
-      int i = (int)(row % 64);
-      int p = (int)((kk % 512) / 64);
-      int u = (int)(kk % 64);
       for (int q = 0; q < 2; ++q) {
-        int sb = 2 * u + q;
-        int64_t byte = (r * S + s) * 8192 + 1024 * p + 16 * i + sb / 8;
-        if ((v >> q) & 1) out[byte] |= (uint8_t)(1u << (sb % 8));
+        int bit;
+        int64_t byte = two_bit_byte(row, kk, q, C, &bit);
+        if ((v >> q) & 1) out[byte] |= (uint8_t)(1u << bit);
       }
     }
   }
@@ -363,18 +364,14 @@ int64_t oracle_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
 
 int oracle_unpack2(const uint8_t* pk, int64_t n, int64_t k, int8_t* t) {
   if (oracle_packed2_bytes(n, k) == 0) return -1;
-  int64_t S = ceil_to(k, 512) / 512;
+  int64_t C = ceil_to(k, 64) / 64;
   for (int64_t row = 0; row < n; ++row) {
     for (int64_t kk = 0; kk < k; ++kk) {
-      int64_t r = row / 64, s = kk / 512;
-      int i = (int)(row % 64);
-      int p = (int)((kk % 512) / 64);
-      int u = (int)(kk % 64);
       int v = 0;
       for (int q = 0; q < 2; ++q) {
-        int sb = 2 * u + q;
-        int64_t byte = (r * S + s) * 8192 + 1024 * p + 16 * i + sb / 8;
-        v |= ((pk[byte] >> (sb % 8)) & 1) << q;
+        int bit;
+        int64_t byte = two_bit_byte(row, kk, q, C, &bit);
+        v |= ((pk[byte] >> bit) & 1) << q;
       }
       if (v > 2) return -2;
       t[row * k + kk] = (int8_t)(v - 1);
