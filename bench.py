@@ -1,0 +1,314 @@
+#!/usr/bin/env python3
+"""Benchmark of the Sherry 1.25-bit ternary hot path on one MI355X.
+
+Workload (the metric's headline configuration): one decode step (M = 1) of the
+linear layers of LLaMA-3.2-1B -- 16 layers x {q 2048x2048, k/v 512x2048,
+o 2048x2048, gate/up 8192x2048, down 2048x8192} -- as 3:4 ternary weights
+packed at 1.25 bits, per-tensor scales U(0.01, 0.05), a fresh fp32 N(0,1)
+activation vector per projection.  A step is the whole hot path on device:
+per-token int8 quantization of the 112 activation vectors (2 launches) and
+the 112 products in one grouped launch.  Weights and activations are rotated
+over 4 copies (about 615 MB, above the 256 MB Infinity Cache).
+
+Prints one JSON line.  `value` = algorithmic bytes of a step / step time
+(GB/s); `roofline` is the grouped product kernel alone (HIP events around each
+launch inside the timed region); `cpu_baseline` is the CPU oracle on the host
+cores over one full step.  With --extra (default on) the M = 2048 prefill GEMM
+on the LLaMA-3.2-3B and -1B shapes is timed too (dense-equivalent TOPS).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+INT8_PEAK_TOPS = 5000.0
+COPIES = 4
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash(files) -> str:
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2601_07892_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------
+# decode step (M = 1)
+# ---------------------------------------------------------------------------
+
+class DecodeStep:
+    """Device buffers of COPIES rotated copies of one decode step."""
+
+    def __init__(self, sh, torch, dev, spec, seed, copies=COPIES):
+        self.sh, self.torch, self.dev = sh, torch, dev
+        self.lins = synth.model_linears(spec)
+        self.count = len(self.lins)
+        t0 = time.time()
+        self.t = []        # host ternary matrices (for the CPU baseline)
+        self.packed = []   # device packed weights, [copy][i]
+        self.scales = []
+        host_packed = []
+        for i, (layer, lin) in enumerate(self.lins):
+            t = synth.ternary_34(lin.n, lin.k, seed, "w", layer, lin.name)
+            self.t.append(t)
+            host_packed.append(sh.sherry_pack(t))
+            self.scales.append(synth.weight_scale(seed, "s", layer, lin.name))
+        log("generated+packed %d weights in %.1fs" % (sum(l.n * l.k for _, l in self.lins),
+                                                       time.time() - t0))
+        self.ks = sorted({lin.k for _, lin in self.lins})
+        self.x_host = {kk: synth.activations(sum(1 for _, l in self.lins if l.k == kk), kk, seed,
+                                             "x", kk) for kk in self.ks}
+        self.copies = []
+        for c in range(copies):
+            w = [torch.from_numpy(p).to(dev) for p in host_packed]
+            xs = {kk: torch.from_numpy(self.x_host[kk]).to(dev) for kk in self.ks}
+            qs = {kk: torch.empty(xs[kk].shape, dtype=torch.int8, device=dev) for kk in self.ks}
+            sxs = {kk: torch.empty(xs[kk].shape[0], dtype=torch.float32, device=dev)
+                   for kk in self.ks}
+            ys = [torch.empty(lin.n, dtype=torch.float32, device=dev) for _, lin in self.lins]
+            descs = (sh.sherry_gemv_desc * self.count)()
+            row = {kk: 0 for kk in self.ks}
+            for i, (_, lin) in enumerate(self.lins):
+                r = row[lin.k]
+                row[lin.k] += 1
+                d = descs[i]
+                d.w = w[i].data_ptr()
+                d.x = qs[lin.k][r].data_ptr()
+                d.x_scale = sxs[lin.k][r:r + 1].data_ptr()
+                d.y = ys[i].data_ptr()
+                d.acc = None
+                d.n, d.k, d.w_scale = lin.n, lin.k, self.scales[i]
+            total = sh.sherry_gemv_batched_prepare(descs)
+            ddev = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+            self.copies.append(dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total))
+        torch.cuda.synchronize()
+        self.total_tiles = self.copies[0]["total"]
+        self.weight_bytes = sum(sh.sherry_packed_bytes(l.n, l.k) for _, l in self.lins)
+        # algorithmic bytes of one grouped product launch: packed weights,
+        # int8 x, its fp32 scale, fp32 y
+        self.gemv_bytes = sum(sh.sherry_packed_bytes(l.n, l.k) + l.k + 4 + 4 * l.n
+                              for _, l in self.lins)
+        # quantization: fp32 x read, int8 q written, fp32 scale written
+        self.quant_bytes = sum(5 * l.k + 4 for _, l in self.lins)
+        self.ops = sum(2 * l.n * l.k for _, l in self.lins)
+        log("working set: %.1f MB of packed weights per copy x %d copies" %
+            (self.weight_bytes / 1e6, copies))
+
+    def quantize(self, c):
+        cp = self.copies[c]
+        for kk in self.ks:
+            self.sh.sherry_quantize_act(cp["xs"][kk], cp["qs"][kk], cp["sxs"][kk])
+
+    def gemv(self, c):
+        cp = self.copies[c]
+        self.sh.sherry_gemv_batched(cp["descs"], self.count, cp["total"])
+
+
+def bench_decode(step: DecodeStep, torch, steps, warmup):
+    for i in range(warmup):
+        step.quantize(i % COPIES)
+        step.gemv(i % COPIES)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(steps):
+        c = i % COPIES
+        step.quantize(c)
+        ev[i][0].record()
+        step.gemv(c)
+        ev[i][1].record()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = start.elapsed_time(stop)
+    gemv_ms = [a.elapsed_time(b) for a, b in ev]
+    return total_ms / steps, float(np.mean(gemv_ms)), float(np.median(gemv_ms)), wall
+
+
+def bench_stream_ceiling(sh, torch, dev, nbytes=2 << 30, reps=20):
+    """Practical HBM read ceiling: 128-bit streaming read of 2 GiB."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    sink = torch.empty(sh.sherry_stream_read_groups(nbytes), dtype=torch.int32, device=dev)
+    for _ in range(3):
+        sh.sherry_stream_read(src, nbytes, sink)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        sh.sherry_stream_read(src, nbytes, sink)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src
+    return nbytes / (ms * 1e-3) / 1e9
+
+
+# ---------------------------------------------------------------------------
+# prefill GEMM (M = 2048)
+# ---------------------------------------------------------------------------
+
+def bench_prefill(sh, torch, dev, spec, m, seed, reps=10):
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    rows = []
+    tot_ops, tot_ms = 0.0, 0.0
+    for lin in blk:
+        t = synth.ternary_34(lin.n, lin.k, seed, "pw", lin.name, lin.k)
+        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        x = torch.from_numpy(synth.activations(m, lin.k, seed, "px", lin.name,
+                                               outlier_frac=0.01)).to(dev)
+        q = torch.empty((m, lin.k), dtype=torch.int8, device=dev)
+        sx = torch.empty(m, dtype=torch.float32, device=dev)
+        y = torch.empty((m, lin.n), dtype=torch.float32, device=dev)
+        sh.sherry_quantize_act(x, q, sx)
+        sw = synth.weight_scale(seed, "ps", lin.name)
+        for _ in range(2):
+            sh.sherry_gemm(w, q, sx, sw, y, None, m, lin.n, lin.k)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            sh.sherry_gemm(w, q, sx, sw, y, None, m, lin.n, lin.k)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        ops = 2.0 * m * lin.n * lin.k
+        tot_ops += ops
+        tot_ms += ms
+        rows.append({"proj": lin.name, "n": lin.n, "k": lin.k, "us": round(ms * 1e3, 2),
+                     "tops": round(ops / (ms * 1e-3) / 1e12, 1)})
+        del w, x, q, y
+    return {"m": m, "per_layer_us": round(tot_ms * 1e3, 2),
+            "tops": round(tot_ops / (tot_ms * 1e-3) / 1e12, 1),
+            "mfma_frac": round(tot_ops / (tot_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+            "shapes": rows}
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on the host cores
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(step: DecodeStep, min_seconds=10.0):
+    import oracle
+    threads = min(16, os.cpu_count() or 1)
+    xk = {kk: oracle.quantize_act(step.x_host[kk]) for kk in step.ks}
+    reps, t_total = 0, 0.0
+    while t_total < min_seconds and reps < 50:
+        t0 = time.perf_counter()
+        row = {kk: 0 for kk in step.ks}
+        for i, (_, lin) in enumerate(step.lins):
+            q, sx = oracle.quantize_act(step.x_host[lin.k][row[lin.k]:row[lin.k] + 1])
+            row[lin.k] += 1
+            acc = oracle.gemm_i32(q, step.t[i], threads=threads)
+            oracle.epilogue(acc, sx, step.scales[i])
+        t_total += time.perf_counter() - t0
+        reps += 1
+    del xk
+    per_step = t_total / reps
+    return {"value": round((step.gemv_bytes + step.quant_bytes) / per_step / 1e9, 3),
+            "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": "%d full decode step(s) of the same workload (112 products of the "
+                      "16-layer LLaMA-3.2-1B linears, quantize + int32 product + fp64 "
+                      "epilogue); algorithmic bytes as the GPU line, the oracle reads "
+                      "T unpacked at 1 byte/weight; %.2f s per step" % (reps, per_step)}
+
+
+def load_traffic(src_hash: str):
+    path = os.path.join(ROOT, "profiles", "traffic_gemv_batched.json")
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_source_hash") != src_hash:
+        return None
+    return d.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--seed", type=int, default=synth.DEFAULT_SEED)
+    ap.add_argument("--no-extra", action="store_true", help="skip the M=2048 GEMM and ceiling")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the product would shard); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2601_07892_amd as sh
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(sh.sherry_version(), torch.cuda.get_device_name(dev))
+
+    step = DecodeStep(sh, torch, dev, synth.LLAMA_1B, args.seed)
+    ms_step, gemv_ms_mean, gemv_ms_med, wall = bench_decode(step, torch, args.steps, args.warmup)
+    step_bytes = step.gemv_bytes + step.quant_bytes
+    value = step_bytes / (ms_step * 1e-3) / 1e9
+    achieved = step.gemv_bytes / (gemv_ms_mean * 1e-3) / 1e9
+    log("step %.2f us, grouped product %.2f us (median %.2f), %.0f GB/s" %
+        (ms_step * 1e3, gemv_ms_mean * 1e3, gemv_ms_med * 1e3, achieved))
+    src_hash = kernel_source_hash(["gemv.hip", "sherry_internal.h"])
+    out = {
+        "metric": "ternary GEMV GB/s & % HBM peak at M=1; GEMM TOPS at M=2048 (LLaMA-1B shapes)",
+        "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int8xternary->int32",
+        "data": "synthetic",
+        "config": {"workload": "llama-3.2-1b decode step, M=1, 16 layers x 7 projections "
+                               "(112 GEMVs), 1.25-bit 3:4 ternary, %d rotated copies" % COPIES,
+                   "weights_mb_per_copy": round(step.weight_bytes / 1e6, 2),
+                   "step": "2 int8 quantize launches + 1 grouped product launch",
+                   "seed": args.seed},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": load_traffic(src_hash),
+                     "kernel": "gemv_batched_kernel", "bytes_per_launch": step.gemv_bytes,
+                     "avg_launch_us": round(gemv_ms_mean * 1e3, 3),
+                     "kernel_source_hash": src_hash},
+    }
+    if not args.no_extra:
+        try:
+            out["hbm_read_ceiling_gbs"] = round(bench_stream_ceiling(sh, torch, dev), 1)
+        except Exception as e:  # pragma: no cover
+            log("ceiling probe failed:", e)
+        pre = {}
+        for name, spec in (("llama-3.2-3b", synth.LLAMA_3B), ("llama-3.2-1b", synth.LLAMA_1B)):
+            pre[name] = bench_prefill(sh, torch, dev, spec, 2048, args.seed)
+            log("prefill %s M=2048: %.1f TOPS" % (name, pre[name]["tops"]))
+        out["prefill_m2048"] = pre
+    if not args.no_cpu:
+        t0 = time.time()
+        out["cpu_baseline"] = cpu_baseline(step)
+        log("cpu baseline %.1f s" % (time.time() - t0))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

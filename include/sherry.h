@@ -1,0 +1,216 @@
+/*
+ * sherry.h -- C ABI of the MI355X (gfx950) library for the Sherry 3:4 sparse
+ * ternary product (arXiv 2601.07892).
+ *
+ * The library computes the inference-time product of Eq. 2,
+ *
+ *     Y = X T alpha,
+ *
+ * where T (N x K here: row n is the paper's output channel j, K its d_in)
+ * has values in {-1, 0, +1} and satisfies the 3:4 constraint of Eq. 3: in
+ * every block of 4 consecutive weights along K exactly one is zero.  Each
+ * block is stored as one 5-bit code (Sec. 3.1, point 3: C(4,3)*2^3 = 32
+ * states), 1.25 bits per weight (offline packing phase, Appendix A).  X is
+ * int8 with one fp32 scale per token, alpha a per-tensor fp32 scale, and the
+ * product is accumulated exactly in int32 (online phase, Appendix A):
+ *
+ *     acc[m][n] = sum_k X[m][k] * T[n][k]                 (exact, int32)
+ *     y[m][n]   = float(acc[m][n]) * (x_scale[m] * w_scale)  (fp32, RNE)
+ *
+ * Conventions for every call:
+ *  - Every entry point returns a sherry_status (0 = SHERRY_OK).  Arguments are
+ *    validated on the host before anything is enqueued; on any error nothing
+ *    runs and output buffers are untouched.
+ *  - "host" pointers are ordinary CPU memory; "device" pointers are HIP device
+ *    memory of the current device.  The caller owns and frees every buffer;
+ *    the library allocates nothing and keeps no mutable global state apart
+ *    from a per-thread record of the last HIP error, so calls from several
+ *    threads are safe (calls that write the same buffers race).
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Device calls are asynchronous: they enqueue kernels and return.  Launch
+ *    failures return SHERRY_E_DEVICE; faults surface at the next sync.
+ *  - Sizes are in elements unless named *_bytes.  All matrices are row-major.
+ *
+ * Packed 5-bit tiled layout (what sherry_pack writes and the products read):
+ *  - code of a block = z | s0<<2 | s1<<3 | s2<<4, z = position (0..3, lowest
+ *    K first) of the zero, si = 1 when the i-th non-zero (ascending position)
+ *    is -1.  code ^ 0x1C negates the block (the mirror pairs of Appendix C).
+ *  - rows padded to Np = ceil(N/64)*64, K to Kp = ceil(K/128)*128; padding
+ *    codes are zero bits.
+ *  - unit (r, c) = 64 rows x 128 weights = 1280 bytes at (r*Kp/128 + c)*1280.
+ *    Row i of the unit is a 160-bit little-endian stream, code j (weights
+ *    128c+4j..+3) at bits [5j, 5j+5); stream bits 0..127 are the 16 bytes at
+ *    16*i, bits 128..159 the 4 bytes at 1024 + 4*i.
+ *  Total size: Np * Kp * 5 / 32 bytes (exactly 5NK/32 when 64 | N, 128 | K).
+ */
+#ifndef SHERRY_H_
+#define SHERRY_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sherry_status {
+  SHERRY_OK = 0,
+  SHERRY_E_INVALID = 1,  /* null pointer or an argument out of its domain   */
+  SHERRY_E_SHAPE = 2,    /* m, n or k < 1, k % 4 != 0, or beyond the limits */
+  SHERRY_E_NOT_3_4 = 3,  /* a block of T is not exactly one 0 and three +-1 */
+  SHERRY_E_BUFSIZE = 4,  /* a caller buffer is smaller than required        */
+  SHERRY_E_ALIGN = 5,    /* a device pointer is not aligned as documented   */
+  SHERRY_E_DEVICE = 6    /* a HIP call or kernel launch failed              */
+} sherry_status;
+
+/* Largest accepted K: |acc| <= 127 * 3K/4 must stay exact in fp32 (< 2^24)
+ * and in int32; 2^24 / (128 * 3/4) = 174762, rounded down to 128 | K. */
+#define SHERRY_MAX_K 174720
+/* Largest accepted N and M (grid limits; far above any LLM layer). */
+#define SHERRY_MAX_N (1LL << 26)
+#define SHERRY_MAX_M (1LL << 24)
+
+/* Kernel selectors for sherry_gemm_ex (the automatic choice is by M). */
+#define SHERRY_KERNEL_AUTO 0
+#define SHERRY_KERNEL_GEMV 1 /* VALU decode + dot4 per token, M <= 4         */
+#define SHERRY_KERNEL_MFMA 2 /* decode to int8 tiles in LDS + int8 MFMA      */
+
+/* Static string for a status code (never NULL). */
+const char* sherry_status_str(int status);
+
+/* Library version string, e.g. "sherry 0.1 gfx950". */
+const char* sherry_version(void);
+
+/* Name of the HIP error behind the calling thread's most recent
+ * SHERRY_E_DEVICE ("hipSuccess" if none).  Static string, never NULL. */
+const char* sherry_last_error(void);
+
+/* ---------------------------------------------------------------------- */
+/* Offline packing (Appendix A, offline phase).  Host only.               */
+/* ---------------------------------------------------------------------- */
+
+/* Bytes of the packed 5-bit tiled layout for an n x k ternary matrix; 0 if
+ * n < 1, k < 1, k % 4 != 0, n > SHERRY_MAX_N or k > SHERRY_MAX_K. */
+size_t sherry_packed_bytes(int64_t n, int64_t k);
+
+/* Packs T (host, int8 [n][k] row-major, values in {-1,0,1}, exactly one zero
+ * in every 4-block along k) into out (host, out_bytes >=
+ * sherry_packed_bytes(n, k)); the first sherry_packed_bytes(n, k) bytes are
+ * written, padding included.  On SHERRY_E_NOT_3_4 the flat index n*(k/4)+b
+ * of the first offending block is stored to *bad_block when bad_block is not
+ * NULL (else it is left alone), and out is unspecified.  Uses host threads. */
+int sherry_pack(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                size_t out_bytes, int64_t* bad_block);
+
+/* Exact inverse of sherry_pack: reads packed (host, packed_bytes >=
+ * sherry_packed_bytes(n, k)) and writes t_out (host, int8 [n][k]). */
+int sherry_unpack(const uint8_t* packed, size_t packed_bytes, int64_t n,
+                  int64_t k, int8_t* t_out);
+
+/* ---------------------------------------------------------------------- */
+/* Activation quantization (the integer inputs of the online phase).       */
+/* ---------------------------------------------------------------------- */
+
+/* Per-token int8 quantization on the device.  x (device, fp32 [m][k], 16-byte
+ * aligned, finite values) -> q (device, int8 [m][k], 4-byte aligned) and
+ * x_scale (device, fp32 [m]):  s = max_k |x| / 127 (fp32 division);
+ * q = clamp(rint(x / s), -127, 127) with round-half-to-even; an all-zero row
+ * gives s = 0 and q = 0.  The paper does not specify activation quantization
+ * (its weights-only setting keeps BF16 activations, Limitations); this is
+ * the int8 per-token reading of the integer accumulation of Appendix A. */
+int sherry_quantize_act(const float* x, int64_t m, int64_t k, int8_t* q,
+                        float* x_scale, void* stream);
+
+/* ---------------------------------------------------------------------- */
+/* Online products (Eq. 2).                                                */
+/* ---------------------------------------------------------------------- */
+
+/* M = 1 product (decode).  w: device, packed layout of an n x k matrix,
+ * 16-byte aligned.  x: device, int8 [k], 4-byte aligned.  x_scale: device,
+ * fp32 [1].  w_scale: the per-tensor alpha.  y: device, fp32 [n], 4-byte
+ * aligned.  acc: device, int32 [n] or NULL (then not written). */
+int sherry_gemv(const uint8_t* w, const int8_t* x, const float* x_scale,
+                float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                void* stream);
+
+/* Any-M product.  x: device, int8 [m][k] row-major, 16-byte aligned.
+ * x_scale: device, fp32 [m].  y: device, fp32 [m][n]; acc: device, int32
+ * [m][n] or NULL.  Other arguments as sherry_gemv.  Chooses the kernel by M
+ * (see sherry_gemm_kernel_for). */
+int sherry_gemm(const uint8_t* w, const int8_t* x, const float* x_scale,
+                float w_scale, float* y, int32_t* acc, int64_t m, int64_t n,
+                int64_t k, void* stream);
+
+/* sherry_gemm with an explicit kernel (SHERRY_KERNEL_*); SHERRY_KERNEL_GEMV
+ * requires m <= 4.  Results are bit-identical across kernels. */
+int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
+                   float w_scale, float* y, int32_t* acc, int64_t m,
+                   int64_t n, int64_t k, int kernel, void* stream);
+
+/* The kernel sherry_gemm picks for this shape (SHERRY_KERNEL_GEMV or
+ * SHERRY_KERNEL_MFMA), or -SHERRY_E_SHAPE for an invalid shape. */
+int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k);
+
+/* ---------------------------------------------------------------------- */
+/* Grouped M = 1 products: many independent GEMVs in one launch.           */
+/* ---------------------------------------------------------------------- */
+
+typedef struct sherry_gemv_desc {
+  const uint8_t* w;      /* device, packed n x k, 16-byte aligned          */
+  const int8_t* x;       /* device, int8 [k], 4-byte aligned               */
+  const float* x_scale;  /* device, fp32 [1]                               */
+  float* y;              /* device, fp32 [n]                               */
+  int32_t* acc;          /* device, int32 [n] or NULL                      */
+  int64_t n, k;
+  float w_scale;
+  int32_t tile_begin;    /* written by sherry_gemv_batched_prepare         */
+} sherry_gemv_desc;
+
+/* Host: validates descs[0..count) and fills each tile_begin (prefix sum of
+ * ceil(n/64)); *total_tiles receives the sum.  count >= 1. */
+int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
+                                int64_t* total_tiles);
+
+/* Runs every GEMV of descs_dev (device, a byte copy of an array accepted by
+ * sherry_gemv_batched_prepare, 8-byte aligned) in one launch.  count and
+ * total_tiles must be the values used with / returned by prepare; the device
+ * descriptors cannot be re-validated here. */
+int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
+                        int64_t total_tiles, void* stream);
+
+/* ---------------------------------------------------------------------- */
+/* 2-bit reference layout (the "2-bit strategy" of Sec. 2.3): one ternary  */
+/* weight per 2 bits, value w+1; unit (r, c) = 64 rows x 64 weights = 1024 */
+/* bytes at (r*Kp/64 + c)*1024, Kp = ceil(K/64)*64; row i's 16 bytes at    */
+/* 16*i hold weight 64c+u at bits [2u, 2u+2); padding is weight 0.         */
+/* Used only to compare bytes moved against the 5-bit layout.             */
+/* ---------------------------------------------------------------------- */
+
+size_t sherry_packed2_bytes(int64_t n, int64_t k);
+
+/* Packs any ternary T (host, int8 [n][k] in {-1,0,1}); SHERRY_E_INVALID for
+ * another value, its flat index in *bad_index when not NULL. */
+int sherry_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                 size_t out_bytes, int64_t* bad_index);
+
+/* M = 1 product on the 2-bit layout; arguments as sherry_gemv. */
+int sherry_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,
+                 float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                 void* stream);
+
+/* ---------------------------------------------------------------------- */
+/* Diagnostics.                                                            */
+/* ---------------------------------------------------------------------- */
+
+/* Streaming-read ceiling probe: reads `bytes` (multiple of 16, src 16-byte
+ * aligned) with 128-bit loads and writes one XOR checksum word per workgroup
+ * to sink (device, uint32 [sherry_stream_read_groups(bytes)]). */
+int sherry_stream_read(const void* src, size_t bytes, uint32_t* sink,
+                       void* stream);
+int64_t sherry_stream_read_groups(size_t bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SHERRY_H_ */

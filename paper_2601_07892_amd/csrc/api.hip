@@ -1,0 +1,149 @@
+// C ABI entry points: argument validation, M-dispatch, launches.
+// Every check happens on the host before anything is enqueued.
+#include <cstdlib>
+
+#include "sherry_internal.h"
+
+namespace sherry {
+namespace {
+thread_local hipError_t g_last_error = hipSuccess;
+}  // namespace
+void set_last_error(hipError_t e) { g_last_error = e; }
+}  // namespace sherry
+
+using namespace sherry;
+
+namespace {
+
+inline bool aligned(const void* p, uintptr_t a) {
+  return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+inline bool shape_ok(int64_t m, int64_t n, int64_t k) {
+  return m >= 1 && n >= 1 && k >= 1 && k % 4 == 0 && m <= SHERRY_MAX_M && n <= SHERRY_MAX_N &&
+         k <= SHERRY_MAX_K;
+}
+
+inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+// Largest M the VALU decode kernel serves; above it the MFMA kernel runs.
+constexpr int64_t kGemvMaxM = 4;
+
+int check_product(const uint8_t* w, const int8_t* x, const float* x_scale, float* y,
+                  int64_t m, int64_t n, int64_t k, uintptr_t x_align) {
+  if (!w || !x || !x_scale || !y) return SHERRY_E_INVALID;
+  if (!shape_ok(m, n, k)) return SHERRY_E_SHAPE;
+  if (!aligned(w, 16) || !aligned(x, x_align) || !aligned(x_scale, 4) || !aligned(y, 4))
+    return SHERRY_E_ALIGN;
+  return SHERRY_OK;
+}
+
+}  // namespace
+
+extern "C" const char* sherry_status_str(int status) {
+  switch (status) {
+    case SHERRY_OK: return "ok";
+    case SHERRY_E_INVALID: return "invalid argument";
+    case SHERRY_E_SHAPE: return "invalid shape";
+    case SHERRY_E_NOT_3_4: return "block is not 3:4 (exactly one zero, three +-1)";
+    case SHERRY_E_BUFSIZE: return "buffer too small";
+    case SHERRY_E_ALIGN: return "misaligned pointer";
+    case SHERRY_E_DEVICE: return "device error";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* sherry_version(void) { return "sherry 0.1 gfx950"; }
+
+extern "C" const char* sherry_last_error(void) { return hipGetErrorName(g_last_error); }
+
+extern "C" int sherry_quantize_act(const float* x, int64_t m, int64_t k, int8_t* q,
+                                   float* x_scale, void* stream) {
+  if (!x || !q || !x_scale) return SHERRY_E_INVALID;
+  if (!shape_ok(m, 1, k)) return SHERRY_E_SHAPE;
+  if (!aligned(x, 16) || !aligned(q, 4) || !aligned(x_scale, 4)) return SHERRY_E_ALIGN;
+  return launch_quantize(x, m, k, q, x_scale, as_stream(stream));
+}
+
+extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
+  if (!shape_ok(m, n, k)) return -SHERRY_E_SHAPE;
+  return m <= kGemvMaxM ? SHERRY_KERNEL_GEMV : SHERRY_KERNEL_MFMA;
+}
+
+extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
+                              float w_scale, float* y, int32_t* acc, int64_t m, int64_t n,
+                              int64_t k, int kernel, void* stream) {
+  if (kernel == SHERRY_KERNEL_AUTO) {
+    const int kk = sherry_gemm_kernel_for(m, n, k);
+    kernel = kk < 0 ? SHERRY_KERNEL_GEMV : kk;
+  }
+  if (kernel == SHERRY_KERNEL_GEMV) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 4);
+    if (st != SHERRY_OK) return st;
+    if (m > kGemvMaxM) return SHERRY_E_SHAPE;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_gemv_valu(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
+  }
+  if (kernel == SHERRY_KERNEL_MFMA) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 16);
+    if (st != SHERRY_OK) return st;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_gemm_mfma(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
+  }
+  return SHERRY_E_INVALID;
+}
+
+extern "C" int sherry_gemm(const uint8_t* w, const int8_t* x, const float* x_scale,
+                           float w_scale, float* y, int32_t* acc, int64_t m, int64_t n,
+                           int64_t k, void* stream) {
+  return sherry_gemm_ex(w, x, x_scale, w_scale, y, acc, m, n, k, SHERRY_KERNEL_AUTO, stream);
+}
+
+extern "C" int sherry_gemv(const uint8_t* w, const int8_t* x, const float* x_scale,
+                           float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                           void* stream) {
+  return sherry_gemm_ex(w, x, x_scale, w_scale, y, acc, 1, n, k, SHERRY_KERNEL_GEMV, stream);
+}
+
+extern "C" int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
+                                           int64_t* total_tiles) {
+  if (!descs || !total_tiles || count < 1) return SHERRY_E_INVALID;
+  int64_t tiles = 0;
+  for (int i = 0; i < count; ++i) {
+    sherry_gemv_desc& d = descs[i];
+    int st = check_product(d.w, d.x, d.x_scale, d.y, 1, d.n, d.k, 4);
+    if (st != SHERRY_OK) return st;
+    if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
+    d.tile_begin = static_cast<int32_t>(tiles);
+    tiles += ceil_div(d.n, kTileRows);
+    if (tiles > INT32_MAX) return SHERRY_E_SHAPE;
+  }
+  *total_tiles = tiles;
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
+                                   int64_t total_tiles, void* stream) {
+  if (!descs_dev || count < 1 || total_tiles < 1 || total_tiles > INT32_MAX)
+    return SHERRY_E_INVALID;
+  if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  return launch_gemv_batched(descs_dev, count, total_tiles, as_stream(stream));
+}
+
+extern "C" int sherry_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,
+                            float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                            void* stream) {
+  int st = check_product(w2, x, x_scale, y, 1, n, k, 4);
+  if (st != SHERRY_OK) return st;
+  if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+  return launch_gemv2(w2, x, x_scale, w_scale, y, acc, n, k, as_stream(stream));
+}
+
+extern "C" int64_t sherry_stream_read_groups(size_t bytes) { return stream_read_groups(bytes); }
+
+extern "C" int sherry_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+  if (!src || !sink) return SHERRY_E_INVALID;
+  if (bytes == 0 || bytes % 16 != 0) return SHERRY_E_SHAPE;
+  if (!aligned(src, 16) || !aligned(sink, 4)) return SHERRY_E_ALIGN;
+  return launch_stream_read(src, bytes, sink, as_stream(stream));
+}

@@ -1,0 +1,241 @@
+// Offline packing (Appendix A, offline phase): host code.
+//
+// sherry_pack turns a ternary 3:4 matrix into the 5-bit tiled layout that the
+// device products stream; sherry_unpack is its exact inverse.  sherry_pack2
+// writes the 2-bit reference layout.  Layouts are defined in sherry.h.
+#include <algorithm>
+#include <atomic>
+#include <cstring>
+#include <thread>
+#include <vector>
+
+#include "sherry_internal.h"
+
+namespace sherry {
+namespace {
+
+// Code of one block, or -1 if it does not hold exactly one zero and three
+// values in {-1, +1} (Eq. 3).
+inline int encode_block(const int8_t* w) {
+  int z = -1;
+  uint32_t neg = 0;  // bit p set when weight p is -1
+  for (int p = 0; p < 4; ++p) {
+    const int v = w[p];
+    if (v == 0) {
+      if (z >= 0) return -1;
+      z = p;
+    } else if (v == -1) {
+      neg |= 1u << p;
+    } else if (v != 1) {
+      return -1;
+    }
+  }
+  if (z < 0) return -1;
+  // drop the zero's position: sign bits of the non-zeros, ascending
+  const uint32_t below = neg & ((1u << z) - 1u);
+  const uint32_t above = neg >> (z + 1);
+  return static_cast<int>(static_cast<uint32_t>(z) | ((below | (above << z)) << 2));
+}
+
+unsigned worker_count(int64_t jobs) {
+  unsigned hw = std::thread::hardware_concurrency();
+  if (hw == 0) hw = 4;
+  hw = std::min(hw, 32u);
+  return static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>(hw, jobs)));
+}
+
+// Runs fn(begin, end) over [0, jobs) split into contiguous ranges.
+template <class Fn>
+void parallel_ranges(int64_t jobs, Fn fn) {
+  const unsigned nt = worker_count(jobs);
+  if (nt <= 1) {
+    fn(int64_t(0), jobs);
+    return;
+  }
+  std::vector<std::thread> th;
+  th.reserve(nt);
+  for (unsigned t = 0; t < nt; ++t) {
+    const int64_t b = jobs * t / nt, e = jobs * (t + 1) / nt;
+    th.emplace_back([=] { fn(b, e); });
+  }
+  for (auto& x : th) x.join();
+}
+
+// Packs the 32 codes of one row container into 16 head bytes + 4 tail bytes.
+inline void put_container(const uint32_t* codes, uint8_t* head, uint8_t* tail) {
+  uint64_t lo = 0, mid = 0;
+  uint32_t hi = 0;
+  for (int j = 0; j < 32; ++j) {
+    const uint64_t c = codes[j];
+    const int b = 5 * j;
+    if (b + 5 <= 64) {
+      lo |= c << b;
+    } else if (b < 64) {  // straddles bit 64
+      lo |= c << b;
+      mid |= c >> (64 - b);
+    } else if (b + 5 <= 128) {
+      mid |= c << (b - 64);
+    } else if (b < 128) {  // straddles bit 128
+      mid |= c << (b - 64);
+      hi |= static_cast<uint32_t>(c >> (128 - b));
+    } else {
+      hi |= static_cast<uint32_t>(c << (b - 128));
+    }
+  }
+  std::memcpy(head, &lo, 8);
+  std::memcpy(head + 8, &mid, 8);
+  std::memcpy(tail, &hi, 4);
+}
+
+inline void get_container(const uint8_t* head, const uint8_t* tail, uint32_t* codes) {
+  uint64_t lo, mid;
+  uint32_t hi;
+  std::memcpy(&lo, head, 8);
+  std::memcpy(&mid, head + 8, 8);
+  std::memcpy(&hi, tail, 4);
+  for (int j = 0; j < 32; ++j) {
+    const int b = 5 * j;
+    uint64_t v;
+    if (b + 5 <= 64) v = lo >> b;
+    else if (b < 64) v = (lo >> b) | (mid << (64 - b));
+    else if (b + 5 <= 128) v = mid >> (b - 64);
+    else if (b < 128) v = (mid >> (b - 64)) | (static_cast<uint64_t>(hi) << (128 - b));
+    else v = hi >> (b - 128);
+    codes[j] = static_cast<uint32_t>(v & 31u);
+  }
+}
+
+}  // namespace
+}  // namespace sherry
+
+using namespace sherry;
+
+extern "C" size_t sherry_packed_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1 || k % 4 != 0 || n > SHERRY_MAX_N || k > SHERRY_MAX_K) return 0;
+  return static_cast<size_t>(ceil_div(n, kTileRows) * kTileRows) *
+         static_cast<size_t>(ceil_div(k, kTileK) * kTileK) * 5 / 32;
+}
+
+extern "C" int sherry_pack(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                           size_t out_bytes, int64_t* bad_block) {
+  if (!t || !out) return SHERRY_E_INVALID;
+  const size_t need = sherry_packed_bytes(n, k);
+  if (need == 0) return SHERRY_E_SHAPE;
+  if (out_bytes < need) return SHERRY_E_BUFSIZE;
+  const int64_t R = ceil_div(n, kTileRows), C = ceil_div(k, kTileK);
+  const int64_t nb = k / 4;
+  std::atomic<int64_t> first_bad{INT64_MAX};
+  parallel_ranges(R, [&](int64_t r0, int64_t r1) {
+    uint32_t codes[32];
+    for (int64_t r = r0; r < r1; ++r) {
+      for (int64_t c = 0; c < C; ++c) {
+        uint8_t* unit = out + static_cast<size_t>(r * C + c) * kUnitBytes;
+        for (int i = 0; i < kTileRows; ++i) {
+          const int64_t row = r * kTileRows + i;
+          for (int j = 0; j < 32; ++j) {
+            const int64_t b = c * 32 + j;
+            int code = 0;
+            if (row < n && b < nb) {
+              code = encode_block(t + row * k + 4 * b);
+              if (code < 0) {
+                const int64_t flat = row * nb + b;
+                int64_t cur = first_bad.load();
+                while (flat < cur && !first_bad.compare_exchange_weak(cur, flat)) {
+                }
+                code = 0;
+              }
+            }
+            codes[j] = static_cast<uint32_t>(code);
+          }
+          put_container(codes, unit + 16 * i, unit + kHeadBytes + 4 * i);
+        }
+      }
+    }
+  });
+  if (first_bad.load() != INT64_MAX) {
+    if (bad_block) *bad_block = first_bad.load();
+    return SHERRY_E_NOT_3_4;
+  }
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_unpack(const uint8_t* packed, size_t packed_bytes, int64_t n,
+                             int64_t k, int8_t* t_out) {
+  if (!packed || !t_out) return SHERRY_E_INVALID;
+  const size_t need = sherry_packed_bytes(n, k);
+  if (need == 0) return SHERRY_E_SHAPE;
+  if (packed_bytes < need) return SHERRY_E_BUFSIZE;
+  const int64_t R = ceil_div(n, kTileRows), C = ceil_div(k, kTileK);
+  const int64_t nb = k / 4;
+  parallel_ranges(R, [&](int64_t r0, int64_t r1) {
+    uint32_t codes[32];
+    for (int64_t r = r0; r < r1; ++r) {
+      for (int64_t c = 0; c < C; ++c) {
+        const uint8_t* unit = packed + static_cast<size_t>(r * C + c) * kUnitBytes;
+        for (int i = 0; i < kTileRows; ++i) {
+          const int64_t row = r * kTileRows + i;
+          if (row >= n) break;
+          get_container(unit + 16 * i, unit + kHeadBytes + 4 * i, codes);
+          for (int j = 0; j < 32; ++j) {
+            const int64_t b = c * 32 + j;
+            if (b >= nb) break;
+            const uint32_t word = decode_word(codes[j]);
+            for (int p = 0; p < 4; ++p)
+              t_out[row * k + 4 * b + p] = static_cast<int8_t>((word >> (8 * p)) & 0xFF);
+          }
+        }
+      }
+    }
+  });
+  return SHERRY_OK;
+}
+
+extern "C" size_t sherry_packed2_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1 || k % 4 != 0 || n > SHERRY_MAX_N || k > SHERRY_MAX_K) return 0;
+  return static_cast<size_t>(ceil_div(n, kTileRows) * kTileRows) *
+         static_cast<size_t>(ceil_div(k, kTileK2) * kTileK2) / 4;
+}
+
+extern "C" int sherry_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                            size_t out_bytes, int64_t* bad_index) {
+  if (!t || !out) return SHERRY_E_INVALID;
+  const size_t need = sherry_packed2_bytes(n, k);
+  if (need == 0) return SHERRY_E_SHAPE;
+  if (out_bytes < need) return SHERRY_E_BUFSIZE;
+  const int64_t R = ceil_div(n, kTileRows), C = ceil_div(k, kTileK2);
+  std::atomic<int64_t> first_bad{INT64_MAX};
+  parallel_ranges(R, [&](int64_t r0, int64_t r1) {
+    for (int64_t r = r0; r < r1; ++r) {
+      for (int64_t c = 0; c < C; ++c) {
+        uint8_t* unit = out + static_cast<size_t>(r * C + c) * kUnit2Bytes;
+        for (int i = 0; i < kTileRows; ++i) {
+          const int64_t row = r * kTileRows + i;
+          uint64_t word[2] = {0x5555555555555555ull, 0x5555555555555555ull};
+          if (row < n) {
+            for (int u = 0; u < kTileK2; ++u) {
+              const int64_t kk = c * kTileK2 + u;
+              if (kk >= k) break;
+              const int v = t[row * k + kk];
+              if (v < -1 || v > 1) {
+                const int64_t flat = row * k + kk;
+                int64_t cur = first_bad.load();
+                while (flat < cur && !first_bad.compare_exchange_weak(cur, flat)) {
+                }
+                continue;
+              }
+              const int sh = (2 * u) & 63;
+              word[u >> 5] &= ~(3ull << sh);
+              word[u >> 5] |= static_cast<uint64_t>(v + 1) << sh;
+            }
+          }
+          std::memcpy(unit + 16 * i, word, 16);
+        }
+      }
+    }
+  });
+  if (first_bad.load() != INT64_MAX) {
+    if (bad_index) *bad_index = first_bad.load();
+    return SHERRY_E_INVALID;
+  }
+  return SHERRY_OK;
+}

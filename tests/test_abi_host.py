@@ -1,0 +1,201 @@
+"""Host-side tests of the C ABI: exports, validation, packing parity.
+
+No GPU needed: every device call here fails host validation before anything
+is enqueued (fake pointers are never dereferenced).
+"""
+import ctypes
+import json
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2601_07892_amd as sh
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sherry.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+L = sh.lib
+FAKE = 0x10000  # 64 KiB-aligned, never dereferenced
+FAKE_MIS = FAKE + 2
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sherry_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 17
+    out = subprocess.run(["nm", "-D", "--defined-only", sh.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (sherry_\w+)", out))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(L, n), n
+    assert set(names) == set(sh.EXPORTS)
+
+
+def test_status_strings_and_version():
+    for st in range(7):
+        assert sh._status_str(st)
+    assert "gfx950" in sh.sherry_version()
+
+
+def test_packed_bytes():
+    assert sh.sherry_packed_bytes(2048, 2048) == 2048 * 2048 * 5 // 32
+    assert sh.sherry_packed_bytes(1, 4) == 64 * 128 * 5 // 32
+    assert sh.sherry_packed_bytes(0, 4) == 0
+    assert sh.sherry_packed_bytes(4, 6) == 0
+    assert sh.sherry_packed_bytes(4, sh.SHERRY_MAX_K + 4) == 0
+    for n, k in [(1, 4), (70, 1032), (2048, 8192)]:
+        assert sh.sherry_packed_bytes(n, k) == oracle.packed_bytes(n, k)
+        assert sh.sherry_packed2_bytes(n, k) == oracle.packed2_bytes(n, k)
+
+
+# ------------------------------------------------------------- packing parity
+
+@pytest.mark.parametrize("n,k", [(1, 4), (1, 8), (3, 124), (63, 128), (64, 132), (65, 516),
+                                 (130, 1032), (257, 2048), (64, 4100)])
+def test_pack_matches_oracle(n, k):
+    t = synth.ternary_34(n, k, 21, "pk")
+    p = sh.sherry_pack(t)
+    assert np.array_equal(p, oracle.pack(t))
+    assert np.array_equal(sh.sherry_unpack(p, n, k), t)
+    assert np.array_equal(oracle.unpack(p, n, k), t)
+    t2 = synth.ternary_any(n, k, 21, "pk2")
+    p2 = sh.sherry_pack2(t2)
+    assert np.array_equal(p2, oracle.pack2(t2))
+    assert np.array_equal(oracle.unpack2(p2, n, k), t2)
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2])
+def test_pack_hand_derived_fixtures(idx):
+    with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
+        fx = json.load(f)["five_bit"][idx]
+    g = oracle.code_table()
+    t = np.tile(np.array([0, 1, 1, 1], np.int8), (fx["n"], fx["k"] // 4))
+    for row, blk, code in fx["blocks"]:
+        t[row, 4 * blk:4 * blk + 4] = g[code]
+    p = sh.sherry_pack(t)
+    assert p.size == fx["total_bytes"]
+    nz = {int(i): int(p[i]) for i in np.nonzero(p)[0]}
+    assert nz == {int(a): b for a, b in fx["nonzero"].items()}
+
+
+def test_pack_large_multithreaded():
+    n, k = 4096, 2048  # many row tiles -> several host threads
+    t = synth.ternary_34(n, k, 22, "big")
+    p = sh.sherry_pack(t)
+    assert np.array_equal(sh.sherry_unpack(p, n, k), t)
+    # spot-check against the oracle on a slice of row tiles
+    sub = t[128:256]
+    assert np.array_equal(sh.sherry_pack(sub), oracle.pack(sub))
+
+
+@pytest.mark.parametrize("zeros", [0, 2, 3, 4])
+def test_pack_rejects_non_34(zeros):
+    n, k = 700, 256
+    t = synth.ternary_34(n, k, 23, "rej")
+    blk = np.array([0] * zeros + [1] * (4 - zeros), np.int8)
+    t[650, 8:12] = blk
+    t[300, 100:104] = blk
+    with pytest.raises(sh.SherryError) as e:
+        sh.sherry_pack(t)
+    assert e.value.status == sh.SHERRY_E_NOT_3_4
+    assert e.value.bad_block == 300 * (k // 4) + 25 == oracle.pack_bad_block(t)
+
+
+def test_pack_rejects_bad_values_and_buffers():
+    t = synth.ternary_34(2, 8, 24, "val")
+    t[1, 4:8] = [0, 1, 2, 1]
+    with pytest.raises(sh.SherryError) as e:
+        sh.sherry_pack(t)
+    assert e.value.bad_block == 3
+    t = synth.ternary_34(2, 8, 24, "buf")
+    small = np.zeros(sh.sherry_packed_bytes(2, 8) - 1, np.uint8)
+    assert L.sherry_pack(t.ctypes.data, 2, 8, small.ctypes.data, small.nbytes, None) == \
+        sh.SHERRY_E_BUFSIZE
+    assert L.sherry_pack(None, 2, 8, small.ctypes.data, small.nbytes, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_pack(t.ctypes.data, 2, 6, small.ctypes.data, small.nbytes, None) == \
+        sh.SHERRY_E_SHAPE
+    t2 = np.zeros((1, 8), np.int8)
+    t2[0, 3] = 5
+    bad = ctypes.c_int64(-1)
+    out = np.zeros(sh.sherry_packed2_bytes(1, 8), np.uint8)
+    assert L.sherry_pack2(t2.ctypes.data, 1, 8, out.ctypes.data, out.nbytes,
+                          ctypes.byref(bad)) == sh.SHERRY_E_INVALID
+    assert bad.value == 3
+
+
+# -------------------------------------------------- validation of device calls
+
+def test_gemm_validation_without_launch():
+    g = L.sherry_gemm_ex
+    # null pointers
+    assert g(None, FAKE, FAKE, 1.0, FAKE, None, 1, 64, 128, 0, None) == sh.SHERRY_E_INVALID
+    assert g(FAKE, FAKE, FAKE, 1.0, None, None, 1, 64, 128, 0, None) == sh.SHERRY_E_INVALID
+    # shapes
+    for m, n, k in [(0, 64, 128), (1, 0, 128), (1, 64, 0), (1, 64, 130),
+                    (1, 64, sh.SHERRY_MAX_K + 4)]:
+        assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, m, n, k, 0, None) == sh.SHERRY_E_SHAPE
+    # GEMV kernel is limited to m <= 4
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 5, 64, 128, sh.SHERRY_KERNEL_GEMV,
+             None) == sh.SHERRY_E_SHAPE
+    # alignment: packed weights 16 B, activations 16 B for the MFMA kernel
+    assert g(FAKE_MIS, FAKE, FAKE, 1.0, FAKE, None, 1, 64, 128, 0, None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE + 4, FAKE, 1.0, FAKE, None, 64, 64, 128, sh.SHERRY_KERNEL_MFMA,
+             None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, FAKE_MIS, 64, 64, 128, sh.SHERRY_KERNEL_MFMA,
+             None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 8, 64, 128, 7, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_gemv(FAKE, FAKE + 1, FAKE, 1.0, FAKE, None, 64, 128, None) == \
+        sh.SHERRY_E_ALIGN
+    assert L.sherry_quantize_act(FAKE + 4, 1, 128, FAKE, FAKE, None) == sh.SHERRY_E_ALIGN
+    assert L.sherry_quantize_act(FAKE, 1, 126, FAKE, FAKE, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_quantize_act(None, 1, 128, FAKE, FAKE, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_gemv2(FAKE, FAKE, FAKE, 1.0, FAKE, None, 64, 126, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_stream_read(FAKE, 100, FAKE, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_stream_read(FAKE + 8, 128, FAKE, None) == sh.SHERRY_E_ALIGN
+
+
+def test_kernel_choice_by_m():
+    for m in (1, 2, 3, 4):
+        assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_GEMV
+    for m in (5, 16, 64, 2048):
+        assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_MFMA
+    assert sh.sherry_gemm_kernel_for(0, 2048, 2048) == -sh.SHERRY_E_SHAPE
+
+
+def test_batched_prepare():
+    shapes = [(2048, 2048), (512, 2048), (8192, 2048), (2048, 8192), (70, 132)]
+    descs = (sh.sherry_gemv_desc * len(shapes))()
+    for i, (n, k) in enumerate(shapes):
+        descs[i].w = FAKE
+        descs[i].x = FAKE
+        descs[i].x_scale = FAKE
+        descs[i].y = FAKE
+        descs[i].acc = None
+        descs[i].n = n
+        descs[i].k = k
+        descs[i].w_scale = 0.02
+    total = sh.sherry_gemv_batched_prepare(descs)
+    begins = [d.tile_begin for d in descs]
+    assert begins == [0, 32, 40, 168, 200]
+    assert total == 202
+    assert ctypes.sizeof(sh.sherry_gemv_desc) == 64
+    descs[3].k = 6
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemv_batched_prepare(descs)
+    descs[3].k = 8192
+    descs[1].w = FAKE + 8
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemv_batched_prepare(descs)
+    assert L.sherry_gemv_batched(None, 1, 1, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_gemv_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN

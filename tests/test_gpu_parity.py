@@ -1,0 +1,346 @@
+"""GPU parity of the HIP path against the CPU oracle (through the C ABI).
+
+int32 accumulators must match bit-exactly; fp32 outputs within 1e-5 relative
+(y_ref = 0 requires y = 0).  Quantized activations and their scales must match
+bit-exactly (both sides decide in fp32).
+"""
+import ctypes
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-5
+
+
+def _sh():
+    import paper_2601_07892_amd as sh
+    return sh
+
+
+def _say(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    d = torch.device("cuda:0")
+    torch.cuda.set_device(d)
+    return d
+
+
+def _y_ok(y, y_ref):
+    y = np.asarray(y, np.float64)
+    bad = np.abs(y - y_ref) > RTOL * np.abs(y_ref)
+    return not bad.any()
+
+
+def _run(dev, t, q, sx, sw, kernel, m, with_acc=True, packed=None):
+    sh = _sh()
+    n, k = t.shape
+    w = torch.from_numpy(packed if packed is not None else sh.sherry_pack(t)).to(dev)
+    qd = torch.from_numpy(np.ascontiguousarray(q)).to(dev)
+    sxd = torch.from_numpy(np.ascontiguousarray(sx)).to(dev)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+    acc = torch.full((m, n), -7, dtype=torch.int32, device=dev) if with_acc else None
+    sh.sherry_gemm_ex(w, qd, sxd, sw, y, acc, m, n, k, kernel)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), (acc.cpu().numpy() if with_acc else None)
+
+
+# ---------------------------------------------------------------- quantizer
+
+@pytest.mark.parametrize("m,k,outl", [(1, 4, 0.0), (3, 1000, 0.0), (7, 2048, 0.01),
+                                      (64, 8192, 0.01), (2048, 3072, 0.01)])
+def test_quantize_bit_exact(dev, m, k, outl):
+    sh = _sh()
+    _say("quantize", m, k, outl)
+    x = synth.activations(m, k, 31, "q", outlier_frac=outl)
+    if m >= 3:
+        x[1] = 0.0           # all-zero token
+        x[2, :4] = [0.5, 1.5, 2.5, -127.0]  # ties after scaling by absmax 127
+        x[2, 4:] = 0.0
+    xd = torch.from_numpy(x).to(dev)
+    q = torch.empty((m, k), dtype=torch.int8, device=dev)
+    sx = torch.empty(m, dtype=torch.float32, device=dev)
+    sh.sherry_quantize_act(xd, q, sx)
+    torch.cuda.synchronize()
+    q_ref, sx_ref = oracle.quantize_act(x)
+    assert np.array_equal(sx.cpu().numpy(), sx_ref)
+    assert np.array_equal(q.cpu().numpy(), q_ref)
+
+
+# ------------------------------------------------------- decode kernel (M<=4)
+
+GEMV_SHAPES = [(1, 4), (64, 128), (65, 132), (1, 124), (130, 1028), (257, 2048),
+               (512, 2048), (300, 3072), (64, 8192 + 4)]
+
+
+@pytest.mark.parametrize("n,k", GEMV_SHAPES)
+@pytest.mark.parametrize("m", [1, 2, 3, 4])
+def test_gemv_kernel_parity(dev, m, n, k):
+    sh = _sh()
+    _say("gemv", m, n, k)
+    t = synth.ternary_34(n, k, 32, "gv", n, k)
+    q = synth.int8_any(m, k, 32, "gv", m, k)
+    sx = np.abs(synth.activations(1, m, 32, "gvs", m)[0]).astype(np.float32) + 0.01
+    sw = synth.weight_scale(32, "gv", n, k)
+    y, acc = _run(dev, t, q, sx, sw, sh.SHERRY_KERNEL_GEMV, m)
+    acc_ref = oracle.gemm_i32(q, t, threads=4)
+    assert np.array_equal(acc, acc_ref)
+    assert _y_ok(y, oracle.epilogue(acc_ref, sx, sw))
+
+
+# ---------------------------------------------------------- MFMA kernel
+
+MFMA_CASES = [(5, 64, 128), (16, 65, 132), (32, 256, 1024), (33, 300, 1032), (64, 512, 2048),
+              (100, 257, 516), (256, 512, 2048), (300, 700, 3072), (512, 1024, 1536),
+              (1, 128, 256), (4, 64, 128)]
+
+
+@pytest.mark.parametrize("m,n,k", MFMA_CASES)
+def test_mfma_kernel_parity(dev, m, n, k):
+    sh = _sh()
+    _say("mfma", m, n, k)
+    t = synth.ternary_34(n, k, 33, "mf", n, k)
+    q = synth.int8_any(m, k, 33, "mf", m, k)
+    sx = np.abs(synth.activations(1, m, 33, "mfs", m)[0]).astype(np.float32) + 0.01
+    sw = synth.weight_scale(33, "mf", n, k)
+    y, acc = _run(dev, t, q, sx, sw, sh.SHERRY_KERNEL_MFMA, m)
+    acc_ref = oracle.gemm_i32(q, t, threads=8)
+    assert np.array_equal(acc, acc_ref)
+    assert _y_ok(y, oracle.epilogue(acc_ref, sx, sw))
+
+
+def test_mfma_large_tile_config(dev):
+    # M, N large enough that the 256x256 tile configuration is chosen
+    sh = _sh()
+    m, n, k = 2048, 8192, 640
+    _say("mfma-large", m, n, k)
+    t = synth.ternary_34(n, k, 34, "ml")
+    q = synth.int8_any(m, k, 34, "ml")
+    sx = np.full(m, 0.5, np.float32)
+    y, acc = _run(dev, t, q, sx, 0.25, sh.SHERRY_KERNEL_MFMA, m)
+    rng = np.random.default_rng(0)
+    for i, j in zip(rng.integers(0, m, 2000), rng.integers(0, n, 2000)):
+        assert acc[i, j] == oracle.dot_i32(q[i], t[j])
+    # exact scale products: y = acc / 8 exactly
+    assert np.array_equal(y.astype(np.float64), acc.astype(np.float64) * 0.125)
+
+
+# ------------------------------------------------------ end-to-end + dispatch
+
+@pytest.mark.parametrize("m,n,k", [(1, 2048, 2048), (4, 1024, 3072), (16, 1024, 3072),
+                                   (64, 1024, 4096)])
+def test_end_to_end_auto(dev, m, n, k):
+    sh = _sh()
+    _say("e2e", m, n, k)
+    t = synth.ternary_34(n, k, 35, "e2e", n, k)
+    x = synth.activations(m, k, 35, "e2e", m, k, outlier_frac=0.01)
+    sw = synth.weight_scale(35, "e2e")
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    xd = torch.from_numpy(x).to(dev)
+    q = torch.empty((m, k), dtype=torch.int8, device=dev)
+    sx = torch.empty(m, dtype=torch.float32, device=dev)
+    y = torch.empty((m, n), dtype=torch.float32, device=dev)
+    acc = torch.empty((m, n), dtype=torch.int32, device=dev)
+    sh.sherry_quantize_act(xd, q, sx)
+    sh.sherry_gemm(w, q, sx, sw, y, acc, m, n, k)
+    torch.cuda.synchronize()
+    q_ref, sx_ref, acc_ref, y_ref = oracle.linear(x, t, sw, threads=8)
+    assert np.array_equal(q.cpu().numpy(), q_ref)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref)
+    assert _y_ok(y.cpu().numpy(), y_ref)
+
+
+def test_kernels_agree_bitwise(dev):
+    sh = _sh()
+    n, k = 320, 1280
+    t = synth.ternary_34(n, k, 36, "agree")
+    for m in (1, 2, 3, 4):
+        q = synth.int8_any(m, k, 36, "agree", m)
+        sx = np.full(m, 0.1, np.float32)
+        y1, a1 = _run(dev, t, q, sx, 0.03, sh.SHERRY_KERNEL_GEMV, m)
+        y2, a2 = _run(dev, t, q, sx, 0.03, sh.SHERRY_KERNEL_MFMA, m)
+        assert np.array_equal(a1, a2) and np.array_equal(y1, y2)
+
+
+# ---------------------------------------------------------- closed forms
+
+def test_one_hot_and_all_ones(dev):
+    sh = _sh()
+    n, k = 200, 384
+    t = synth.ternary_34(n, k, 37, "oh")
+    for kk in (0, 1, 127, 128, 383):
+        e = np.zeros((1, k), np.int8)
+        e[0, kk] = 1
+        _, acc = _run(dev, t, e, np.ones(1, np.float32), 1.0, sh.SHERRY_KERNEL_GEMV, 1)
+        assert np.array_equal(acc[0], t[:, kk].astype(np.int32))
+    ones = np.ones((1, k), np.int8)
+    _, acc = _run(dev, t, ones, np.ones(1, np.float32), 1.0, sh.SHERRY_KERNEL_GEMV, 1)
+    assert np.array_equal(acc[0], t.astype(np.int32).sum(1))
+
+
+def test_identity_reads_back_t(dev):
+    # X = identity (M = K): acc = T^T, every weight read back through the MFMA path
+    sh = _sh()
+    n, k = 192, 256
+    t = synth.ternary_34(n, k, 38, "id")
+    eye = np.eye(k, dtype=np.int8)
+    _, acc = _run(dev, t, eye, np.ones(k, np.float32), 1.0, sh.SHERRY_KERNEL_MFMA, k)
+    assert np.array_equal(acc, t.T.astype(np.int32))
+
+
+def test_mirror_negates(dev):
+    # flipping every sign bit (code ^ 0x1C) is T -> -T: the product negates
+    sh = _sh()
+    n, k = 128, 512
+    t = synth.ternary_34(n, k, 39, "mir")
+    q = synth.int8_any(2, k, 39, "mir")
+    _, a1 = _run(dev, t, q, np.ones(2, np.float32), 1.0, sh.SHERRY_KERNEL_GEMV, 2)
+    _, a2 = _run(dev, (-t).astype(np.int8), q, np.ones(2, np.float32), 1.0,
+                 sh.SHERRY_KERNEL_GEMV, 2)
+    assert np.array_equal(a1, -a2)
+
+
+def test_extreme_activations(dev):
+    sh = _sh()
+    n, k = 64, 8192
+    t = synth.ternary_34(n, k, 40, "ext")
+    for val in (-128, 127):
+        q = np.full((1, k), val, np.int8)
+        for kern in (sh.SHERRY_KERNEL_GEMV, sh.SHERRY_KERNEL_MFMA):
+            _, acc = _run(dev, t, q, np.ones(1, np.float32), 1.0, kern, 1)
+            assert np.array_equal(acc[0], val * t.astype(np.int32).sum(1))
+
+
+def test_zero_scale_and_no_acc(dev):
+    sh = _sh()
+    n, k = 96, 256
+    t = synth.ternary_34(n, k, 41, "zs")
+    q = synth.int8_any(1, k, 41, "zs")
+    y, _ = _run(dev, t, q, np.zeros(1, np.float32), 0.02, sh.SHERRY_KERNEL_GEMV, 1,
+                with_acc=False)
+    assert np.all(y == 0)
+
+
+def test_guard_bands_and_determinism(dev):
+    sh = _sh()
+    n, k, m = 100, 260, 3
+    t = synth.ternary_34(n, k, 42, "gb")
+    q = synth.int8_any(m, k, 42, "gb")
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    qd = torch.from_numpy(q).to(dev)
+    sx = torch.ones(m, dtype=torch.float32, device=dev)
+    pad = 256
+    for kern in (sh.SHERRY_KERNEL_GEMV, sh.SHERRY_KERNEL_MFMA):
+        ybuf = torch.full((m * n + 2 * pad,), 12345.0, dtype=torch.float32, device=dev)
+        abuf = torch.full((m * n + 2 * pad,), 777, dtype=torch.int32, device=dev)
+        y = ybuf[pad:pad + m * n]
+        a = abuf[pad:pad + m * n]
+        outs = []
+        for _ in range(3):
+            sh.sherry_gemm_ex(w, qd, sx, 1.0, y, a, m, n, k, kern)
+            torch.cuda.synchronize()
+            outs.append(a.cpu().numpy().copy())
+        yb, ab = ybuf.cpu().numpy(), abuf.cpu().numpy()
+        assert np.all(yb[:pad] == 12345.0) and np.all(yb[pad + m * n:] == 12345.0)
+        assert np.all(ab[:pad] == 777) and np.all(ab[pad + m * n:] == 777)
+        assert all(np.array_equal(outs[0], o) for o in outs[1:])
+        assert np.array_equal(outs[0].reshape(m, n), oracle.gemm_i32(q, t))
+
+
+# ---------------------------------------------------------- batched decode
+
+def _batched(dev, shapes, seed, want_acc=True):
+    sh = _sh()
+    descs = (sh.sherry_gemv_desc * len(shapes))()
+    keep, refs = [], []
+    for i, (n, k) in enumerate(shapes):
+        t = synth.ternary_34(n, k, seed, "b", i)
+        q = synth.int8_any(1, k, seed, "b", i)
+        sx = np.array([0.01 * (i + 1)], np.float32)
+        sw = synth.weight_scale(seed, "b", i)
+        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        qd = torch.from_numpy(q).to(dev)
+        sxd = torch.from_numpy(sx).to(dev)
+        y = torch.full((n,), float("nan"), dtype=torch.float32, device=dev)
+        a = torch.full((n,), -9, dtype=torch.int32, device=dev) if want_acc else None
+        keep += [w, qd, sxd, y, a]
+        d = descs[i]
+        d.w, d.x, d.x_scale, d.y = w.data_ptr(), qd.data_ptr(), sxd.data_ptr(), y.data_ptr()
+        d.acc = a.data_ptr() if want_acc else None
+        d.n, d.k, d.w_scale = n, k, sw
+        refs.append((t, q, sx, sw, y, a))
+    total = sh.sherry_gemv_batched_prepare(descs)
+    ddev = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+    sh.sherry_gemv_batched(ddev, len(shapes), total)
+    torch.cuda.synchronize()
+    return refs
+
+
+def test_batched_gemv_parity(dev):
+    _say("batched small")
+    shapes = [(64, 128), (65, 132), (2048, 2048), (512, 2048), (300, 8192), (1, 4), (70, 1032)]
+    for t, q, sx, sw, y, a in _batched(dev, shapes, 43):
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a.cpu().numpy(), acc_ref[0])
+        assert _y_ok(y.cpu().numpy(), oracle.epilogue(acc_ref, sx, sw)[0])
+
+
+def test_batched_decode_step_llama_1b(dev):
+    # one decode step of LLaMA-3.2-1B linear layers (16 layers x 7 shapes), in
+    # the grouped launch the benchmark times; checked on sampled rows
+    _say("batched llama-1b step")
+    spec = synth.LLAMA_1B
+    shapes = [(lin.n, lin.k) for _, lin in synth.model_linears(spec)]
+    refs = _batched(dev, shapes, 44)
+    rng = np.random.default_rng(1)
+    for t, q, sx, sw, y, a in refs:
+        acc = a.cpu().numpy()
+        yy = y.cpu().numpy()
+        rows = rng.integers(0, t.shape[0], 24)
+        for j in rows:
+            r = oracle.dot_i32(q[0], t[j])
+            assert acc[j] == r
+            yr = oracle.epilogue(np.array([[r]], np.int32), sx, sw)[0, 0]
+            assert abs(float(yy[j]) - yr) <= RTOL * abs(yr)
+
+
+# ---------------------------------------------------------- 2-bit reference
+
+@pytest.mark.parametrize("n,k", [(64, 64), (65, 68), (300, 2048), (128, 4100)])
+def test_gemv2_parity(dev, n, k):
+    sh = _sh()
+    t = synth.ternary_any(n, k, 45, "g2", n, k)
+    q = synth.int8_any(1, k, 45, "g2", n, k)
+    w2 = torch.from_numpy(sh.sherry_pack2(t)).to(dev)
+    qd = torch.from_numpy(q).to(dev)
+    sx = torch.full((1,), 0.5, dtype=torch.float32, device=dev)
+    y = torch.empty(n, dtype=torch.float32, device=dev)
+    a = torch.empty(n, dtype=torch.int32, device=dev)
+    sh.sherry_gemv2(w2, qd, sx, 0.25, y, a, n, k)
+    torch.cuda.synchronize()
+    acc_ref = oracle.gemm_i32(q, t)[0]
+    assert np.array_equal(a.cpu().numpy(), acc_ref)
+    assert np.array_equal(y.cpu().numpy().astype(np.float64), acc_ref * 0.125)
+
+
+def test_stream_read_checksum(dev):
+    sh = _sh()
+    nbytes = 3 * 256 * 1024 + 4096
+    src = torch.randint(0, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, device=dev)
+    groups = sh.sherry_stream_read_groups(nbytes)
+    sink = torch.empty(groups, dtype=torch.int32, device=dev)
+    sh.sherry_stream_read(src, nbytes, sink)
+    torch.cuda.synchronize()
+    h = src.cpu().numpy().view(np.uint32)
+    per = 256 * 1024 // 4
+    ref = [np.bitwise_xor.reduce(h[g * per:(g + 1) * per]) for g in range(groups)]
+    assert np.array_equal(sink.cpu().numpy().view(np.uint32), np.array(ref, np.uint32))
