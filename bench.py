@@ -99,7 +99,7 @@ class DecodeStep:
             ddev = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
             self.copies.append(dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total))
         torch.cuda.synchronize()
-        self.total_tiles = self.copies[0]["total"]
+        self.total_blocks = self.copies[0]["total"]
         self.weight_bytes = sum(sh.sherry_packed_bytes(l.n, l.k) for _, l in self.lins)
         # algorithmic bytes of one grouped product launch: packed weights,
         # int8 x, its fp32 scale, fp32 y
@@ -254,6 +254,10 @@ def main():
     ap.add_argument("--seed", type=int, default=synth.DEFAULT_SEED)
     ap.add_argument("--no-extra", action="store_true", help="skip the M=2048 GEMM and ceiling")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--only", choices=["decode"], default=None,
+                    help="run only the timed decode step (for counter passes)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="run 10 plain device copies of BYTES and exit (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -266,6 +270,19 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     log(sh.sherry_version(), torch.cuda.get_device_name(dev))
+
+    if args.copy_probe:
+        n = args.copy_probe // 4 * 4
+        src = torch.ones(n // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "launches": 10}), flush=True)
+        return
+    if args.only:
+        args.no_extra = args.no_cpu = True
 
     step = DecodeStep(sh, torch, dev, synth.LLAMA_1B, args.seed)
     ms_step, gemv_ms_mean, gemv_ms_med, wall = bench_decode(step, torch, args.steps, args.warmup)

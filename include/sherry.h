@@ -163,20 +163,23 @@ typedef struct sherry_gemv_desc {
   int32_t* acc;          /* device, int32 [n] or NULL                      */
   int64_t n, k;
   float w_scale;
-  int32_t tile_begin;    /* written by sherry_gemv_batched_prepare         */
+  int32_t block_begin;   /* written by sherry_gemv_batched_prepare         */
 } sherry_gemv_desc;
 
-/* Host: validates descs[0..count) and fills each tile_begin (prefix sum of
- * ceil(n/64)); *total_tiles receives the sum.  count >= 1. */
+/* Host: validates descs[0..count) and fills each block_begin, the index of
+ * the first workgroup of that product (a product of n rows and k columns
+ * takes ceil(ceil(n/64) * S / 4) workgroups, S = 1, 2 or 4 waves per 64-row
+ * tile as k grows past 3071 and 6143); *total_blocks receives the sum.
+ * count >= 1. */
 int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
-                                int64_t* total_tiles);
+                                int64_t* total_blocks);
 
 /* Runs every GEMV of descs_dev (device, a byte copy of an array accepted by
  * sherry_gemv_batched_prepare, 8-byte aligned) in one launch.  count and
- * total_tiles must be the values used with / returned by prepare; the device
- * descriptors cannot be re-validated here. */
+ * total_blocks must be the values used with / returned by prepare; the
+ * device descriptors cannot be re-validated here. */
 int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
-                        int64_t total_tiles, void* stream);
+                        int64_t total_blocks, void* stream);
 
 /* ---------------------------------------------------------------------- */
 /* 2-bit reference layout (the "2-bit strategy" of Sec. 2.3): one ternary  */

@@ -50,7 +50,7 @@ class sherry_gemv_desc(ctypes.Structure):
     _fields_ = [
         ("w", ctypes.c_void_p), ("x", ctypes.c_void_p), ("x_scale", ctypes.c_void_p),
         ("y", ctypes.c_void_p), ("acc", ctypes.c_void_p), ("n", ctypes.c_int64),
-        ("k", ctypes.c_int64), ("w_scale", ctypes.c_float), ("tile_begin", ctypes.c_int32),
+        ("k", ctypes.c_int64), ("w_scale", ctypes.c_float), ("block_begin", ctypes.c_int32),
     ]
 
 
@@ -211,16 +211,16 @@ def sherry_gemm_kernel_for(m: int, n: int, k: int) -> int:
 
 
 def sherry_gemv_batched_prepare(descs) -> int:
-    """Fills tile_begin of a ctypes array of sherry_gemv_desc; returns total tiles."""
+    """Fills block_begin of a ctypes array of sherry_gemv_desc; returns total blocks."""
     total = ctypes.c_int64(0)
     _check(lib.sherry_gemv_batched_prepare(descs, len(descs), ctypes.byref(total)),
            "sherry_gemv_batched_prepare")
     return int(total.value)
 
 
-def sherry_gemv_batched(descs_dev, count: int, total_tiles: int, stream=None):
+def sherry_gemv_batched(descs_dev, count: int, total_blocks: int, stream=None):
     """descs_dev: device uint8 tensor holding a byte copy of prepared descriptors."""
-    _check(lib.sherry_gemv_batched(_ptr(descs_dev), count, total_tiles, _stream(stream)),
+    _check(lib.sherry_gemv_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
            "sherry_gemv_batched")
 
 

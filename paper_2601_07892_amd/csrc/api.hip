@@ -106,28 +106,29 @@ extern "C" int sherry_gemv(const uint8_t* w, const int8_t* x, const float* x_sca
 }
 
 extern "C" int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
-                                           int64_t* total_tiles) {
-  if (!descs || !total_tiles || count < 1) return SHERRY_E_INVALID;
-  int64_t tiles = 0;
+                                           int64_t* total_blocks) {
+  if (!descs || !total_blocks || count < 1) return SHERRY_E_INVALID;
+  int64_t blocks = 0;
   for (int i = 0; i < count; ++i) {
     sherry_gemv_desc& d = descs[i];
     int st = check_product(d.w, d.x, d.x_scale, d.y, 1, d.n, d.k, 4);
     if (st != SHERRY_OK) return st;
     if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
-    d.tile_begin = static_cast<int32_t>(tiles);
-    tiles += ceil_div(d.n, kTileRows);
-    if (tiles > INT32_MAX) return SHERRY_E_SHAPE;
+    d.block_begin = static_cast<int32_t>(blocks);
+    const int S = gemv_split(static_cast<int>(ceil_div(d.k, kTileK)));
+    blocks += ceil_div(ceil_div(d.n, kTileRows) * S, 4);
+    if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
   }
-  *total_tiles = tiles;
+  *total_blocks = blocks;
   return SHERRY_OK;
 }
 
 extern "C" int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
-                                   int64_t total_tiles, void* stream) {
-  if (!descs_dev || count < 1 || total_tiles < 1 || total_tiles > INT32_MAX)
+                                   int64_t total_blocks, void* stream) {
+  if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
     return SHERRY_E_INVALID;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
-  return launch_gemv_batched(descs_dev, count, total_tiles, as_stream(stream));
+  return launch_gemv_batched(descs_dev, count, total_blocks, as_stream(stream));
 }
 
 extern "C" int sherry_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,

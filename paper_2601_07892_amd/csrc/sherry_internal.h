@@ -23,6 +23,10 @@ constexpr int kUnit2Bytes = 1024;
 
 constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Waves that share one 64-row tile in the decode kernel, for C containers
+// per row: about 16 containers per wave, at most 4 waves (one workgroup).
+__host__ __device__ constexpr int gemv_split(int C) { return C >= 48 ? 4 : (C >= 24 ? 2 : 1); }
+
 // Decoded weights of a 5-bit code as a little-endian int8x4 word (byte p =
 // weight at block position p: +1 -> 0x01, -1 -> 0xFF, 0 -> 0x00).  The code
 // is z | s0<<2 | s1<<3 | s2<<4: z = zero position, si = sign bit of the i-th
@@ -56,6 +60,11 @@ __host__ __device__ constexpr uint32_t decode_word(uint32_t code) {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Word 3 of a raw buffer resource on gfx9-family GPUs (untyped 32-bit data,
+// no swizzle): address = base + voffset + soffset + imm, bounded by the
+// resource's byte count.
+constexpr int kBufferWord3 = 0x00020000;
+
 template <class T>
 __device__ __forceinline__ const SHERRY_CONST T* as_const(const T* p) {
   return (const SHERRY_CONST T*)(p);
@@ -79,7 +88,7 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
                      int64_t n, int64_t k, hipStream_t s);
 
 int launch_gemv_batched(const sherry_gemv_desc* descs, int count,
-                        int64_t total_tiles, hipStream_t s);
+                        int64_t total_blocks, hipStream_t s);
 
 int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale,
                      float w_scale, float* y, int32_t* acc, int64_t m,

@@ -186,9 +186,10 @@ def test_batched_prepare():
         descs[i].k = k
         descs[i].w_scale = 0.02
     total = sh.sherry_gemv_batched_prepare(descs)
-    begins = [d.tile_begin for d in descs]
-    assert begins == [0, 32, 40, 168, 200]
-    assert total == 202
+    begins = [d.block_begin for d in descs]
+    # tiles x waves-per-tile / 4: (32*1)/4, (8*1)/4, (128*1)/4, (32*4)/4, (2*1)/4
+    assert begins == [0, 8, 10, 42, 74]
+    assert total == 75
     assert ctypes.sizeof(sh.sherry_gemv_desc) == 64
     descs[3].k = 6
     with pytest.raises(sh.SherryError):

@@ -57,7 +57,8 @@ def _run(dev, t, q, sx, sw, kernel, m, with_acc=True, packed=None):
 # ---------------------------------------------------------------- quantizer
 
 @pytest.mark.parametrize("m,k,outl", [(1, 4, 0.0), (3, 1000, 0.0), (7, 2048, 0.01),
-                                      (64, 8192, 0.01), (2048, 3072, 0.01)])
+                                      (64, 8192, 0.01), (2048, 3072, 0.01), (5, 14336, 0.01),
+                                      (3, 16388, 0.0), (2, 40000, 0.01)])
 def test_quantize_bit_exact(dev, m, k, outl):
     sh = _sh()
     _say("quantize", m, k, outl)
@@ -289,6 +290,18 @@ def test_batched_gemv_parity(dev):
     _say("batched small")
     shapes = [(64, 128), (65, 132), (2048, 2048), (512, 2048), (300, 8192), (1, 4), (70, 1032)]
     for t, q, sx, sw, y, a in _batched(dev, shapes, 43):
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a.cpu().numpy(), acc_ref[0])
+        assert _y_ok(y.cpu().numpy(), oracle.epilogue(acc_ref, sx, sw)[0])
+
+
+def test_batched_split_paths(dev):
+    # K chosen so that the tiles are split over 1, 2 and 4 waves, with uneven
+    # and partial last containers
+    _say("batched split paths")
+    shapes = [(3072, 3072), (1024, 3072), (130, 3076), (200, 6140), (64, 6148), (100, 8196),
+              (65, 14336), (3, 4)]
+    for t, q, sx, sw, y, a in _batched(dev, shapes, 46):
         acc_ref = oracle.gemm_i32(q, t, threads=8)
         assert np.array_equal(a.cpu().numpy(), acc_ref[0])
         assert _y_ok(y.cpu().numpy(), oracle.epilogue(acc_ref, sx, sw)[0])
