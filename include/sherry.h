@@ -167,9 +167,9 @@ typedef struct sherry_gemv_desc {
 } sherry_gemv_desc;
 
 /* Host: validates descs[0..count) and fills each block_begin, the index of
- * the first workgroup of that product (a product of n rows and k columns
- * takes ceil(ceil(n/64) * S / 4) workgroups, S = 1, 2 or 4 waves per 64-row
- * tile as k grows past 3071 and 6143); *total_blocks receives the sum.
+ * the first workgroup of that product, and *total_blocks with their sum
+ * (the number of workgroups depends on n and k through the library's work
+ * split; descriptors only need to be prepared again if n or k change).
  * count >= 1. */
 int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
                                 int64_t* total_blocks);

@@ -116,7 +116,7 @@ extern "C" int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
     if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
     const int S = gemv_split(static_cast<int>(ceil_div(d.k, kTileK)));
-    blocks += ceil_div(ceil_div(d.n, kTileRows) * S, 4);
+    blocks += ceil_div(ceil_div(d.n, kTileRows) * S, kGemvWaves);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
   }
   *total_blocks = blocks;

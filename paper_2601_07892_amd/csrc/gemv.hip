@@ -1,22 +1,23 @@
 // Decode-path product for M <= 4 tokens (online phase of Appendix A, Eq. 2).
 //
-// Work mapping.  A workgroup is 4 waves; lane i of a wave owns row 64*r + i
-// of one 64-row tile r, so the activations of a container (128 weights) are
-// the same for the whole wave and live in SGPRs (scalar loads).  Each tile's
-// containers are split among S = gemv_split(C) waves (1, 2 or 4, so that a
-// wave streams about 16 containers); a workgroup covers 4/S tiles and its
-// waves combine their int32 partial sums through LDS.
+// Work mapping.  A workgroup is kGemvWaves waves; lane i of a wave owns row
+// 64*r + i of one 64-row tile r, so the activations of a container (128
+// weights) are the same for the whole wave and are read with scalar loads
+// into SGPRs.
+// Each tile's containers are split among S = gemv_split(C) waves (a power of
+// two, so that a wave streams a few containers); a workgroup covers
+// kGemvWaves/S tiles and its waves combine their int32 partial sums through
+// LDS.
 //
 // Streaming.  A container is two contiguous wave-wide loads: the 64 rows'
-// 16-byte heads (1 KB) and 4-byte tails (256 B).  Each wave double-buffers
-// two register sets of kSet containers: one set is in flight while the
-// other is decoded.
+// 16-byte heads (1 KB) and 4-byte tails (256 B).  Each wave keeps a ring of
+// kRing containers in registers, refilling each slot as soon as it has been
+// decoded.
 //
 // Decode.  Per code: a funnel shift and mask (or one SDWA mask) give code*4,
 // one LDS read of the 32-entry table gives the int8x4 weights, one v_dot4 per
 // token accumulates x . w in int32.  The table holds one dword per code, so
-// any 64 lookups are free of bank conflicts; codes are processed in groups
-// so 8 or 16 table reads are in flight.
+// any 64 lookups are free of bank conflicts.
 #include <utility>
 
 #include "sherry_internal.h"
@@ -24,8 +25,8 @@
 namespace sherry {
 namespace {
 
-constexpr int kGemvThreads = 256;
-constexpr int kSet = 4;  // containers per register set (two sets per wave)
+constexpr int kGemvThreads = 64 * kGemvWaves;
+constexpr int kRing = 3;  // containers per wave held in the register ring
 
 // Byte offset (code*4) of code j of a 160-bit container held in d[0..4].
 template <int j>
@@ -96,92 +97,75 @@ __device__ __forceinline__ void dot_container(const uint32_t (&d)[5],
   }
 }
 
-// Container c of a tile through a buffer resource spanning exactly that
-// tile's containers (reads outside it return zero, never fault): 16-byte
-// head at lane*16, 4-byte tail at 1024 + lane*4, container offset in SGPRs.
+// Activation source: the activation words of container c, read with scalar
+// loads (wave-uniform) into SGPRs; dot masks the words past K of a partial
+// last container.
+template <int M>
+struct XFromSgpr {
+  const SHERRY_CONST int32_t* xw0;  // [M][k/4] words in global memory
+  int k;
+  __device__ __forceinline__ void dot_full(const uint32_t (&d)[5], int c, const uint32_t* lut,
+                                           int32_t (&acc)[M]) const {
+    dot_container<M, false>(d, xw0 + c * (kTileK / 4), k >> 2, 32, lut, acc);
+  }
+  __device__ __forceinline__ void dot(const uint32_t (&d)[5], int c, const uint32_t* lut,
+                                      int32_t (&acc)[M]) const {
+    const int kb = c * kTileK;
+    if (kb + kTileK <= k) dot_full(d, c, lut, acc);
+    else dot_container<M, true>(d, xw0 + (kb >> 2), k >> 2, (k - kb) >> 2, lut, acc);
+  }
+};
+
+// Container c through a buffer resource spanning a wave's containers (reads
+// outside it return zero and never fault): 16-byte head at lane*16, 4-byte
+// tail at 1024 + lane*4, container offset in SGPRs.
 __device__ __forceinline__ void load_container(uint32_t (&d)[5], __amdgpu_buffer_rsrc_t r,
                                                int c, int lane) {
-  const u32x4 h = __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, c * kUnitBytes, 0);
+  const u32x4 h =
+      __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, c * kUnitBytes, kLoadStream);
   d[0] = h.x;
   d[1] = h.y;
   d[2] = h.z;
   d[3] = h.w;
-  d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, c * kUnitBytes, 0);
+  d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, c * kUnitBytes,
+                                              kLoadStream);
 }
 
-template <int P>
-__device__ __forceinline__ void load_set(uint32_t (&d)[P][5], __amdgpu_buffer_rsrc_t r, int c,
-                                         int lane) {
-#pragma unroll
-  for (int u = 0; u < P; ++u) load_container(d[u], r, c + u, lane);
-}
-
-template <int M>
-__device__ __forceinline__ void dot_any(const uint32_t (&d)[5], int cc,
-                                        const SHERRY_CONST int32_t* xw0, int k,
-                                        const uint32_t* lut, int32_t (&acc)[M]) {
-  const int kb = cc * kTileK;
-  if (kb + kTileK <= k) dot_container<M, false>(d, xw0 + (kb >> 2), k >> 2, 32, lut, acc);
-  else dot_container<M, true>(d, xw0 + (kb >> 2), k >> 2, (k - kb) >> 2, lut, acc);
-}
-
-template <int M, int P>
-__device__ __forceinline__ void dot_set(const uint32_t (&d)[P][5], int c,
-                                        const SHERRY_CONST int32_t* xw0, int kw,
-                                        const uint32_t* lut, int32_t (&acc)[M]) {
-#pragma unroll
-  for (int u = 0; u < P; ++u)
-    dot_container<M, false>(d[u], xw0 + (c + u) * (kTileK / 4), kw, 32, lut, acc);
-}
-
-// Streams containers [c0, c1) of one tile with two register sets of kSet
-// containers: set B is loaded while set A is decoded and the reverse, so
-// kSet containers are always in flight.  Sets only cover full containers
-// [c0, cf): cf excludes a partial last container at the end of K.  Every
-// set load is issued only after checking it lies in [c0, cf); at the top of
-// the loop the outstanding loads are always exactly set A's, so the compiler
-// waits on exact counts.  What is left (fewer than kSet containers, and the
-// partial one) is drained one container at a time.
-template <int M>
-__device__ __forceinline__ void stream_tile(__amdgpu_buffer_rsrc_t tile, int c0, int c1,
-                                            const SHERRY_CONST int32_t* xw0, int k,
-                                            const uint32_t* lut, int32_t (&acc)[M]) {
+// Streams containers [c0, c1) of one tile through a ring of kRing register
+// slots: slot u is decoded and immediately refilled with the container kRing
+// ahead, so kRing - 1 containers are always in flight.  The resource r spans
+// exactly [c0, c1) (container indices are relative to c0): refills past the
+// end are issued unconditionally and read zeros without touching memory,
+// which keeps the outstanding loads identical on every path so the compiler
+// waits on exact counts; only the decode is skipped past the end.
+template <int M, class X>
+__device__ __forceinline__ void stream_tile(__amdgpu_buffer_rsrc_t r, int c0, int c1,
+                                            const X& xsrc, const uint32_t* lut,
+                                            int32_t (&acc)[M]) {
   const int lane = threadIdx.x & 63;
-  const int kw = k >> 2;
-  const int cf = (c1 * kTileK > k) ? c1 - 1 : c1;
-  uint32_t a[kSet][5], b[kSet][5];
-  int c = c0;
-  if (c + kSet <= cf) {
-    load_set<kSet>(a, tile, c, lane);
-    while (true) {
-      // set A holds [c, c + kSet), inside [c0, cf)
-      if (c + 2 * kSet <= cf) {
-        load_set<kSet>(b, tile, c + kSet, lane);
-        dot_set<M, kSet>(a, c, xw0, kw, lut, acc);
-        if (c + 3 * kSet <= cf) {
-          load_set<kSet>(a, tile, c + 2 * kSet, lane);
-          dot_set<M, kSet>(b, c + kSet, xw0, kw, lut, acc);
-          c += 2 * kSet;
-          continue;
-        }
-        dot_set<M, kSet>(b, c + kSet, xw0, kw, lut, acc);
-        c += 2 * kSet;
-        break;
-      }
-      dot_set<M, kSet>(a, c, xw0, kw, lut, acc);
-      c += kSet;
-      break;
-    }
+  const int n = c1 - c0;
+  uint32_t ring[kRing][5];
+  // issue the slots strictly in order (head and tail of slot 0 first), so
+  // that slot u's loads are always the oldest outstanding ones when it is
+  // decoded
+#pragma unroll
+  for (int u = 0; u < kRing; ++u) {
+    load_container(ring[u], r, u, lane);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  for (; c < c1; ++c) {
-    uint32_t d[5];
-    load_container(d, tile, c, lane);
-    dot_any<M>(d, c, xw0, k, lut, acc);
+  for (int i = 0; i < n; i += kRing) {
+#pragma unroll
+    for (int u = 0; u < kRing; ++u) {
+      if (i + u < n) xsrc.dot(ring[u], c0 + i + u, lut, acc);
+      __builtin_amdgcn_sched_barrier(0);
+      load_container(ring[u], r, i + u + kRing, lane);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 }
 
 // One workgroup of a product: block g of a problem whose tiles are split
-// over S waves each.
+// over S waves each.  lut and red are LDS; the caller has filled lut.
 template <int M>
 __device__ __forceinline__ void gemv_block(const uint8_t* w_, const int8_t* x_,
                                            const float* x_scale, float w_scale, float* y,
@@ -191,20 +175,20 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const int8_t* x_,
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int C = (k + kTileK - 1) / kTileK;
   const int R = static_cast<int>((n + kTileRows - 1) / kTileRows);
-  const int tpb = 4 / S;           // tiles per block
+  const int tpb = kGemvWaves / S;  // tiles per block
   const int lt = wave / S;         // tile of this wave inside the block
   const int part = wave - lt * S;  // part of the tile's containers
   const int r = g * tpb + lt;
-
   int32_t acc[M];
 #pragma unroll
   for (int m = 0; m < M; ++m) acc[m] = 0;
   if (r < R) {
     const int c0 = (part * C) / S, c1 = ((part + 1) * C) / S;
-    const __amdgpu_buffer_rsrc_t tile = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint8_t*>(w_) + int64_t(r) * C * kUnitBytes, 0, C * kUnitBytes,
-        kBufferWord3);
-    stream_tile<M>(tile, c0, c1, as_const(reinterpret_cast<const int32_t*>(x_)), k, lut, acc);
+    const __amdgpu_buffer_rsrc_t range = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(w_) + (int64_t(r) * C + c0) * kUnitBytes, 0,
+        (c1 - c0) * kUnitBytes, kBufferWord3);
+    stream_tile<M>(range, c0, c1,
+                   XFromSgpr<M>{as_const(reinterpret_cast<const int32_t*>(x_)), k}, lut, acc);
   }
 
 #pragma unroll
@@ -228,7 +212,6 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const int8_t* x_,
 
 __device__ __forceinline__ void fill_lut(uint32_t* lut) {
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
-  __syncthreads();
 }
 
 template <int M>
@@ -237,7 +220,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(
     const float* __restrict__ x_scale, float w_scale, float* __restrict__ y,
     int32_t* __restrict__ acc, int64_t n, int64_t k, int split) {
   __shared__ uint32_t lut[32];
-  __shared__ int32_t red[4 * M * 64];
+  __shared__ int32_t red[kGemvWaves * M * 64];
   fill_lut(lut);
   gemv_block<M>(w, x, x_scale, w_scale, y, acc, n, static_cast<int>(k), blockIdx.x, split, lut,
                 red);
@@ -246,15 +229,24 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(
 __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
     const sherry_gemv_desc* __restrict__ descs, int count) {
   __shared__ uint32_t lut[32];
-  __shared__ int32_t red[4 * 64];
+  __shared__ int32_t red[kGemvWaves * 64];
   fill_lut(lut);
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
-  int lo = 0, hi = count - 1;  // last descriptor with block_begin <= blk
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (descs[mid].block_begin <= blk) lo = mid;
-    else hi = mid - 1;
+  // last descriptor with block_begin <= blk: block_begin strictly increases,
+  // so the descriptors that qualify form a prefix; each lane tests one
+  // descriptor and the prefix length comes from a ballot (one load round
+  // trip per 64 descriptors instead of a chain of dependent loads)
+  const int lane = threadIdx.x & 63;
+  int lo = 0;
+  for (int base = 0; base < count; base += 64) {
+    const int i = base + lane;
+    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
+    const uint64_t m = __ballot(ok);
+    const int len = __popcll(m);
+    lo = base + len - 1;
+    if (len < 64) break;
   }
+  lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemv_desc& d = descs[lo];
   const int k = static_cast<int>(d.k);
   const int S = gemv_split(static_cast<int>((k + kTileK - 1) / kTileK));
@@ -269,9 +261,9 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale, fl
   const int64_t R = ceil_div(n, kTileRows);
   const int C = static_cast<int>(ceil_div(k, kTileK));
   // a lone launch has only this product to fill the GPU: split every tile
-  // over 4 waves unless there are plenty of tiles
-  const int S = (R * gemv_split(C) >= 2048) ? gemv_split(C) : 4;
-  const dim3 grid(static_cast<unsigned>(ceil_div(R * S, 4)));
+  // over all waves of a workgroup unless there are plenty of tiles
+  const int S = (R * gemv_split(C) >= 4096) ? gemv_split(C) : kGemvWaves;
+  const dim3 grid(static_cast<unsigned>(ceil_div(R * S, kGemvWaves)));
   const dim3 block(kGemvThreads);
   switch (m) {
     case 1: return launch(gemv_kernel<1>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, n, k, S);

