@@ -149,13 +149,28 @@ def bench_decode(step: DecodeStep, torch, steps, warmup):
     return total_ms / steps, float(np.mean(gemv_ms)), float(np.median(gemv_ms)), wall
 
 
+def heat(sh, torch, dev, seconds=0.03):
+    """Brings the GPU to its steady loaded state before a timed loop (the
+    first few milliseconds of sustained HBM load run slower): repeated
+    streaming reads of 1 GiB, a different kernel from the ones timed."""
+    nbytes = 1 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    sink = torch.empty(sh.sherry_stream_read_groups(nbytes), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            sh.sherry_stream_read(src, nbytes, sink)
+        torch.cuda.synchronize()
+    del src, sink
+
+
 def bench_product_only(step: DecodeStep, torch, launches):
     """Average duration of the grouped product kernel alone: back-to-back
     launches over the rotated copies, one event pair around the whole run, so
     that per-launch event overhead does not enter the figure."""
     ncp = len(step.copies)
-    for i in range(ncp):
-        step.gemv(i)
+    heat(step.sh, torch, step.dev)
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -276,8 +291,11 @@ def main():
                     help="rotated weight copies (working set = copies x 152 MB)")
     ap.add_argument("--no-extra", action="store_true", help="skip the M=2048 GEMM and ceiling")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--only", choices=["decode"], default=None,
-                    help="run only the timed decode step (for counter passes)")
+    ap.add_argument("--only", choices=["decode", "product"], default=None,
+                    help="run only the timed decode steps, or only the back-to-back "
+                         "product launches (for profiler runs)")
+    ap.add_argument("--product-launches", type=int, default=1000,
+                    help="back-to-back grouped product launches timed for the roofline")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="run 10 plain device copies of BYTES and exit (counter calibration)")
     args = ap.parse_args()
@@ -307,8 +325,20 @@ def main():
         args.no_extra = args.no_cpu = True
 
     step = DecodeStep(sh, torch, dev, synth.LLAMA_1B, args.seed, copies=args.copies)
+    if args.only == "product":
+        kern_ms = bench_product_only(step, torch, args.product_launches)
+        log("grouped product %.2f us back to back over %d launches" %
+            (kern_ms * 1e3, args.product_launches))
+        print(json.dumps({"kernel": "gemv_batched_kernel", "launches": args.product_launches,
+                          "avg_launch_us": round(kern_ms * 1e3, 3),
+                          "bytes_per_launch": step.gemv_bytes}), flush=True)
+        return
+    heat(sh, torch, dev)
     ms_step, gemv_ms_mean, gemv_ms_med, wall = bench_decode(step, torch, args.steps, args.warmup)
-    kern_ms = bench_product_only(step, torch, args.steps)
+    if args.only == "decode":
+        log("step %.2f us" % (ms_step * 1e3))
+        return
+    kern_ms = bench_product_only(step, torch, args.product_launches)
     step_bytes = step.gemv_bytes + step.quant_bytes
     value = step_bytes / (ms_step * 1e-3) / 1e9
     achieved = step.gemv_bytes / (kern_ms * 1e-3) / 1e9
