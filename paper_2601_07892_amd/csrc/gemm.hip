@@ -2,15 +2,20 @@
 // per workgroup into an int8 tile in LDS and multiplied with int8 MFMA.
 //
 // Per K-step of 128 (one unit column of the packed layout):
-//  - X tile  BM x 128 int8: 16-byte global loads, written to LDS;
-//  - T tile  BN x 128: BN/64 units of 1280 bytes; each thread decodes 32/TPR
-//    codes of one row through the 32-entry table and writes int8 to LDS;
-//  - 4 waves, each owning a (BM/WGM) x (BN/WGN) block of C made of 32x32
+//  - X tile  BM x 128 int8: 16-byte buffer loads, written to LDS as is;
+//  - T tile  BN x 128: BN/64 units of 1280 bytes; the PARTS threads of a T
+//    row each decode 32/PARTS of its codes through the 32-entry table and
+//    write int8x4 words to LDS;
+//  - the waves, each owning a (BM/WGM) x (BN/WGN) block of C made of 32x32
 //    fragments, run v_mfma_i32_32x32x32_i8 over four 32-wide k slices.
+// LDS holds two stages of [X tile | T tile]: while the MFMAs of step s read
+// one stage, the registers loaded during step s-1 are written into the other
+// and the loads of step s+2 are issued, so there is one barrier per step and
+// every global load has a whole step to land.  Eight waves (two per SIMD)
+// let one wave's decode and LDS traffic overlap the other's MFMAs.
 // LDS rows are 128 bytes; 16-byte chunk c of row r lives at chunk c ^ (r&7),
 // so the 8 rows read by any 8 lanes of a fragment load hit 8 distinct chunk
-// positions (all 32 banks once).  Global loads for step s+1 are issued before
-// the MFMAs of step s (register double buffering).
+// positions (all 32 banks once).
 #include "sherry_internal.h"
 
 namespace sherry {
@@ -19,45 +24,60 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int kGemmThreads = 256;
 constexpr int kBK = 128;
+constexpr int kLutBytes = 128;
 
-template <int BM_, int BN_, int WGM_, int WGN_>
+template <int BM_, int BN_, int WGM_, int WGN_, int THREADS_>
 struct GemmCfg {
-  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
-  static_assert(WGM * WGN == 4, "4 waves per workgroup");
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, THREADS = THREADS_;
+  static_assert(WGM * WGN * 64 == THREADS, "one wave per C block");
   static constexpr int WM = BM / WGM, WN = BN / WGN;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "32x32 fragments");
   static constexpr int FM = WM / 32, FN = WN / 32;
-  static constexpr int XPT = BM * 8 / kGemmThreads;  // 16-byte X chunks per thread
-  static_assert(XPT >= 1 && BM * 8 % kGemmThreads == 0, "X tile split");
-  static constexpr int TPR = kGemmThreads / BN;  // threads decoding one T row
-  static_assert(TPR >= 1 && TPR <= 4 && kGemmThreads % BN == 0, "T tile split");
-  static constexpr int CPT = 32 / TPR;           // codes decoded per thread
-  static constexpr int LDS_X = BM * kBK, LDS_W = BN * kBK;
+  static constexpr int XPT = BM * 8 / THREADS;  // 16-byte X chunks per thread
+  static_assert(XPT >= 1 && BM * 8 % THREADS == 0, "X tile split");
+  // threads per T row; each decodes CPP consecutive codes of the row.  BN is
+  // a multiple of 64, so a wave's threads share one part (uniform branch)
+  static constexpr int PARTS = THREADS / BN;
+  static_assert(BN % 64 == 0 && THREADS % BN == 0 && (PARTS == 1 || PARTS == 2 || PARTS == 4),
+                "T tile split");
+  static constexpr int CPP = 32 / PARTS;
+  static constexpr int LDS_X = BM * kBK, LDS_W = BN * kBK, STAGE = LDS_X + LDS_W;
 };
 
 __device__ __forceinline__ int swz(int row, int chunk) { return row * kBK + ((chunk ^ (row & 7)) << 4); }
 
-// code*4 of code j (runtime j) of a container in d[0..4]
-__device__ __forceinline__ uint32_t code_x4_rt(const uint32_t (&d)[5], int j) {
-  const int bit = 5 * j, i = bit >> 5, off = bit & 31;
-  const uint32_t lo = d[i];
-  const uint32_t hi = (i < 4) ? d[i + 1] : d[i];
-  const uint32_t prev = (i > 0) ? d[i - 1] : 0u;
-  if (off >= 2) return __builtin_amdgcn_alignbit(hi, lo, off - 2) & 0x7Cu;
-  return __builtin_amdgcn_alignbit(lo, prev, 30 + off) & 0x7Cu;
+// Decodes codes [j0, j0 + n) (n a multiple of 4) of the row stream in d and
+// writes them as int8 to the T tile row: 16-byte chunk per 4 codes.
+template <int j0, int n>
+__device__ __forceinline__ void decode_codes(const uint32_t (&d)[5], const uint32_t* lut,
+                                             int8_t* ws, int wrow) {
+  if constexpr (n > 0) {
+    uint32_t q[4];
+    q[0] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + code_x4<j0>(d));
+    q[1] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) +
+                                              code_x4<j0 + 1>(d));
+    q[2] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) +
+                                              code_x4<j0 + 2>(d));
+    q[3] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) +
+                                              code_x4<j0 + 3>(d));
+    *reinterpret_cast<uint4*>(ws + swz(wrow, j0 >> 2)) = make_uint4(q[0], q[1], q[2], q[3]);
+    decode_codes<j0 + 4, n - 4>(d, lut, ws, wrow);
+  }
 }
 
-template <class G>
-__global__ __launch_bounds__(kGemmThreads) void gemm_kernel(
+// kFullK: K % 128 == 0, every X chunk of a step is in its row, so all loads
+// are branch-free buffer loads (rows past M and units past N read as zero).
+template <class G, bool kFullK>
+__global__ __launch_bounds__(G::THREADS) void gemm_kernel(
     const uint8_t* __restrict__ w, const int8_t* __restrict__ x,
     const float* __restrict__ x_scale, float w_scale, float* __restrict__ y,
     int32_t* __restrict__ acc_out, int64_t M, int64_t N, int64_t K, int MT, int NT) {
-  __shared__ uint32_t lut[32];
-  __shared__ __attribute__((aligned(16))) int8_t xs[G::LDS_X];
-  __shared__ __attribute__((aligned(16))) int8_t ws[G::LDS_W];
-
+  // LDS: the 32-entry code table at address 0 (table reads then need no base
+  // in their address), then the two stages
+  __shared__ __attribute__((aligned(16))) int8_t lds[kLutBytes + 2 * G::STAGE];
+  uint32_t* lut = reinterpret_cast<uint32_t*>(lds);
+  int8_t* smem = lds + kLutBytes;
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
 
   // tile of this block; XCD-aware: consecutive blocks land on different XCDs,
@@ -77,70 +97,80 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(
   const int64_t C = (K + kBK - 1) / kBK;           // K-steps == unit columns
   const int64_t R = (N + kTileRows - 1) / kTileRows;  // unit rows
 
-  // ---- per-thread load assignment ----
-  // X: chunk q = tid + 256*v -> row q>>3, chunk q&7
-  // T: row wrow = tid / TPR of the tile, part = tid % TPR
-  const int wrow = tid / G::TPR, wpart = tid % G::TPR;
-  const int64_t wunit_row = (n0 + wrow) / kTileRows;  // unit row of this T row
-  const int wi = (int)((n0 + wrow) % kTileRows);
-  const bool wrow_ok = wunit_row < R;
+  // T row of this thread within the tile and its part (wave-uniform)
+  const int wrow = tid % G::BN;
+  const int part = __builtin_amdgcn_readfirstlane(tid / G::BN);
+  const int wi = wrow % kTileRows;  // row within its unit (n0 is a multiple of 64)
 
   uint4 xr[G::XPT];
   uint32_t wd[5];
   const bool k16 = (K % 16) == 0;
 
+  // buffer resources spanning this tile's X rows and T unit rows
+  const int64_t xrows = (M - m0 < G::BM) ? M - m0 : G::BM;
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int8_t*>(x) + m0 * K, 0, static_cast<int>(xrows * K), kBufferWord3);
+  const int64_t u0 = n0 / kTileRows;
+  const int64_t urows = (R - u0 < G::BN / kTileRows) ? R - u0 : G::BN / kTileRows;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(w) + u0 * C * kUnitBytes, 0,
+      static_cast<int>(urows * C * kUnitBytes), kBufferWord3);
+  const int wvo = static_cast<int>((wrow / kTileRows) * C * kUnitBytes);  // unit row in tile
+
   auto load_step = [&](int64_t ks) {
-    const int64_t kb = ks * kBK;
+    const int kb = static_cast<int>(ks * kBK);
 #pragma unroll
     for (int v = 0; v < G::XPT; ++v) {
-      const int q = tid + kGemmThreads * v;
+      const int q = tid + G::THREADS * v;
       const int row = q >> 3, ch = q & 7;
-      const int64_t gm = m0 + row, gk = kb + ch * 16;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (gm < M) {
-        const int8_t* src = x + gm * K + gk;
-        if (k16 && gk + 16 <= K) {
-          val = *reinterpret_cast<const uint4*>(src);
-        } else {
-          uint32_t t4[4] = {0, 0, 0, 0};
+      if constexpr (kFullK) {
+        const u32x4 val = __builtin_amdgcn_raw_buffer_load_b128(
+            xrs, static_cast<int>(row * K) + ch * 16, kb, 0);
+        xr[v] = make_uint4(val.x, val.y, val.z, val.w);
+      } else {
+        const int64_t gm = m0 + row, gk = kb + ch * 16;
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (gm < M) {
+          const int8_t* src = x + gm * K + gk;
+          if (k16 && gk + 16 <= K) {
+            val = *reinterpret_cast<const uint4*>(src);
+          } else {
+            uint32_t t4[4] = {0, 0, 0, 0};
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (gk + 4 * e < K) t4[e] = *reinterpret_cast<const uint32_t*>(src + 4 * e);
-          val = make_uint4(t4[0], t4[1], t4[2], t4[3]);
+            for (int e = 0; e < 4; ++e)
+              if (gk + 4 * e < K) t4[e] = *reinterpret_cast<const uint32_t*>(src + 4 * e);
+            val = make_uint4(t4[0], t4[1], t4[2], t4[3]);
+          }
         }
+        xr[v] = val;
       }
-      xr[v] = val;
     }
-    if (wrow_ok) {
-      const uint8_t* unit = w + (wunit_row * C + ks) * kUnitBytes;
-      const uint4 h = *reinterpret_cast<const uint4*>(unit + 16 * wi);
-      wd[0] = h.x;
-      wd[1] = h.y;
-      wd[2] = h.z;
-      wd[3] = h.w;
-      wd[4] = *reinterpret_cast<const uint32_t*>(unit + kHeadBytes + 4 * wi);
-    } else {
-      wd[0] = wd[1] = wd[2] = wd[3] = wd[4] = 0;
-    }
+    const u32x4 h = __builtin_amdgcn_raw_buffer_load_b128(wrs, wvo + 16 * wi, ks * kUnitBytes, 0);
+    wd[0] = h.x;
+    wd[1] = h.y;
+    wd[2] = h.z;
+    wd[3] = h.w;
+    wd[4] = __builtin_amdgcn_raw_buffer_load_b32(wrs, wvo + kHeadBytes + 4 * wi,
+                                                 ks * kUnitBytes, 0);
   };
 
-  auto store_step = [&]() {
+  // writes the registers of one step into a stage: X as is, T decoded
+  auto store_step = [&](int8_t* stage) {
+    int8_t* xs = stage;
+    int8_t* ws = stage + G::LDS_X;
 #pragma unroll
     for (int v = 0; v < G::XPT; ++v) {
-      const int q = tid + kGemmThreads * v;
+      const int q = tid + G::THREADS * v;
       *reinterpret_cast<uint4*>(xs + swz(q >> 3, q & 7)) = xr[v];
     }
-    // decode this thread's codes: CPT codes = CPT/4 chunks of 16 bytes
-#pragma unroll
-    for (int cc = 0; cc < G::CPT / 4; ++cc) {
-      const int j0 = wpart * G::CPT + cc * 4;
-      uint32_t q4[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t a4 = code_x4_rt(wd, j0 + e);
-        q4[e] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + a4);
-      }
-      *reinterpret_cast<uint4*>(ws + swz(wrow, j0 >> 2)) = make_uint4(q4[0], q4[1], q4[2], q4[3]);
+    if (part == 0) {
+      decode_codes<0, G::CPP>(wd, lut, ws, wrow);
+    } else if constexpr (G::PARTS == 2) {
+      decode_codes<16, 16>(wd, lut, ws, wrow);
+    } else if constexpr (G::PARTS == 4) {
+      if (part == 1) decode_codes<8, 8>(wd, lut, ws, wrow);
+      else if (part == 2) decode_codes<16, 8>(wd, lut, ws, wrow);
+      else decode_codes<24, 8>(wd, lut, ws, wrow);
     }
   };
 
@@ -150,14 +180,11 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(
 #pragma unroll
     for (int bb = 0; bb < G::FN; ++bb) acc[a][bb] = v16i{};
 
-  load_step(0);
-  __syncthreads();  // lut ready
-  store_step();
-  __syncthreads();
-
   const int frow = lane & 31, fhalf = lane >> 5;
-  for (int64_t ks = 0; ks < C; ++ks) {
-    if (ks + 1 < C) load_step(ks + 1);
+  // MFMAs of one step from a stage: four 32-wide k slices
+  auto compute = [&](const int8_t* stage) {
+    const int8_t* xs = stage;
+    const int8_t* ws = stage + G::LDS_X;
 #pragma unroll
     for (int t = 0; t < kBK / 32; ++t) {
       v4i af[G::FM], bf[G::FN];
@@ -177,12 +204,34 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_kernel(
         for (int bb = 0; bb < G::FN; ++bb)
           acc[a][bb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[a], bf[bb], acc[a][bb], 0, 0, 0);
     }
+  };
+
+  load_step(0);
+  __syncthreads();  // lut ready
+  store_step(smem);
+  if (C > 1) load_step(1);
+  __syncthreads();
+
+  // steady state: the stage of step ks + 1 is filled from registers (loaded
+  // one step earlier), the loads of step ks + 2 are issued, then the MFMAs
+  // of step ks run; one barrier per step
+  int64_t ks = 0;
+  for (; ks + 2 < C; ++ks) {
+    store_step(smem + ((ks + 1) & 1) * G::STAGE);
+    // issue the loads before the MFMAs, so they have a whole step to land
+    __builtin_amdgcn_sched_barrier(0);
+    load_step(ks + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(smem + (ks & 1) * G::STAGE);
     __syncthreads();
-    if (ks + 1 < C) {
-      store_step();
-      __syncthreads();
-    }
   }
+  if (ks + 1 < C) {
+    store_step(smem + ((ks + 1) & 1) * G::STAGE);
+    compute(smem + (ks & 1) * G::STAGE);
+    __syncthreads();
+    ++ks;
+  }
+  compute(smem + (ks & 1) * G::STAGE);
 
   // ---- epilogue: lane holds C[i][j] with j = lane%32 and
   //      i = 8*(r/4) + 4*(lane/32) + r%4 for accumulator element r
@@ -210,22 +259,47 @@ int launch_cfg(const uint8_t* w, const int8_t* x, const float* x_scale, float w_
                float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
   const int MT = static_cast<int>(ceil_div(m, G::BM));
   const int NT = static_cast<int>(ceil_div(n, G::BN));
-  return launch(gemm_kernel<G>, dim3(static_cast<unsigned>(MT) * NT), dim3(kGemmThreads),
-                     0, s, w, x, x_scale, w_scale, y, acc, m, n, k, MT, NT);
+  const dim3 grid(static_cast<unsigned>(MT) * NT), block(G::THREADS);
+  if (k % kBK == 0)
+    return launch(gemm_kernel<G, true>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, m, n,
+                  k, MT, NT);
+  return launch(gemm_kernel<G, false>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, m, n, k,
+                MT, NT);
 }
 
-using CfgLarge = GemmCfg<256, 256, 2, 2>;  // wave tile 128 x 128
-using CfgMid = GemmCfg<128, 256, 2, 2>;    // wave tile 64 x 128
-using CfgSkinny = GemmCfg<32, 256, 1, 4>;  // wave tile 32 x 64
+using CfgLarge = GemmCfg<256, 256, 2, 4, 512>;  // wave block 128 x 64
+using CfgMid = GemmCfg<128, 256, 2, 4, 512>;    // wave block 64 x 64
+using CfgSmall = GemmCfg<128, 128, 2, 4, 512>;  // wave block 64 x 32
+using CfgSkinny = GemmCfg<32, 256, 1, 4, 256>;  // wave block 32 x 64
+
+constexpr int64_t kCUs = 256;
+
+// Rounds of one-workgroup-per-CU waves a configuration needs, weighted by
+// its tile area (a proxy for time when every configuration keeps its MFMAs
+// similarly busy).
+template <class G>
+int64_t gemm_cost(int64_t m, int64_t n) {
+  return ceil_div(ceil_div(m, G::BM) * ceil_div(n, G::BN), kCUs) * G::BM * G::BN;
+}
 
 }  // namespace
 
+int gemm_config_for(int64_t m, int64_t n) {
+  if (m <= 32) return 0;
+  const int64_t cl = gemm_cost<CfgLarge>(m, n), cm = gemm_cost<CfgMid>(m, n),
+                cs = gemm_cost<CfgSmall>(m, n);
+  if (cl <= cm && cl <= cs) return 3;
+  return cm <= cs ? 2 : 1;
+}
+
 int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
                      float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
-  if (m <= 32) return launch_cfg<CfgSkinny>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
-  const int64_t big_tiles = ceil_div(m, 256) * ceil_div(n, 256);
-  if (big_tiles >= 256) return launch_cfg<CfgLarge>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
-  return launch_cfg<CfgMid>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
+  switch (gemm_config_for(m, n)) {
+    case 0: return launch_cfg<CfgSkinny>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
+    case 1: return launch_cfg<CfgSmall>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
+    case 2: return launch_cfg<CfgMid>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
+    default: return launch_cfg<CfgLarge>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
+  }
 }
 
 }  // namespace sherry

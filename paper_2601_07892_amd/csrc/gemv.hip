@@ -28,20 +28,6 @@ namespace {
 constexpr int kGemvThreads = 64 * kGemvWaves;
 constexpr int kRing = 3;  // containers per wave held in the register ring
 
-// Byte offset (code*4) of code j of a 160-bit container held in d[0..4].
-template <int j>
-__device__ __forceinline__ uint32_t code_x4(const uint32_t (&d)[5]) {
-  constexpr int bit = 5 * j, i = bit >> 5, off = bit & 31;
-  if constexpr (off >= 2) {
-    constexpr int hi = (i < 4) ? i + 1 : i;
-    return __builtin_amdgcn_alignbit(d[hi], d[i], off - 2) & 0x7Cu;
-  } else if constexpr (i > 0) {
-    return __builtin_amdgcn_alignbit(d[i], d[i - 1], 30 + off) & 0x7Cu;
-  } else {
-    return (d[0] << 2) & 0x7Cu;
-  }
-}
-
 template <int j0, int... js>
 __device__ __forceinline__ void group_offsets(const uint32_t (&d)[5], uint32_t* a4,
                                               std::integer_sequence<int, js...>) {

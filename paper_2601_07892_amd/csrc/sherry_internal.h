@@ -54,6 +54,22 @@ __host__ __device__ constexpr uint32_t decode_word(uint32_t code) {
   return word;
 }
 
+// Byte offset (code*4) in the 32-entry table of code j (0..31) of a row's
+// 160-bit stream held in d[0..4] (stream bit b = bit b%32 of d[b/32]): one
+// funnel shift and one mask.
+template <int j>
+__device__ __forceinline__ uint32_t code_x4(const uint32_t (&d)[5]) {
+  constexpr int bit = 5 * j, i = bit >> 5, off = bit & 31;
+  if constexpr (off >= 2) {
+    constexpr int hi = (i < 4) ? i + 1 : i;
+    return __builtin_amdgcn_alignbit(d[hi], d[i], off - 2) & 0x7Cu;
+  } else if constexpr (i > 0) {
+    return __builtin_amdgcn_alignbit(d[i], d[i - 1], 30 + off) & 0x7Cu;
+  } else {
+    return (d[0] << 2) & 0x7Cu;
+  }
+}
+
 // Address-space views of device pointers.  Pointers read from memory (e.g.
 // from a descriptor array) are generic to the compiler; these casts let it
 // emit global loads, and scalar loads for data that is read-only during the
@@ -103,6 +119,9 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
 int launch_gemv_batched(const sherry_gemv_desc* descs, int count,
                         int64_t total_blocks, hipStream_t s);
 
+// MFMA tile configuration chosen for an m x n product: 0 skinny (32 x 256),
+// 1 small (128 x 128), 2 mid (128 x 256), 3 large (256 x 256).
+int gemm_config_for(int64_t m, int64_t n);
 int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale,
                      float w_scale, float* y, int32_t* acc, int64_t m,
                      int64_t n, int64_t k, hipStream_t s);

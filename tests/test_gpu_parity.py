@@ -135,6 +135,36 @@ def test_mfma_large_tile_config(dev):
     assert np.array_equal(y.astype(np.float64), acc.astype(np.float64) * 0.125)
 
 
+# The MFMA tile configuration follows from (m, n): m <= 32 -> 32x256; else
+# the cheapest of 256x256, 128x256, 128x128 by rounds of 256 workgroups x
+# tile area.  These are the M = 2048 prefill shapes of LLaMA-3.2-3B (the
+# launch configurations the benchmark times), checked on sampled outputs:
+# q/o and down -> 128x256, k/v -> 128x128, gate/up -> 256x256.
+PREFILL_3B = [("q", 3072, 3072), ("k", 1024, 3072), ("gate", 8192, 3072), ("down", 3072, 8192)]
+
+
+@pytest.mark.parametrize("name,n,k", PREFILL_3B)
+def test_mfma_prefill_shapes_sampled(dev, name, n, k):
+    sh = _sh()
+    m = 2048
+    _say("mfma-prefill", name, m, n, k)
+    t = synth.ternary_34(n, k, 35, "pf", name)
+    x = synth.activations(m, k, 35, "pfx", name, outlier_frac=0.01)
+    q, sx = oracle.quantize_act(x)
+    sw = synth.weight_scale(35, "pfs", name)
+    y, acc = _run(dev, t, q, sx, sw, sh.SHERRY_KERNEL_MFMA, m)
+    rng = np.random.default_rng(1)
+    ii, jj = rng.integers(0, m, 1500), rng.integers(0, n, 1500)
+    # corners of the output too (first/last rows and columns of tiles)
+    ii = np.concatenate([ii, [0, m - 1, 0, m - 1, 255, 256, 127, 128]])
+    jj = np.concatenate([jj, [0, n - 1, n - 1, 0, 255, 256, 127, 128]])
+    for i, j in zip(ii, jj):
+        a = oracle.dot_i32(q[i], t[j])
+        assert acc[i, j] == a, (i, j)
+        ref = oracle.epilogue(np.array([[a]], np.int32), sx[i:i + 1], sw)[0, 0]
+        assert abs(float(y[i, j]) - ref) <= 1e-5 * abs(ref)
+
+
 # ------------------------------------------------------ end-to-end + dispatch
 
 @pytest.mark.parametrize("m,n,k", [(1, 2048, 2048), (4, 1024, 3072), (16, 1024, 3072),
