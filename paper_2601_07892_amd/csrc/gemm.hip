@@ -13,9 +13,8 @@
 // and the loads of step s+2 are issued, so there is one barrier per step and
 // every global load has a whole step to land.  Eight waves (two per SIMD)
 // let one wave's decode and LDS traffic overlap the other's MFMAs.
-// LDS rows are 128 bytes; 16-byte chunk c of row r lives at chunk c ^ (r&7),
-// so the 8 rows read by any 8 lanes of a fragment load hit 8 distinct chunk
-// positions (all 32 banks once).
+// LDS rows are 128 bytes, with 16-byte chunks swizzled per row (swz) so
+// that fragment reads and tile writes are free of bank conflicts.
 #include "sherry_internal.h"
 
 namespace sherry {
@@ -45,7 +44,13 @@ struct GemmCfg {
   static constexpr int LDS_X = BM * kBK, LDS_W = BN * kBK, STAGE = LDS_X + LDS_W;
 };
 
-__device__ __forceinline__ int swz(int row, int chunk) { return row * kBK + ((chunk ^ (row & 7)) << 4); }
+// 16-byte chunk c of LDS row r is stored at chunk c ^ (r & 7) ^ ((r >> 3) & 1):
+// a 16-byte access by 16 consecutive rows at one logical chunk then covers
+// all 64 LDS banks once (rows 8 apart differ in the low chunk bit and rows
+// of equal swizzle differ in parity), and 8 consecutive rows cover 32 banks.
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * kBK + ((chunk ^ (row & 7) ^ ((row >> 3) & 1)) << 4);
+}
 
 // Decodes codes [j0, j0 + n) (n a multiple of 4) of the row stream in d and
 // writes them as int8 to the T tile row: 16-byte chunk per 4 codes.
@@ -215,14 +220,26 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
   // steady state: the stage of step ks + 1 is filled from registers (loaded
   // one step earlier), the loads of step ks + 2 are issued, then the MFMAs
   // of step ks run; one barrier per step
+  // Half of the waves (one per SIMD) run the MFMAs first and fill the next
+  // stage after them, so that on every SIMD one wave's decode and LDS writes
+  // overlap the other wave's MFMAs.
+  const bool mfma_first = G::THREADS >= 512 && (wave & 4);
   int64_t ks = 0;
   for (; ks + 2 < C; ++ks) {
-    store_step(smem + ((ks + 1) & 1) * G::STAGE);
-    // issue the loads before the MFMAs, so they have a whole step to land
-    __builtin_amdgcn_sched_barrier(0);
-    load_step(ks + 2);
+    if (!mfma_first) {
+      store_step(smem + ((ks + 1) & 1) * G::STAGE);
+      // issue the loads before the MFMAs, so they have a whole step to land
+      __builtin_amdgcn_sched_barrier(0);
+      load_step(ks + 2);
+    }
     __builtin_amdgcn_sched_barrier(0);
     compute(smem + (ks & 1) * G::STAGE);
+    __builtin_amdgcn_sched_barrier(0);
+    if (mfma_first) {
+      store_step(smem + ((ks + 1) & 1) * G::STAGE);
+      __builtin_amdgcn_sched_barrier(0);
+      load_step(ks + 2);
+    }
     __syncthreads();
   }
   if (ks + 1 < C) {

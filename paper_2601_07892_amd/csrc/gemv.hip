@@ -34,10 +34,11 @@ __device__ __forceinline__ void group_offsets(const uint32_t (&d)[5], uint32_t* 
   ((a4[js] = code_x4<j0 + js>(d)), ...);
 }
 
-// Codes decoded per batch of table reads: 16 for one token; 8 when several
-// tokens' activation words must sit in SGPRs at once.
+// Codes decoded per batch of table reads: all 32 of a container for one
+// token (one wait for 32 table reads in flight); 8 when several tokens'
+// activation words must sit in SGPRs at once.
 template <int M>
-constexpr int group_size() { return M == 1 ? 16 : 8; }
+constexpr int group_size() { return M == 1 ? 32 : 8; }
 
 // Decodes codes [g, g + G) of a container in d[0..4] and accumulates the dot
 // products with the activation words at xw (M tokens, row stride kw words,
