@@ -5,17 +5,19 @@ Workload (the metric's headline configuration): one decode step (M = 1) of the
 linear layers of LLaMA-3.2-1B -- 16 layers x {q 2048x2048, k/v 512x2048,
 o 2048x2048, gate/up 8192x2048, down 2048x8192} -- as 3:4 ternary weights
 packed at 1.25 bits, per-tensor scales U(0.01, 0.05), a fresh fp32 N(0,1)
-activation vector per projection.  A step is the whole hot path on device:
-per-token int8 quantization of the 112 activation vectors (2 launches) and
-the 112 products in one grouped launch.  Weights and activations are rotated
-over 16 copies (2.4 GB, about 10x the 256 MB Infinity Cache, so cache hits
-cannot inflate the figures).
+activation vector per projection.  A step is the whole hot path on device in
+one launch: per-token int8 quantization of each of the 112 activation vectors
+fused with its product (sherry_gemv_f32_batched).  Weights and activations are
+rotated over 16 copies (2.4 GB, about 10x the 256 MB Infinity Cache, so cache
+hits cannot inflate the figures).
 
 Prints one JSON line.  `value` = algorithmic bytes of a step / step time
-(GB/s); `roofline` is the grouped product kernel alone (HIP events around a
-run of back-to-back launches over the rotated copies, on the stream the kernel
-runs on); `cpu_baseline` is the CPU oracle on the host cores over full steps.  With --extra (default on) the M = 2048 prefill GEMM
-on the LLaMA-3.2-3B and -1B shapes is timed too (dense-equivalent TOPS).
+(GB/s), timed with HIP events around back-to-back steps on the stream the
+kernel runs on, after a heat-up; `roofline` is that same fused kernel;
+`unfused` times the same step as separate quantize and int8 product launches;
+`cpu_baseline` is the CPU oracle on the host cores over full steps.  Unless
+--no-extra, the M = 2048 prefill GEMM on the LLaMA-3.2-3B and -1B shapes is
+timed too (dense-equivalent TOPS).
 """
 from __future__ import annotations
 
@@ -98,7 +100,18 @@ class DecodeStep:
                 d.n, d.k, d.w_scale = lin.n, lin.k, self.scales[i]
             total = sh.sherry_gemv_batched_prepare(descs)
             ddev = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
-            self.copies.append(dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total))
+            # fused descriptors: fp32 activations in, scales written back
+            fdescs = (sh.sherry_gemv_f32_desc * self.count)()
+            for i in range(self.count):
+                f, d = fdescs[i], descs[i]
+                lin = self.lins[i][1]
+                f.w, f.y, f.acc, f.x_scale = d.w, d.y, None, d.x_scale
+                f.x = xs[lin.k].data_ptr() + (d.x - qs[lin.k].data_ptr()) * 4
+                f.n, f.k, f.w_scale = d.n, d.k, d.w_scale
+            ftotal = sh.sherry_gemv_f32_batched_prepare(fdescs)
+            fdev = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
+            self.copies.append(dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total,
+                                    fdescs=fdev, ftotal=ftotal))
         torch.cuda.synchronize()
         self.total_blocks = self.copies[0]["total"]
         self.weight_bytes = sum(sh.sherry_packed_bytes(l.n, l.k) for _, l in self.lins)
@@ -108,6 +121,9 @@ class DecodeStep:
                               for _, l in self.lins)
         # quantization: fp32 x read, int8 q written, fp32 scale written
         self.quant_bytes = sum(5 * l.k + 4 for _, l in self.lins)
+        # fused step: packed weights, fp32 x, its scale written, fp32 y
+        self.fused_bytes = sum(sh.sherry_packed_bytes(l.n, l.k) + 4 * l.k + 4 + 4 * l.n
+                               for _, l in self.lins)
         self.ops = sum(2 * l.n * l.k for _, l in self.lins)
         log("working set: %.1f MB of packed weights per copy x %d copies" %
             (self.weight_bytes / 1e6, copies))
@@ -121,32 +137,65 @@ class DecodeStep:
         cp = self.copies[c]
         self.sh.sherry_gemv_batched(cp["descs"], self.count, cp["total"])
 
+    def fused(self, c):
+        cp = self.copies[c]
+        self.sh.sherry_gemv_f32_batched(cp["fdescs"], self.count, cp["ftotal"])
 
-def bench_decode(step: DecodeStep, torch, steps, warmup):
+
+def _events(torch):
+    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+
+def settle(run, torch, seconds=0.02):
+    """Untimed back-to-back launches of the timed loop's own work for about
+    `seconds`: the first few milliseconds over a cold working set run slower
+    than the steady state that the timed loop reports."""
+    torch.cuda.synchronize()
+    t0, i = time.perf_counter(), 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(32):
+            run(i)
+            i += 1
+        torch.cuda.synchronize()
+
+
+def bench_fused(step: DecodeStep, torch, steps, warmup):
+    """ms per decode step (one fused launch), back to back after a heat-up."""
     ncp = len(step.copies)
+    heat(step.sh, torch, step.dev)
+    settle(lambda i: step.fused(i % ncp), torch)
+    for i in range(warmup):
+        step.fused(i % ncp)
+    start, stop = _events(torch)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        step.fused(i % ncp)
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps
+
+
+def bench_unfused(step: DecodeStep, torch, steps, warmup):
+    """ms per step as separate launches (2 quantize + grouped int8 product)."""
+    ncp = len(step.copies)
+
+    def unfused(i):
+        step.quantize(i % ncp)
+        step.gemv(i % ncp)
+    settle(unfused, torch)
     for i in range(warmup):
         step.quantize(i % ncp)
         step.gemv(i % ncp)
+    start, stop = _events(torch)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
     start.record()
     for i in range(steps):
-        c = i % ncp
-        step.quantize(c)
-        ev[i][0].record()
-        step.gemv(c)
-        ev[i][1].record()
+        step.quantize(i % ncp)
+        step.gemv(i % ncp)
     stop.record()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    total_ms = start.elapsed_time(stop)
-    gemv_ms = [a.elapsed_time(b) for a, b in ev]
-    return total_ms / steps, float(np.mean(gemv_ms)), float(np.median(gemv_ms)), wall
+    return start.elapsed_time(stop) / steps
 
 
 def heat(sh, torch, dev, seconds=0.03):
@@ -170,9 +219,8 @@ def bench_product_only(step: DecodeStep, torch, launches):
     launches over the rotated copies, one event pair around the whole run, so
     that per-launch event overhead does not enter the figure."""
     ncp = len(step.copies)
-    heat(step.sh, torch, step.dev)
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
+    settle(lambda i: step.gemv(i % ncp), torch)
+    start, stop = _events(torch)
     torch.cuda.synchronize()
     start.record()
     for i in range(launches):
@@ -261,7 +309,7 @@ def cpu_baseline(step: DecodeStep, min_seconds=10.0):
         reps += 1
     del xk
     per_step = t_total / reps
-    return {"value": round((step.gemv_bytes + step.quant_bytes) / per_step / 1e9, 3),
+    return {"value": round(step.fused_bytes / per_step / 1e9, 3),
             "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": "%d full decode step(s) of the same workload (112 products of the "
                       "16-layer LLaMA-3.2-1B linears, quantize + int32 product + fp64 "
@@ -270,7 +318,7 @@ def cpu_baseline(step: DecodeStep, min_seconds=10.0):
 
 
 def load_traffic(src_hash: str):
-    path = os.path.join(ROOT, "profiles", "traffic_gemv_batched.json")
+    path = os.path.join(ROOT, "profiles", "traffic_gemv_f32_batched.json")
     try:
         with open(path) as f:
             d = json.load(f)
@@ -326,25 +374,27 @@ def main():
 
     step = DecodeStep(sh, torch, dev, synth.LLAMA_1B, args.seed, copies=args.copies)
     if args.only == "product":
+        heat(sh, torch, dev)
         kern_ms = bench_product_only(step, torch, args.product_launches)
-        log("grouped product %.2f us back to back over %d launches" %
+        log("int8 grouped product %.2f us back to back over %d launches" %
             (kern_ms * 1e3, args.product_launches))
         print(json.dumps({"kernel": "gemv_batched_kernel", "launches": args.product_launches,
                           "avg_launch_us": round(kern_ms * 1e3, 3),
                           "bytes_per_launch": step.gemv_bytes}), flush=True)
         return
-    heat(sh, torch, dev)
-    ms_step, gemv_ms_mean, gemv_ms_med, wall = bench_decode(step, torch, args.steps, args.warmup)
+    ms_step = bench_fused(step, torch, args.steps, args.warmup)
+    value = step.fused_bytes / (ms_step * 1e-3) / 1e9
+    log("decode step (fused quantize + product, one launch) %.2f us, %.0f GB/s" %
+        (ms_step * 1e3, value))
     if args.only == "decode":
-        log("step %.2f us" % (ms_step * 1e3))
+        print(json.dumps({"kernel": "gemv_f32_batched_kernel", "launches": args.steps,
+                          "avg_launch_us": round(ms_step * 1e3, 3),
+                          "bytes_per_launch": step.fused_bytes}), flush=True)
         return
+    ms_unfused = bench_unfused(step, torch, args.steps, args.warmup)
     kern_ms = bench_product_only(step, torch, args.product_launches)
-    step_bytes = step.gemv_bytes + step.quant_bytes
-    value = step_bytes / (ms_step * 1e-3) / 1e9
-    achieved = step.gemv_bytes / (kern_ms * 1e-3) / 1e9
-    log("step %.2f us; grouped product %.2f us back to back (%.0f GB/s), %.2f us inside "
-        "the step between event pairs (median %.2f)" %
-        (ms_step * 1e3, kern_ms * 1e3, achieved, gemv_ms_mean * 1e3, gemv_ms_med * 1e3))
+    log("unfused step %.2f us; int8 grouped product alone %.2f us (%.0f GB/s)" %
+        (ms_unfused * 1e3, kern_ms * 1e3, step.gemv_bytes / (kern_ms * 1e-3) / 1e9))
     src_hash = kernel_source_hash(["gemv.hip", "sherry_internal.h"])
     out = {
         "metric": "ternary GEMV GB/s & % HBM peak at M=1; GEMM TOPS at M=2048 (LLaMA-1B shapes)",
@@ -356,15 +406,18 @@ def main():
                                "(112 GEMVs), 1.25-bit 3:4 ternary, %d rotated copies" % args.copies,
                    "weights_mb_per_copy": round(step.weight_bytes / 1e6, 2),
                    "working_set_mb": round(step.weight_bytes * args.copies / 1e6, 1),
-                   "step": "2 int8 quantize launches + 1 grouped product launch",
+                   "step": "1 launch: per-token int8 quantization fused with the 112 products",
                    "seed": args.seed},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "roofline": {"bound": "hbm", "achieved": round(value, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 4),
                      "traffic": load_traffic(src_hash),
-                     "kernel": "gemv_batched_kernel", "bytes_per_launch": step.gemv_bytes,
-                     "avg_launch_us": round(kern_ms * 1e3, 3),
-                     "in_step_event_pair_us": round(gemv_ms_mean * 1e3, 3),
+                     "kernel": "gemv_f32_batched_kernel", "bytes_per_launch": step.fused_bytes,
+                     "avg_launch_us": round(ms_step * 1e3, 3),
                      "kernel_source_hash": src_hash},
+        "unfused": {"step_us": round(ms_unfused * 1e3, 2),
+                    "int8_product_us": round(kern_ms * 1e3, 3),
+                    "int8_product_gbs": round(step.gemv_bytes / (kern_ms * 1e-3) / 1e9, 1),
+                    "int8_product_bytes": step.gemv_bytes},
     }
     if not args.no_extra:
         try:

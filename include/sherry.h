@@ -69,6 +69,9 @@ typedef enum sherry_status {
 /* Largest accepted N and M (grid limits; far above any LLM layer). */
 #define SHERRY_MAX_N (1LL << 26)
 #define SHERRY_MAX_M (1LL << 24)
+/* Longest activation row of the fused quantize + product calls (the
+ * quantized row is staged on chip). */
+#define SHERRY_FUSED_MAX_K 32768
 
 /* Kernel selectors for sherry_gemm_ex (the automatic choice is by M). */
 #define SHERRY_KERNEL_AUTO 0
@@ -180,6 +183,41 @@ int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
  * device descriptors cannot be re-validated here. */
 int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
                         int64_t total_blocks, void* stream);
+
+/* ---------------------------------------------------------------------- */
+/* Fused quantization + M = 1 product: fp32 activations in, one launch.    */
+/* Each workgroup quantizes the activation row (exactly as                 */
+/* sherry_quantize_act) and runs the product of sherry_gemv on it, so the  */
+/* results are bit-identical to sherry_quantize_act followed by            */
+/* sherry_gemv, without the int8 round trip through memory and the second */
+/* launch (the engine quantizes activations on the fly, Appendix A).       */
+/* ---------------------------------------------------------------------- */
+
+/* x: device, fp32 [k], 16-byte aligned, finite values, k <=
+ * SHERRY_FUSED_MAX_K.  x_scale: device, fp32 [1] that receives the
+ * activation scale (absmax / 127, 0 for an all-zero row), or NULL.  Other
+ * arguments as sherry_gemv. */
+int sherry_gemv_f32(const uint8_t* w, const float* x, float* x_scale,
+                    float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                    void* stream);
+
+typedef struct sherry_gemv_f32_desc {
+  const uint8_t* w;      /* device, packed n x k, 16-byte aligned          */
+  const float* x;        /* device, fp32 [k], 16-byte aligned              */
+  float* x_scale;        /* device, fp32 [1] output, or NULL               */
+  float* y;              /* device, fp32 [n]                               */
+  int32_t* acc;          /* device, int32 [n] or NULL                      */
+  int64_t n, k;          /* k <= SHERRY_FUSED_MAX_K                        */
+  float w_scale;
+  int32_t block_begin;   /* written by sherry_gemv_f32_batched_prepare     */
+} sherry_gemv_f32_desc;
+
+/* As sherry_gemv_batched_prepare / sherry_gemv_batched, for fused
+ * descriptors: every product of the array runs in one launch. */
+int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int count,
+                                    int64_t* total_blocks);
+int sherry_gemv_f32_batched(const sherry_gemv_f32_desc* descs_dev, int count,
+                            int64_t total_blocks, void* stream);
 
 /* ---------------------------------------------------------------------- */
 /* 2-bit reference layout (the "2-bit strategy" of Sec. 2.3): one ternary  */

@@ -27,13 +27,15 @@ SHERRY_KERNEL_AUTO = 0
 SHERRY_KERNEL_GEMV = 1
 SHERRY_KERNEL_MFMA = 2
 SHERRY_MAX_K = 174720
+SHERRY_FUSED_MAX_K = 32768
 
 EXPORTS = [
     "sherry_status_str", "sherry_version", "sherry_last_error", "sherry_packed_bytes", "sherry_pack",
     "sherry_unpack", "sherry_quantize_act", "sherry_gemv", "sherry_gemm", "sherry_gemm_ex",
     "sherry_gemm_kernel_for", "sherry_gemv_batched_prepare", "sherry_gemv_batched",
     "sherry_packed2_bytes", "sherry_pack2", "sherry_gemv2", "sherry_stream_read",
-    "sherry_stream_read_groups",
+    "sherry_stream_read_groups", "sherry_gemv_f32", "sherry_gemv_f32_batched_prepare",
+    "sherry_gemv_f32_batched",
 ]
 
 
@@ -47,6 +49,14 @@ class SherryError(RuntimeError):
 
 
 class sherry_gemv_desc(ctypes.Structure):
+    _fields_ = [
+        ("w", ctypes.c_void_p), ("x", ctypes.c_void_p), ("x_scale", ctypes.c_void_p),
+        ("y", ctypes.c_void_p), ("acc", ctypes.c_void_p), ("n", ctypes.c_int64),
+        ("k", ctypes.c_int64), ("w_scale", ctypes.c_float), ("block_begin", ctypes.c_int32),
+    ]
+
+
+class sherry_gemv_f32_desc(ctypes.Structure):
     _fields_ = [
         ("w", ctypes.c_void_p), ("x", ctypes.c_void_p), ("x_scale", ctypes.c_void_p),
         ("y", ctypes.c_void_p), ("acc", ctypes.c_void_p), ("n", ctypes.c_int64),
@@ -87,6 +97,10 @@ def _load():
         "sherry_gemv2": ([vp, vp, vp, f32, vp, vp, i64, i64, vp], ctypes.c_int),
         "sherry_stream_read": ([vp, ctypes.c_size_t, vp, vp], ctypes.c_int),
         "sherry_stream_read_groups": ([ctypes.c_size_t], i64),
+        "sherry_gemv_f32": ([vp, vp, vp, f32, vp, vp, i64, i64, vp], ctypes.c_int),
+        "sherry_gemv_f32_batched_prepare": ([ctypes.POINTER(sherry_gemv_f32_desc), ctypes.c_int,
+                                             i64p], ctypes.c_int),
+        "sherry_gemv_f32_batched": ([vp, ctypes.c_int, i64, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -222,6 +236,26 @@ def sherry_gemv_batched(descs_dev, count: int, total_blocks: int, stream=None):
     """descs_dev: device uint8 tensor holding a byte copy of prepared descriptors."""
     _check(lib.sherry_gemv_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
            "sherry_gemv_batched")
+
+
+def sherry_gemv_f32(w, x, x_scale, w_scale: float, y, acc, n: int, k: int, stream=None):
+    """Quantizes the fp32 activation row x and multiplies, in one launch."""
+    _check(lib.sherry_gemv_f32(_ptr(w), _ptr(x), _ptr(x_scale), float(w_scale), _ptr(y),
+                               _ptr(acc), n, k, _stream(stream)), "sherry_gemv_f32")
+
+
+def sherry_gemv_f32_batched_prepare(descs) -> int:
+    """Fills block_begin of a ctypes array of sherry_gemv_f32_desc; returns total blocks."""
+    total = ctypes.c_int64(0)
+    _check(lib.sherry_gemv_f32_batched_prepare(descs, len(descs), ctypes.byref(total)),
+           "sherry_gemv_f32_batched_prepare")
+    return int(total.value)
+
+
+def sherry_gemv_f32_batched(descs_dev, count: int, total_blocks: int, stream=None):
+    """descs_dev: device uint8 tensor holding a byte copy of prepared f32 descriptors."""
+    _check(lib.sherry_gemv_f32_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
+           "sherry_gemv_f32_batched")
 
 
 def sherry_gemv2(w2, x, x_scale, w_scale: float, y, acc, n: int, k: int, stream=None):

@@ -26,6 +26,16 @@ inline bool shape_ok(int64_t m, int64_t n, int64_t k) {
 
 inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
+int check_fused(const uint8_t* w, const float* x, const float* x_scale, float* y,
+                const int32_t* acc, int64_t n, int64_t k) {
+  if (!w || !x || !y) return SHERRY_E_INVALID;
+  if (!shape_ok(1, n, k) || k > SHERRY_FUSED_MAX_K) return SHERRY_E_SHAPE;
+  if (!aligned(w, 16) || !aligned(x, 16) || !aligned(y, 4) || (x_scale && !aligned(x_scale, 4)) ||
+      (acc && !aligned(acc, 4)))
+    return SHERRY_E_ALIGN;
+  return SHERRY_OK;
+}
+
 // Largest M the VALU decode kernel serves; above it the MFMA kernel runs.
 constexpr int64_t kGemvMaxM = 4;
 
@@ -105,6 +115,14 @@ extern "C" int sherry_gemv(const uint8_t* w, const int8_t* x, const float* x_sca
   return sherry_gemm_ex(w, x, x_scale, w_scale, y, acc, 1, n, k, SHERRY_KERNEL_GEMV, stream);
 }
 
+namespace {
+// Workgroups of one grouped M = 1 product (same split as the batched kernels).
+int64_t gemv_blocks(int64_t n, int64_t k, int target) {
+  const int S = gemv_split(static_cast<int>(ceil_div(k, kTileK)), target);
+  return ceil_div(ceil_div(n, kTileRows) * S, kGemvWaves);
+}
+}  // namespace
+
 extern "C" int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
                                            int64_t* total_blocks) {
   if (!descs || !total_blocks || count < 1) return SHERRY_E_INVALID;
@@ -115,8 +133,7 @@ extern "C" int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
     if (st != SHERRY_OK) return st;
     if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
-    const int S = gemv_split(static_cast<int>(ceil_div(d.k, kTileK)));
-    blocks += ceil_div(ceil_div(d.n, kTileRows) * S, kGemvWaves);
+    blocks += gemv_blocks(d.n, d.k, kGemvTarget);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
   }
   *total_blocks = blocks;
@@ -147,4 +164,35 @@ extern "C" int sherry_stream_read(const void* src, size_t bytes, uint32_t* sink,
   if (bytes == 0 || bytes % 16 != 0) return SHERRY_E_SHAPE;
   if (!aligned(src, 16) || !aligned(sink, 4)) return SHERRY_E_ALIGN;
   return launch_stream_read(src, bytes, sink, as_stream(stream));
+}
+
+extern "C" int sherry_gemv_f32(const uint8_t* w, const float* x, float* x_scale, float w_scale,
+                               float* y, int32_t* acc, int64_t n, int64_t k, void* stream) {
+  int st = check_fused(w, x, x_scale, y, acc, n, k);
+  if (st != SHERRY_OK) return st;
+  return launch_gemv_f32(w, x, x_scale, w_scale, y, acc, n, k, as_stream(stream));
+}
+
+extern "C" int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int count,
+                                               int64_t* total_blocks) {
+  if (!descs || !total_blocks || count < 1) return SHERRY_E_INVALID;
+  int64_t blocks = 0;
+  for (int i = 0; i < count; ++i) {
+    sherry_gemv_f32_desc& d = descs[i];
+    int st = check_fused(d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k);
+    if (st != SHERRY_OK) return st;
+    d.block_begin = static_cast<int32_t>(blocks);
+    blocks += gemv_blocks(d.n, d.k, kFusedTarget);
+    if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
+  }
+  *total_blocks = blocks;
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_gemv_f32_batched(const sherry_gemv_f32_desc* descs_dev, int count,
+                                       int64_t total_blocks, void* stream) {
+  if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
+    return SHERRY_E_INVALID;
+  if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  return launch_gemv_f32_batched(descs_dev, count, total_blocks, as_stream(stream));
 }

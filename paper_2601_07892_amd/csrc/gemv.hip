@@ -84,6 +84,30 @@ __device__ __forceinline__ void dot_container(const uint32_t (&d)[5],
   }
 }
 
+// Decodes codes [g, g + 16) of a container and accumulates them against the
+// activation words at xv (LDS, 16-byte aligned; zero past K).
+template <int g>
+__device__ __forceinline__ void dot_container_lds(const uint32_t (&d)[5], const u32x4* xv,
+                                                  const uint32_t* lut, int32_t (&acc)[1]) {
+  if constexpr (g < 32) {
+    __builtin_amdgcn_sched_barrier(0);
+    u32x4 xw[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xw[i] = xv[g / 4 + i];
+    uint32_t a4[16];
+    group_offsets<g>(d, a4, std::make_integer_sequence<int, 16>{});
+    uint32_t wv[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      wv[j] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + a4[j]);
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      acc[0] = __builtin_amdgcn_sdot4(static_cast<int32_t>(xw[j >> 2][j & 3]),
+                                      static_cast<int32_t>(wv[j]), acc[0], false);
+    dot_container_lds<g + 16>(d, xv, lut, acc);
+  }
+}
+
 // Activation source: the activation words of container c, read with scalar
 // loads (wave-uniform) into SGPRs; dot masks the words past K of a partial
 // last container.
@@ -100,6 +124,17 @@ struct XFromSgpr {
     const int kb = c * kTileK;
     if (kb + kTileK <= k) dot_full(d, c, lut, acc);
     else dot_container<M, true>(d, xw0 + (kb >> 2), k >> 2, (k - kb) >> 2, lut, acc);
+  }
+};
+
+// Activation source of the fused quantize + product kernel: the int8 words
+// of the whole (zero-padded) activation row in LDS, read with wave-uniform
+// 16-byte LDS loads (broadcast) in groups of 16 codes.
+struct XFromLds {
+  const int8_t* xq;  // LDS, ceil(k/128)*128 bytes
+  __device__ __forceinline__ void dot(const uint32_t (&d)[5], int c, const uint32_t* lut,
+                                      int32_t (&acc)[1]) const {
+    dot_container_lds<0>(d, reinterpret_cast<const u32x4*>(xq + c * kTileK), lut, acc);
   }
 };
 
@@ -125,13 +160,9 @@ __device__ __forceinline__ void load_container(uint32_t (&d)[5], __amdgpu_buffer
 // end are issued unconditionally and read zeros without touching memory,
 // which keeps the outstanding loads identical on every path so the compiler
 // waits on exact counts; only the decode is skipped past the end.
-template <int M, class X>
-__device__ __forceinline__ void stream_tile(__amdgpu_buffer_rsrc_t r, int c0, int c1,
-                                            const X& xsrc, const uint32_t* lut,
-                                            int32_t (&acc)[M]) {
+// ring_fill issues the first kRing containers; ring_run decodes them all.
+__device__ __forceinline__ void ring_fill(uint32_t (&ring)[kRing][5], __amdgpu_buffer_rsrc_t r) {
   const int lane = threadIdx.x & 63;
-  const int n = c1 - c0;
-  uint32_t ring[kRing][5];
   // issue the slots strictly in order (head and tail of slot 0 first), so
   // that slot u's loads are always the oldest outstanding ones when it is
   // decoded
@@ -140,6 +171,14 @@ __device__ __forceinline__ void stream_tile(__amdgpu_buffer_rsrc_t r, int c0, in
     load_container(ring[u], r, u, lane);
     __builtin_amdgcn_sched_barrier(0);
   }
+}
+
+template <int M, class X>
+__device__ __forceinline__ void ring_run(uint32_t (&ring)[kRing][5], __amdgpu_buffer_rsrc_t r,
+                                         int c0, int c1, const X& xsrc, const uint32_t* lut,
+                                         int32_t (&acc)[M]) {
+  const int lane = threadIdx.x & 63;
+  const int n = c1 - c0;
   for (int i = 0; i < n; i += kRing) {
 #pragma unroll
     for (int u = 0; u < kRing; ++u) {
@@ -152,12 +191,14 @@ __device__ __forceinline__ void stream_tile(__amdgpu_buffer_rsrc_t r, int c0, in
 }
 
 // One workgroup of a product: block g of a problem whose tiles are split
-// over S waves each.  lut and red are LDS; the caller has filled lut.
-template <int M>
-__device__ __forceinline__ void gemv_block(const uint8_t* w_, const int8_t* x_,
-                                           const float* x_scale, float w_scale, float* y,
-                                           int32_t* acc_out, int64_t n, int k, int g, int S,
-                                           const uint32_t* lut, int32_t* red) {
+// over S waves each.  prelude.issue() then prelude.finish(sx) run before the
+// weight stream; finish yields the tokens' activation scales sx[m].  lut and red are
+// LDS; the caller has filled lut.
+template <int M, class X, class Prelude>
+__device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Prelude prelude,
+                                           float w_scale, float* y, int32_t* acc_out, int64_t n,
+                                           int k, int g, int S, const uint32_t* lut,
+                                           int32_t* red) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int C = (k + kTileK - 1) / kTileK;
@@ -169,14 +210,20 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const int8_t* x_,
   int32_t acc[M];
 #pragma unroll
   for (int m = 0; m < M; ++m) acc[m] = 0;
-  if (r < R) {
-    const int c0 = (part * C) / S, c1 = ((part + 1) * C) / S;
-    const __amdgpu_buffer_rsrc_t range = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint8_t*>(w_) + (int64_t(r) * C + c0) * kUnitBytes, 0,
-        (c1 - c0) * kUnitBytes, kBufferWord3);
-    stream_tile<M>(range, c0, c1,
-                   XFromSgpr<M>{as_const(reinterpret_cast<const int32_t*>(x_)), k}, lut, acc);
-  }
+  // a wave past the last tile streams an empty range (its loads read zeros)
+  const int c0 = (r < R) ? (part * C) / S : 0, c1 = (r < R) ? ((part + 1) * C) / S : 0;
+  const __amdgpu_buffer_rsrc_t range = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(w_) + (int64_t(r < R ? r : 0) * C + c0) * kUnitBytes, 0,
+      (c1 - c0) * kUnitBytes, kBufferWord3);
+  // the prelude (e.g. quantizing the activations) runs to completion before
+  // the first weight loads: its few loads then do not queue behind the
+  // weight stream of every wave on the GPU; every thread of the block runs it
+  prelude.issue();
+  float sx[M];
+  prelude.finish(sx);
+  uint32_t ring[kRing][5];
+  ring_fill(ring, range);
+  ring_run<M>(ring, range, c0, c1, xsrc, lut, acc);
 
 #pragma unroll
   for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + lane] = acc[m];
@@ -191,11 +238,22 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const int8_t* x_,
     if (r2 >= R || row >= n) continue;
     int32_t a = 0;
     for (int p = 0; p < S; ++p) a += red[((lt2 * S + p) * M + m) * 64 + i];
-    const float s = as_const(x_scale)[m] * w_scale;
+    const float s = sx[m] * w_scale;
     as_global_mut(y)[m * n + row] = static_cast<float>(a) * s;
     if (acc_out) as_global_mut(acc_out)[m * n + row] = a;
   }
 }
+
+// Prelude of the int8 products: the activation scales are inputs.
+template <int M>
+struct ReadScales {
+  const float* x_scale;
+  __device__ __forceinline__ void issue() const {}
+  __device__ __forceinline__ void finish(float (&sx)[M]) const {
+#pragma unroll
+    for (int m = 0; m < M; ++m) sx[m] = as_const(x_scale)[m];
+  }
+};
 
 __device__ __forceinline__ void fill_lut(uint32_t* lut) {
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
@@ -209,8 +267,9 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(
   __shared__ uint32_t lut[32];
   __shared__ int32_t red[kGemvWaves * M * 64];
   fill_lut(lut);
-  gemv_block<M>(w, x, x_scale, w_scale, y, acc, n, static_cast<int>(k), blockIdx.x, split, lut,
-                red);
+  gemv_block<M>(w, XFromSgpr<M>{as_const(reinterpret_cast<const int32_t*>(x)), static_cast<int>(k)},
+                ReadScales<M>{x_scale}, w_scale, y, acc, n, static_cast<int>(k), blockIdx.x, split,
+                lut, red);
 }
 
 __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
@@ -237,8 +296,152 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
   const sherry_gemv_desc& d = descs[lo];
   const int k = static_cast<int>(d.k);
   const int S = gemv_split(static_cast<int>((k + kTileK - 1) / kTileK));
-  gemv_block<1>(d.w, d.x, d.x_scale, d.w_scale, d.y, d.acc, d.n, k, blk - d.block_begin, S,
+  gemv_block<1>(d.w, XFromSgpr<1>{as_const(reinterpret_cast<const int32_t*>(d.x)), k},
+                ReadScales<1>{d.x_scale}, d.w_scale, d.y, d.acc, d.n, k, blk - d.block_begin, S,
                 lut, red);
+}
+
+// ---- fused per-token quantization + product (M = 1) ----
+
+// Barrier for LDS traffic only: outstanding global loads (the weight ring)
+// stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Block-wide max of one value per thread (part: kGemvWaves floats of LDS).
+__device__ __forceinline__ float block_max_f32(float v, float* part) {
+  v = wave_max_f32(v);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+  lds_barrier();
+  v = part[0];
+#pragma unroll
+  for (int i = 1; i < kGemvWaves; ++i) v = fmaxf(v, part[i]);
+  return v;
+}
+
+// Prelude of the fused kernels: quantizes the fp32 row x[0..k) into xq
+// (LDS, int8, zero-padded to kp bytes) exactly as the quantize kernel does;
+// the scale (0 for an all-zero row) is written to *x_scale by one thread
+// when write_scale.  Rows of up to NV*4*kGemvThreads values are loaded once
+// into registers by issue(); NV = 0 reads longer rows twice in finish() (the
+// second time from cache).
+template <int NV>
+struct QuantizeRow {
+  const float* x;
+  int k, kp;
+  int8_t* xq;
+  float* part;  // LDS, kGemvWaves floats
+  float* x_scale;
+  bool write_scale;
+  float4 v[NV > 0 ? NV : 1];
+
+  __device__ __forceinline__ void issue() {
+    if constexpr (NV > 0) {
+      const float4* x4 = reinterpret_cast<const float4*>(as_global(x));
+#pragma unroll
+      for (int e = 0; e < NV; ++e) {
+        const int i = threadIdx.x + e * kGemvThreads;
+        v[e] = (i < (k >> 2)) ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void finish(float (&sx)[1]) {
+    const float4* x4 = reinterpret_cast<const float4*>(as_global(x));
+    const int k4 = k >> 2;
+    uint32_t* q4 = reinterpret_cast<uint32_t*>(xq);
+    float amax = 0.0f;
+    if constexpr (NV > 0) {
+#pragma unroll
+      for (int e = 0; e < NV; ++e)
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[e].x), fabsf(v[e].y)),
+                                 fmaxf(fabsf(v[e].z), fabsf(v[e].w))));
+      amax = block_max_f32(amax, part);
+      const float s = amax / 127.0f;
+      const float rs = 1.0f / s;
+#pragma unroll
+      for (int e = 0; e < NV; ++e) {
+        const int i = threadIdx.x + e * kGemvThreads;
+        if (i < (kp >> 2)) q4[i] = (i < k4 && amax != 0.0f) ? quant4(v[e], s, rs) : 0u;
+      }
+    } else {
+      for (int i = threadIdx.x; i < k4; i += kGemvThreads) {
+        const float4 w = x4[i];
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(w.x), fabsf(w.y)), fmaxf(fabsf(w.z), fabsf(w.w))));
+      }
+      amax = block_max_f32(amax, part);
+      const float s = amax / 127.0f;
+      const float rs = 1.0f / s;
+      for (int i = threadIdx.x; i < (kp >> 2); i += kGemvThreads)
+        q4[i] = (i < k4 && amax != 0.0f) ? quant4(x4[i], s, rs) : 0u;
+    }
+    lds_barrier();
+    sx[0] = amax == 0.0f ? 0.0f : amax / 127.0f;
+    if (write_scale && threadIdx.x == 0 && x_scale) as_global_mut(x_scale)[0] = sx[0];
+  }
+};
+
+// Fused product of one block: the row length picks the quantizer (rows up
+// to 2048 and 8192 values from registers, longer ones in two passes).
+__device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, float* x_scale,
+                                            bool write_scale, float w_scale, float* y,
+                                            int32_t* acc, int64_t n, int k, int g, int S,
+                                            const uint32_t* lut, int32_t* red, float* part,
+                                            int8_t* xq) {
+  const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
+  if (kp <= 4 * kGemvThreads) {
+    gemv_block<1>(w, XFromLds{xq}, QuantizeRow<1>{x, k, kp, xq, part, x_scale, write_scale},
+                  w_scale, y, acc, n, k, g, S, lut, red);
+  } else if (kp <= 16 * kGemvThreads) {
+    gemv_block<1>(w, XFromLds{xq}, QuantizeRow<4>{x, k, kp, xq, part, x_scale, write_scale},
+                  w_scale, y, acc, n, k, g, S, lut, red);
+  } else {
+    gemv_block<1>(w, XFromLds{xq}, QuantizeRow<0>{x, k, kp, xq, part, x_scale, write_scale},
+                  w_scale, y, acc, n, k, g, S, lut, red);
+  }
+}
+
+__global__ __launch_bounds__(kGemvThreads) void gemv_f32_kernel(
+    const uint8_t* __restrict__ w, const float* __restrict__ x, float* __restrict__ x_scale,
+    float w_scale, float* __restrict__ y, int32_t* __restrict__ acc, int64_t n, int64_t k,
+    int split) {
+  __shared__ uint32_t lut[32];
+  __shared__ int32_t red[kGemvWaves * 64];
+  __shared__ float part[kGemvWaves];
+  __shared__ __attribute__((aligned(16))) int8_t xq[kFusedMaxK];
+  fill_lut(lut);
+  fused_block(w, x, x_scale, blockIdx.x == 0, w_scale, y, acc, n, static_cast<int>(k), blockIdx.x,
+              split, lut, red, part, xq);
+}
+
+__global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
+    const sherry_gemv_f32_desc* __restrict__ descs, int count) {
+  __shared__ uint32_t lut[32];
+  __shared__ int32_t red[kGemvWaves * 64];
+  __shared__ float part[kGemvWaves];
+  __shared__ __attribute__((aligned(16))) int8_t xq[kFusedMaxK];
+  fill_lut(lut);
+  const int32_t blk = static_cast<int32_t>(blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  int lo = 0;
+  for (int base = 0; base < count; base += 64) {
+    const int i = base + lane;
+    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
+    const uint64_t m = __ballot(ok);
+    const int len = __popcll(m);
+    lo = base + len - 1;
+    if (len < 64) break;
+  }
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  const sherry_gemv_f32_desc& d = descs[lo];
+  const int k = static_cast<int>(d.k);
+  const int C = (k + kTileK - 1) / kTileK;
+  const int S = gemv_split(C, kFusedTarget);
+  fused_block(d.w, d.x, d.x_scale, blk == d.block_begin, d.w_scale, d.y, d.acc, d.n, k,
+              blk - d.block_begin, S, lut, red, part, xq);
 }
 
 }  // namespace
@@ -264,6 +467,21 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale, fl
 int launch_gemv_batched(const sherry_gemv_desc* descs, int count, int64_t total_blocks,
                         hipStream_t s) {
   return launch(gemv_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
+                dim3(kGemvThreads), 0, s, descs, count);
+}
+
+int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, float w_scale, float* y,
+                    int32_t* acc, int64_t n, int64_t k, hipStream_t s) {
+  const int64_t R = ceil_div(n, kTileRows);
+  const int C = static_cast<int>(ceil_div(k, kTileK));
+  const int S = (R * gemv_split(C, kFusedTarget) >= 4096) ? gemv_split(C, kFusedTarget) : kGemvWaves;
+  return launch(gemv_f32_kernel, dim3(static_cast<unsigned>(ceil_div(R * S, kGemvWaves))),
+                dim3(kGemvThreads), 0, s, w, x, x_scale, w_scale, y, acc, n, k, S);
+}
+
+int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_t total_blocks,
+                            hipStream_t s) {
+  return launch(gemv_f32_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
                 dim3(kGemvThreads), 0, s, descs, count);
 }
 

@@ -12,26 +12,8 @@ namespace {
 
 constexpr int kQuantThreads = 256;
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-  return v;
-}
-
-__device__ __forceinline__ uint32_t quant4(float4 v, float s) {
-  float r[4] = {v.x / s, v.y / s, v.z / s, v.w / s};  // IEEE fp32 division
-  uint32_t out = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float t = rintf(r[i]);  // round half to even
-    t = fminf(fmaxf(t, -127.0f), 127.0f);
-    out |= (static_cast<uint32_t>(static_cast<int>(t)) & 0xFFu) << (8 * i);
-  }
-  return out;
-}
-
 __device__ __forceinline__ float block_max(float amax, float* part) {
-  amax = wave_max(amax);
+  amax = wave_max_f32(amax);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = amax;
   __syncthreads();
   return fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3]));
@@ -59,10 +41,11 @@ __global__ __launch_bounds__(kQuantThreads) void quantize_rows_reg(
   }
   amax = block_max(amax, part);
   const float s = amax / 127.0f;
+  const float rs = 1.0f / s;
 #pragma unroll
   for (int e = 0; e < NV; ++e) {
     const int i = threadIdx.x + e * kQuantThreads;
-    if (i < k4) qr[i] = (amax == 0.0f) ? 0u : quant4(v[e], s);
+    if (i < k4) qr[i] = (amax == 0.0f) ? 0u : quant4(v[e], s, rs);
   }
   if (threadIdx.x == 0) x_scale[row] = (amax == 0.0f) ? 0.0f : s;
 }
@@ -89,7 +72,8 @@ __global__ __launch_bounds__(kQuantThreads) void quantize_rows(
     return;
   }
   const float s = amax / 127.0f;
-  for (int64_t i = threadIdx.x; i < k4; i += kQuantThreads) qr[i] = quant4(xr[i], s);
+  const float rs = 1.0f / s;
+  for (int64_t i = threadIdx.x; i < k4; i += kQuantThreads) qr[i] = quant4(xr[i], s, rs);
   if (threadIdx.x == 0) x_scale[row] = s;
 }
 

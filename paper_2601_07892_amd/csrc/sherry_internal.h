@@ -25,14 +25,20 @@ constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Decode kernel work split.  A workgroup has kGemvWaves waves; the
 // containers of a 64-row tile are split among S waves of one workgroup,
-// S = the smallest power of two with C / S <= kGemvTarget, at most
-// kGemvWaves.  Short waves keep many workgroups queued behind the resident
-// ones, so a CU that finishes early is refilled instead of idling.
+// S = the smallest power of two with C / S <= target, at most kGemvWaves.
+// Short waves keep many workgroups queued behind the resident ones, so a CU
+// that finishes early is refilled instead of idling (target kGemvTarget).
+// The fused quantize + product kernels quantize the activation row once per
+// workgroup, so they use fewer, longer workgroups (kFusedTarget).
 constexpr int kGemvWaves = 8;
 constexpr int kGemvTarget = 8;
-__host__ __device__ constexpr int gemv_split(int C) {
+constexpr int kFusedTarget = 16;
+// Longest activation row of the fused quantize + product kernels (the
+// quantized row is held in LDS); equals SHERRY_FUSED_MAX_K.
+constexpr int kFusedMaxK = SHERRY_FUSED_MAX_K;
+__host__ __device__ constexpr int gemv_split(int C, int target = kGemvTarget) {
   int s = 1;
-  while (s < kGemvWaves && C > s * kGemvTarget) s *= 2;
+  while (s < kGemvWaves && C > s * target) s *= 2;
   return s;
 }
 
@@ -68,6 +74,44 @@ __device__ __forceinline__ uint32_t code_x4(const uint32_t (&d)[5]) {
   } else {
     return (d[0] << 2) & 0x7Cu;
   }
+}
+
+// Per-token activation quantization, shared by the quantize kernel and the
+// fused quantize + product kernel so that both take identical decisions:
+// max over a wave, and four values to int8 with s = absmax / 127:
+// q = clamp(rint(x / s), -127, 127), IEEE fp32 division, ties to even.
+__device__ __forceinline__ float wave_max_f32(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// rint(x / s) with the IEEE quotient, mostly without dividing.  rs = 1 / s
+// (correctly rounded) and t = x * rs are each within half an ulp, so t is
+// within 2^-23 * |x / s| <= 1.6e-5 of the exact quotient (|x / s| <= 127 +
+// a few ulps), and the rounded quotient within 2^-18 of it.  When t lies
+// at least 2^-13 from every half-integer, the rounded quotient is in the
+// same unit interval and rounds to the same integer as t; otherwise (also
+// for a non-finite t, e.g. a tiny s whose reciprocal overflows) the
+// division itself decides.
+__device__ __forceinline__ float round_quotient(float x, float s, float rs) {
+  const float t = x * rs;
+  const float k = rintf(t);
+  const float d = fabsf(t - k);  // exact: distance to the nearest integer
+  if (!(d <= 0.5f - 0x1p-13f)) return rintf(x / s);
+  return k;
+}
+
+__device__ __forceinline__ uint32_t quant4(float4 v, float s, float rs) {
+  const float r[4] = {round_quotient(v.x, s, rs), round_quotient(v.y, s, rs),
+                      round_quotient(v.z, s, rs), round_quotient(v.w, s, rs)};
+  uint32_t out = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float t = fminf(fmaxf(r[i], -127.0f), 127.0f);
+    out |= (static_cast<uint32_t>(static_cast<int>(t)) & 0xFFu) << (8 * i);
+  }
+  return out;
 }
 
 // Address-space views of device pointers.  Pointers read from memory (e.g.
@@ -118,6 +162,10 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
 
 int launch_gemv_batched(const sherry_gemv_desc* descs, int count,
                         int64_t total_blocks, hipStream_t s);
+int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, float w_scale, float* y,
+                    int32_t* acc, int64_t n, int64_t k, hipStream_t s);
+int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_t total_blocks,
+                            hipStream_t s);
 
 // MFMA tile configuration chosen for an m x n product: 0 skinny (32 x 256),
 // 1 small (128 x 128), 2 mid (128 x 256), 3 large (256 x 256).

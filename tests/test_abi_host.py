@@ -202,3 +202,33 @@ def test_batched_prepare():
         sh.sherry_gemv_batched_prepare(descs)
     assert L.sherry_gemv_batched(None, 1, 1, None) == sh.SHERRY_E_INVALID
     assert L.sherry_gemv_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
+
+
+def test_fused_validation_without_launch():
+    f = L.sherry_gemv_f32
+    assert f(None, FAKE, FAKE, 1.0, FAKE, None, 64, 128, None) == sh.SHERRY_E_INVALID
+    assert f(FAKE, None, FAKE, 1.0, FAKE, None, 64, 128, None) == sh.SHERRY_E_INVALID
+    assert f(FAKE, FAKE, FAKE, 1.0, None, None, 64, 128, None) == sh.SHERRY_E_INVALID
+    # k beyond the on-chip row, not a multiple of 4, zero n
+    assert f(FAKE, FAKE, FAKE, 1.0, FAKE, None, 64, sh.SHERRY_FUSED_MAX_K + 4, None) == \
+        sh.SHERRY_E_SHAPE
+    assert f(FAKE, FAKE, FAKE, 1.0, FAKE, None, 64, 130, None) == sh.SHERRY_E_SHAPE
+    assert f(FAKE, FAKE, FAKE, 1.0, FAKE, None, 0, 128, None) == sh.SHERRY_E_SHAPE
+    # fp32 activations need 16-byte alignment; scale and acc 4
+    assert f(FAKE, FAKE + 4, FAKE, 1.0, FAKE, None, 64, 128, None) == sh.SHERRY_E_ALIGN
+    assert f(FAKE, FAKE, FAKE + 2, 1.0, FAKE, None, 64, 128, None) == sh.SHERRY_E_ALIGN
+    assert f(FAKE, FAKE, FAKE, 1.0, FAKE, FAKE + 2, 64, 128, None) == sh.SHERRY_E_ALIGN
+    shapes = [(2048, 2048), (8192, 2048), (2048, 8192)]
+    descs = (sh.sherry_gemv_f32_desc * len(shapes))()
+    for i, (n, k) in enumerate(shapes):
+        descs[i].w, descs[i].x, descs[i].x_scale, descs[i].y = FAKE, FAKE, None, FAKE
+        descs[i].n, descs[i].k, descs[i].w_scale = n, k, 0.02
+    total = sh.sherry_gemv_f32_batched_prepare(descs)
+    # fused workgroups are longer: C/S <= 16 containers per wave
+    assert [d.block_begin for d in descs] == [0, 4, 20] and total == 36
+    assert ctypes.sizeof(sh.sherry_gemv_f32_desc) == 64
+    descs[2].k = 40000
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemv_f32_batched_prepare(descs)
+    assert L.sherry_gemv_f32_batched(None, 1, 1, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_gemv_f32_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN

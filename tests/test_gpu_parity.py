@@ -77,6 +77,58 @@ def test_quantize_bit_exact(dev, m, k, outl):
     assert np.array_equal(q.cpu().numpy(), q_ref)
 
 
+def _near_tie_rows(k, seed):
+    """Rows whose values sit on, or within a few ulps of, the rounding
+    boundaries (j + 1/2) * s of their own scale s = absmax / 127, for several
+    absmax values (s exact, s inexact, s denormal-range)."""
+    rng = np.random.default_rng(seed)
+    rows = []
+    for amax in (127.0, 1.0, 3.0e-3, 1.7e-36, 2.5e30, 0.7):
+        s = np.float32(np.float32(amax) / np.float32(127.0))
+        j = rng.integers(-127, 127, k).astype(np.float32)
+        x = ((j + np.float32(0.5)) * s).astype(np.float32)
+        steps = rng.integers(-3, 4, k)
+        x = np.array([np.float32(v) if d == 0 else
+                      np.nextafter(v, np.float32(np.inf) if d > 0 else np.float32(-np.inf),
+                                   dtype=np.float32) for v, d in zip(x, steps)], np.float32)
+        for d in range(2):  # some values two and three ulps away
+            sel = rng.random(k) < 0.2
+            x[sel] = np.nextafter(x[sel], np.float32(np.inf), dtype=np.float32)
+        x[0] = np.float32(amax)
+        x = np.clip(x, -np.float32(amax), np.float32(amax))
+        rows.append(x)
+    return np.stack(rows).astype(np.float32)
+
+
+@pytest.mark.parametrize("k", [256, 4096])
+def test_quantize_near_ties(dev, k):
+    # values on and next to the half-integer boundaries of x / s: the kernels
+    # round through a reciprocal and fall back to the division near them
+    sh = _sh()
+    x = _near_tie_rows(k, 36 + k)
+    m = x.shape[0]
+    xd = torch.from_numpy(x).to(dev)
+    q = torch.empty((m, k), dtype=torch.int8, device=dev)
+    sx = torch.empty(m, dtype=torch.float32, device=dev)
+    sh.sherry_quantize_act(xd, q, sx)
+    torch.cuda.synchronize()
+    q_ref, sx_ref = oracle.quantize_act(x)
+    assert np.array_equal(sx.cpu().numpy(), sx_ref)
+    assert np.array_equal(q.cpu().numpy(), q_ref)
+    # the fused kernel quantizes the same rows on chip: one-hot T reads q back
+    n = 64
+    t = np.tile(np.array([0, 1, 1, 1], np.int8), (n, k // 4))
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    for r in range(m):
+        a = torch.empty(n, dtype=torch.int32, device=dev)
+        y = torch.empty(n, dtype=torch.float32, device=dev)
+        s1 = torch.empty(1, dtype=torch.float32, device=dev)
+        sh.sherry_gemv_f32(w, xd[r].contiguous(), s1, 1.0, y, a, n, k)
+        torch.cuda.synchronize()
+        assert s1.item() == sx_ref[r]
+        assert np.array_equal(a.cpu().numpy(), oracle.gemm_i32(q_ref[r:r + 1], t)[0])
+
+
 # ------------------------------------------------------- decode kernel (M<=4)
 
 GEMV_SHAPES = [(1, 4), (64, 128), (65, 132), (1, 124), (130, 1028), (257, 2048),
@@ -387,3 +439,116 @@ def test_stream_read_checksum(dev):
     per = 256 * 1024 // 4
     ref = [np.bitwise_xor.reduce(h[g * per:(g + 1) * per]) for g in range(groups)]
     assert np.array_equal(sink.cpu().numpy().view(np.uint32), np.array(ref, np.uint32))
+
+
+# ------------------------------------------ fused quantization + M = 1 product
+
+def _fused_ref(x, t, sw):
+    q, sx = oracle.quantize_act(x)
+    acc = oracle.gemm_i32(q, t, threads=8)
+    return sx, acc, oracle.epilogue(acc, sx, sw)
+
+
+@pytest.mark.parametrize("n,k,outl", [(64, 128, 0.0), (65, 132, 0.01), (2048, 2048, 0.01),
+                                      (300, 8192, 0.01), (1, 4, 0.0), (70, 1032, 0.0),
+                                      (130, 14336, 0.01), (64, 32768, 0.01), (3, 32764, 0.0)])
+def test_fused_gemv_parity(dev, n, k, outl):
+    sh = _sh()
+    _say("fused", n, k, outl)
+    t = synth.ternary_34(n, k, 47, "fu", n, k)
+    x = synth.activations(1, k, 47, "fux", n, k, outlier_frac=outl)
+    sw = synth.weight_scale(47, "fus", n, k)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    xd = torch.from_numpy(x).to(dev)
+    sxd = torch.full((1,), float("nan"), dtype=torch.float32, device=dev)
+    y = torch.full((n,), float("nan"), dtype=torch.float32, device=dev)
+    a = torch.full((n,), -7, dtype=torch.int32, device=dev)
+    sh.sherry_gemv_f32(w, xd, sxd, sw, y, a, n, k)
+    torch.cuda.synchronize()
+    sx_ref, acc_ref, y_ref = _fused_ref(x, t, sw)
+    assert sxd.cpu().numpy()[0] == sx_ref[0]
+    assert np.array_equal(a.cpu().numpy(), acc_ref[0])
+    assert _y_ok(y.cpu().numpy(), y_ref[0])
+    # bit-identical to quantize + product as two calls
+    q2 = torch.empty(k, dtype=torch.int8, device=dev)
+    s2 = torch.empty(1, dtype=torch.float32, device=dev)
+    y2 = torch.empty(n, dtype=torch.float32, device=dev)
+    sh.sherry_quantize_act(xd.view(1, k), q2.view(1, k), s2)
+    sh.sherry_gemv(w, q2, s2, sw, y2, None, n, k)
+    torch.cuda.synchronize()
+    assert np.array_equal(y2.cpu().numpy().view(np.uint32), y.cpu().numpy().view(np.uint32))
+
+
+def test_fused_gemv_zero_row_and_no_outputs(dev):
+    sh = _sh()
+    n, k = 200, 640
+    t = synth.ternary_34(n, k, 48, "fz")
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    xd = torch.zeros(k, dtype=torch.float32, device=dev)
+    sxd = torch.full((1,), 5.0, dtype=torch.float32, device=dev)
+    y = torch.full((n,), float("nan"), dtype=torch.float32, device=dev)
+    a = torch.full((n,), -7, dtype=torch.int32, device=dev)
+    sh.sherry_gemv_f32(w, xd, sxd, 0.5, y, a, n, k)
+    torch.cuda.synchronize()
+    assert sxd.item() == 0.0
+    assert not a.any().item() and not y.any().item()
+    # x_scale and acc are optional
+    x = synth.activations(1, k, 48, "fzx")
+    xd = torch.from_numpy(x).to(dev)
+    sh.sherry_gemv_f32(w, xd, None, 0.5, y, None, n, k)
+    torch.cuda.synchronize()
+    _, _, y_ref = _fused_ref(x, t, 0.5)
+    assert _y_ok(y.cpu().numpy(), y_ref[0])
+
+
+def _fused_batched(dev, shapes, seed, with_scale=True):
+    sh = _sh()
+    descs = (sh.sherry_gemv_f32_desc * len(shapes))()
+    keep = []
+    for i, (n, k) in enumerate(shapes):
+        t = synth.ternary_34(n, k, seed, "fb", i)
+        x = synth.activations(1, k, seed, "fbx", i, outlier_frac=0.01)
+        sw = synth.weight_scale(seed, "fbs", i)
+        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        xd = torch.from_numpy(x).to(dev)
+        sxd = torch.full((1,), float("nan"), dtype=torch.float32, device=dev)
+        y = torch.full((n,), float("nan"), dtype=torch.float32, device=dev)
+        a = torch.full((n,), -7, dtype=torch.int32, device=dev)
+        d = descs[i]
+        d.w, d.x, d.y, d.acc = w.data_ptr(), xd.data_ptr(), y.data_ptr(), a.data_ptr()
+        d.x_scale = sxd.data_ptr() if with_scale else None
+        d.n, d.k, d.w_scale = n, k, sw
+        keep.append((t, x, sw, w, xd, sxd, y, a))
+    total = sh.sherry_gemv_f32_batched_prepare(descs)
+    dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+    sh.sherry_gemv_f32_batched(dd, len(shapes), total)
+    torch.cuda.synchronize()
+    return keep
+
+
+def test_fused_batched_parity(dev):
+    _say("fused batched")
+    shapes = [(64, 128), (65, 132), (2048, 2048), (512, 2048), (300, 8192), (1, 4), (70, 1032),
+              (100, 8196), (65, 14336), (3, 32768)]
+    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 49):
+        sx_ref, acc_ref, y_ref = _fused_ref(x, t, sw)
+        assert sxd.cpu().numpy()[0] == sx_ref[0]
+        assert np.array_equal(a.cpu().numpy(), acc_ref[0])
+        assert _y_ok(y.cpu().numpy(), y_ref[0])
+
+
+def test_fused_batched_decode_step_llama_1b(dev):
+    # the benchmark's decode step: 112 products of LLaMA-3.2-1B, one fused
+    # launch; sampled rows checked against the oracle
+    _say("fused batched llama-1b step")
+    shapes = [(lin.n, lin.k) for _, lin in synth.model_linears(synth.LLAMA_1B)]
+    rng = np.random.default_rng(2)
+    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 50, with_scale=False):
+        q, sx = oracle.quantize_act(x)
+        acc = a.cpu().numpy()
+        yy = y.cpu().numpy()
+        for j in rng.integers(0, t.shape[0], 16):
+            r = oracle.dot_i32(q[0], t[j])
+            assert acc[j] == r
+            yr = oracle.epilogue(np.array([[r]], np.int32), sx, sw)[0, 0]
+            assert abs(float(yy[j]) - yr) <= RTOL * abs(yr)
