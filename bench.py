@@ -59,7 +59,7 @@ def kernel_source_hash(files) -> str:
 class DecodeStep:
     """Device buffers of COPIES rotated copies of one decode step."""
 
-    def __init__(self, sh, torch, dev, spec, seed, copies=COPIES):
+    def __init__(self, sh, torch, dev, spec, seed, copies=COPIES, keep_host=True):
         self.sh, self.torch, self.dev = sh, torch, dev
         self.lins = synth.model_linears(spec)
         self.count = len(self.lins)
@@ -70,7 +70,8 @@ class DecodeStep:
         host_packed = []
         for i, (layer, lin) in enumerate(self.lins):
             t = synth.ternary_34(lin.n, lin.k, seed, "w", layer, lin.name)
-            self.t.append(t)
+            if keep_host:
+                self.t.append(t)
             host_packed.append(sh.sherry_pack(t))
             self.scales.append(synth.weight_scale(seed, "s", layer, lin.name))
         log("generated+packed %d weights in %.1fs" % (sum(l.n * l.k for _, l in self.lins),
@@ -289,6 +290,118 @@ def bench_prefill(sh, torch, dev, spec, m, seed, reps=10):
 
 
 # ---------------------------------------------------------------------------
+# other decode configurations: LLaMA-3.2-3B and the 8B-scale stress model
+# ---------------------------------------------------------------------------
+
+def time_graph(run, count, torch, replays=5):
+    """us per launch of run(0..count-1), captured once in a HIP graph and
+    replayed (no host launch cost between the kernels)."""
+    for i in range(count):
+        run(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(count):
+                run(i)
+    torch.cuda.synchronize()
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    a, b = _events(torch)
+    a.record()
+    for _ in range(replays):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (replays * count) * 1e3
+
+
+def bench_model_step(sh, torch, dev, spec, seed, copies, steps=100):
+    """One fused decode step (all linears of the model, M = 1) in one launch."""
+    step = DecodeStep(sh, torch, dev, spec, seed, copies=copies, keep_host=False)
+    ms = bench_fused(step, torch, steps, 10)
+    out = {"products": step.count, "copies": copies,
+           "working_set_mb": round(step.weight_bytes * copies / 1e6, 1),
+           "step_us": round(ms * 1e3, 2), "bytes_per_step": step.fused_bytes,
+           "gbs": round(step.fused_bytes / (ms * 1e-3) / 1e9, 1)}
+    out["frac"] = round(out["gbs"] / HBM_PEAK_GBS, 4)
+    del step
+    torch.cuda.empty_cache()
+    return out
+
+
+def _rotation(nbytes, floor=512 << 20):
+    """Copies of a buffer of nbytes that together exceed floor (rotated so
+    that the 256 MB Infinity Cache cannot serve them)."""
+    return max(2, -(-floor // nbytes))
+
+
+def bench_shapes(sh, torch, dev, spec, seed, ms, shapes=("q", "gate", "down"), reps=3):
+    """Per-projection products at M tokens (sherry_gemm, automatic kernel
+    choice), each timed over rotated copies of its weights, launched from a
+    captured graph."""
+    blk = {lin.name: lin for lin in synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])}
+    rows = []
+    for name in shapes:
+        lin = blk[name]
+        t = synth.ternary_34(lin.n, lin.k, seed, "sk", name)
+        packed = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        nb = packed.numel()
+        ws = [packed.clone() for _ in range(_rotation(nb))]
+        for m in ms:
+            x = torch.from_numpy(synth.activations(m, lin.k, seed, "skx", name, m)).to(dev)
+            q = torch.empty((m, lin.k), dtype=torch.int8, device=dev)
+            sx = torch.empty(m, dtype=torch.float32, device=dev)
+            sh.sherry_quantize_act(x, q, sx)
+            y = torch.empty((m, lin.n), dtype=torch.float32, device=dev)
+            run = lambda i: sh.sherry_gemm(ws[i % len(ws)], q, sx, 0.02, y, None, m, lin.n, lin.k)
+            us = time_graph(run, reps * len(ws), torch)
+            byts = nb + m * lin.k + 4 * m + 4 * m * lin.n
+            rows.append({"proj": name, "n": lin.n, "k": lin.k, "m": m, "us": round(us, 3),
+                         "gbs": round(byts / (us * 1e-6) / 1e9, 1),
+                         "tops": round(2.0 * m * lin.n * lin.k / (us * 1e-6) / 1e12, 2),
+                         "kernel": "gemv" if sh.sherry_gemm_kernel_for(m, lin.n, lin.k) ==
+                         sh.SHERRY_KERNEL_GEMV else "mfma"})
+            del x, q, sx, y
+        del ws, packed
+        torch.cuda.empty_cache()
+    return rows
+
+
+def bench_two_bit(sh, torch, dev, spec, seed, shapes=("q", "gate", "down"), reps=3):
+    """The same ternary weights as 1.25-bit codes and as the 2-bit reference
+    layout, M = 1, each timed over rotated copies (launched from a captured
+    graph): time and bytes moved."""
+    blk = {lin.name: lin for lin in synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])}
+    rows = []
+    for name in shapes:
+        lin = blk[name]
+        t = synth.ternary_34(lin.n, lin.k, seed, "tb", name)
+        q = torch.from_numpy(synth.int8_any(1, lin.k, seed, "tbx", name)).to(dev)
+        sx = torch.full((1,), 0.01, dtype=torch.float32, device=dev)
+        y = torch.empty(lin.n, dtype=torch.float32, device=dev)
+        row = {"proj": name, "n": lin.n, "k": lin.k}
+        for fmt, pack, call in (("sherry", sh.sherry_pack, sh.sherry_gemv),
+                                ("two_bit", sh.sherry_pack2, sh.sherry_gemv2)):
+            packed = torch.from_numpy(pack(t)).to(dev)
+            ws = [packed.clone() for _ in range(_rotation(packed.numel()))]
+            run = lambda i: call(ws[i % len(ws)], q, sx, 0.02, y, None, lin.n, lin.k)
+            us = time_graph(run, reps * len(ws), torch)
+            row[fmt + "_bytes"] = packed.numel()
+            row[fmt + "_us"] = round(us, 3)
+            row[fmt + "_gbs"] = round(packed.numel() / (us * 1e-6) / 1e9, 1)
+            del ws, packed
+        row["time_ratio"] = round(row["sherry_us"] / row["two_bit_us"], 3)
+        row["bytes_ratio"] = round(row["sherry_bytes"] / row["two_bit_bytes"], 3)
+        rows.append(row)
+        torch.cuda.empty_cache()
+    return rows
+
+
+# ---------------------------------------------------------------------------
 # CPU baseline: the oracle on the host cores
 # ---------------------------------------------------------------------------
 
@@ -429,6 +542,21 @@ def main():
             pre[name] = bench_prefill(sh, torch, dev, spec, 2048, args.seed)
             log("prefill %s M=2048: %.1f TOPS" % (name, pre[name]["tops"]))
         out["prefill_m2048"] = pre
+        other = {}
+        for name, spec, copies in (("llama-3.2-3b", synth.LLAMA_3B, 2),
+                                   ("stress-8b", synth.STRESS_8B, 1)):
+            other[name] = bench_model_step(sh, torch, dev, spec, args.seed, copies)
+            log("decode step %s (%d products): %.2f us, %.0f GB/s" %
+                (name, other[name]["products"], other[name]["step_us"], other[name]["gbs"]))
+        out["decode_other_models"] = other
+        out["projections_by_m"] = {
+            "llama-3.2-3b": bench_shapes(sh, torch, dev, synth.LLAMA_3B, args.seed, (1, 4, 16)),
+            "stress-8b": bench_shapes(sh, torch, dev, synth.STRESS_8B, args.seed, (1, 64)),
+        }
+        out["two_bit_vs_sherry_8b"] = bench_two_bit(sh, torch, dev, synth.STRESS_8B, args.seed)
+        for r in out["two_bit_vs_sherry_8b"]:
+            log("8b %s: 1.25-bit %.2f us vs 2-bit %.2f us (bytes %.3f, time %.3f)" %
+                (r["proj"], r["sherry_us"], r["two_bit_us"], r["bytes_ratio"], r["time_ratio"]))
     if not args.no_cpu:
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(step)
