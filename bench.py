@@ -333,6 +333,47 @@ def bench_model_step(sh, torch, dev, spec, seed, copies, steps=100):
     return out
 
 
+def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20):
+    """All linears of the model at M tokens in one grouped launch
+    (sherry_gemm_batched, small-M MFMA kernel), int8 activations ready."""
+    lins = synth.model_linears(spec)
+    host = [sh.sherry_pack(synth.ternary_34(l.n, l.k, seed, "w", layer, l.name))
+            for layer, l in lins]
+    sets = []
+    for c in range(copies):
+        w = [torch.from_numpy(p).to(dev) for p in host]
+        ks = sorted({l.k for _, l in lins})
+        q = {kk: torch.randint(-127, 128, (m, kk), dtype=torch.int8, device=dev) for kk in ks}
+        sx = torch.full((m,), 0.01, dtype=torch.float32, device=dev)
+        ys = [torch.empty((m, l.n), dtype=torch.float32, device=dev) for _, l in lins]
+        descs = (sh.sherry_gemm_desc * len(lins))()
+        for i, (_, l) in enumerate(lins):
+            d = descs[i]
+            d.w, d.x, d.x_scale, d.y, d.acc = (w[i].data_ptr(), q[l.k].data_ptr(),
+                                               sx.data_ptr(), ys[i].data_ptr(), None)
+            d.n, d.k, d.m, d.w_scale = l.n, l.k, m, 0.02
+        total, max_m = sh.sherry_gemm_batched_prepare(descs)
+        dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+        sets.append((w, q, sx, ys, dd, total, max_m))
+    run = lambda i: sh.sherry_gemm_batched(sets[i % copies][4], len(lins), sets[i % copies][5],
+                                           sets[i % copies][6])
+    settle(run, torch, 0.02)
+    a, b = _events(torch)
+    a.record()
+    for i in range(reps):
+        run(i)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) / reps * 1e3
+    wbytes = sum(int(p.size) for p in host)
+    byts = wbytes + sum(m * l.k + 4 * m + 4 * m * l.n for _, l in lins)
+    del sets
+    torch.cuda.empty_cache()
+    return {"m": m, "products": len(lins), "step_us": round(us, 2), "bytes_per_step": byts,
+            "gbs": round(byts / (us * 1e-6) / 1e9, 1),
+            "tops": round(sum(2.0 * m * l.n * l.k for _, l in lins) / (us * 1e-6) / 1e12, 1)}
+
+
 def _rotation(nbytes, floor=512 << 20):
     """Copies of a buffer of nbytes that together exceed floor (rotated so
     that the 256 MB Infinity Cache cannot serve them)."""
@@ -549,6 +590,15 @@ def main():
             log("decode step %s (%d products): %.2f us, %.0f GB/s" %
                 (name, other[name]["products"], other[name]["step_us"], other[name]["gbs"]))
         out["decode_other_models"] = other
+        grouped = {"llama-3.2-3b": [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed,
+                                                       mm, 2) for mm in (4, 16)],
+                   "stress-8b": [bench_model_step_m(sh, torch, dev, synth.STRESS_8B, args.seed,
+                                                    64, 1)]}
+        for name, rows in grouped.items():
+            for r in rows:
+                log("grouped step %s M=%d: %.2f us, %.0f GB/s, %.1f TOPS" %
+                    (name, r["m"], r["step_us"], r["gbs"], r["tops"]))
+        out["decode_small_m_grouped"] = grouped
         out["projections_by_m"] = {
             "llama-3.2-3b": bench_shapes(sh, torch, dev, synth.LLAMA_3B, args.seed, (1, 4, 16)),
             "stress-8b": bench_shapes(sh, torch, dev, synth.STRESS_8B, args.seed, (1, 64)),

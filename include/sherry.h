@@ -77,6 +77,8 @@ typedef enum sherry_status {
 #define SHERRY_KERNEL_AUTO 0
 #define SHERRY_KERNEL_GEMV 1 /* VALU decode + dot4 per token, M <= 4         */
 #define SHERRY_KERNEL_MFMA 2 /* decode to int8 tiles in LDS + int8 MFMA      */
+#define SHERRY_KERNEL_SKINNY 3 /* decode in registers + int8 MFMA, M <= 64;
+                                  chosen automatically for 5 <= M <= 32      */
 
 /* Static string for a status code (never NULL). */
 const char* sherry_status_str(int status);
@@ -145,7 +147,8 @@ int sherry_gemm(const uint8_t* w, const int8_t* x, const float* x_scale,
                 int64_t k, void* stream);
 
 /* sherry_gemm with an explicit kernel (SHERRY_KERNEL_*); SHERRY_KERNEL_GEMV
- * requires m <= 4.  Results are bit-identical across kernels. */
+ * requires m <= 4 and SHERRY_KERNEL_SKINNY m <= 64.  Results are
+ * bit-identical across kernels. */
 int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
                    float w_scale, float* y, int32_t* acc, int64_t m,
                    int64_t n, int64_t k, int kernel, void* stream);
@@ -183,6 +186,34 @@ int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
  * device descriptors cannot be re-validated here. */
 int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
                         int64_t total_blocks, void* stream);
+
+/* ---------------------------------------------------------------------- */
+/* Grouped small-M products (1 <= m <= 64 tokens each): many independent  */
+/* products in one launch, on the small-M kernel (SHERRY_KERNEL_SKINNY).   */
+/* ---------------------------------------------------------------------- */
+
+typedef struct sherry_gemm_desc {
+  const uint8_t* w;      /* device, packed n x k, 16-byte aligned          */
+  const int8_t* x;       /* device, int8 [m][k], 16-byte aligned           */
+  const float* x_scale;  /* device, fp32 [m]                               */
+  float* y;              /* device, fp32 [m][n]                            */
+  int32_t* acc;          /* device, int32 [m][n] or NULL                   */
+  int32_t n, k, m;       /* 1 <= m <= 64                                   */
+  float w_scale;
+  int32_t block_begin;   /* written by sherry_gemm_batched_prepare         */
+  int32_t reserved;      /* set to 0                                       */
+} sherry_gemm_desc;
+
+/* Host: validates descs[0..count), fills each block_begin, *total_blocks
+ * and *max_m (the largest m, which selects the launch's staging). */
+int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
+                                int64_t* total_blocks, int32_t* max_m);
+
+/* Runs every product of descs_dev (device, a byte copy of an array accepted
+ * by sherry_gemm_batched_prepare, 8-byte aligned) in one launch; count,
+ * total_blocks and max_m as returned by prepare. */
+int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
+                        int64_t total_blocks, int32_t max_m, void* stream);
 
 /* ---------------------------------------------------------------------- */
 /* Fused quantization + M = 1 product: fp32 activations in, one launch.    */

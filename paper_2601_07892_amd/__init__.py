@@ -26,6 +26,7 @@ SHERRY_E_DEVICE = 6
 SHERRY_KERNEL_AUTO = 0
 SHERRY_KERNEL_GEMV = 1
 SHERRY_KERNEL_MFMA = 2
+SHERRY_KERNEL_SKINNY = 3
 SHERRY_MAX_K = 174720
 SHERRY_FUSED_MAX_K = 32768
 
@@ -35,7 +36,7 @@ EXPORTS = [
     "sherry_gemm_kernel_for", "sherry_gemv_batched_prepare", "sherry_gemv_batched",
     "sherry_packed2_bytes", "sherry_pack2", "sherry_gemv2", "sherry_stream_read",
     "sherry_stream_read_groups", "sherry_gemv_f32", "sherry_gemv_f32_batched_prepare",
-    "sherry_gemv_f32_batched",
+    "sherry_gemv_f32_batched", "sherry_gemm_batched_prepare", "sherry_gemm_batched",
 ]
 
 
@@ -61,6 +62,15 @@ class sherry_gemv_f32_desc(ctypes.Structure):
         ("w", ctypes.c_void_p), ("x", ctypes.c_void_p), ("x_scale", ctypes.c_void_p),
         ("y", ctypes.c_void_p), ("acc", ctypes.c_void_p), ("n", ctypes.c_int64),
         ("k", ctypes.c_int64), ("w_scale", ctypes.c_float), ("block_begin", ctypes.c_int32),
+    ]
+
+
+class sherry_gemm_desc(ctypes.Structure):
+    _fields_ = [
+        ("w", ctypes.c_void_p), ("x", ctypes.c_void_p), ("x_scale", ctypes.c_void_p),
+        ("y", ctypes.c_void_p), ("acc", ctypes.c_void_p), ("n", ctypes.c_int32),
+        ("k", ctypes.c_int32), ("m", ctypes.c_int32), ("w_scale", ctypes.c_float),
+        ("block_begin", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
 
@@ -101,6 +111,9 @@ def _load():
         "sherry_gemv_f32_batched_prepare": ([ctypes.POINTER(sherry_gemv_f32_desc), ctypes.c_int,
                                              i64p], ctypes.c_int),
         "sherry_gemv_f32_batched": ([vp, ctypes.c_int, i64, vp], ctypes.c_int),
+        "sherry_gemm_batched_prepare": ([ctypes.POINTER(sherry_gemm_desc), ctypes.c_int, i64p,
+                                         ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+        "sherry_gemm_batched": ([vp, ctypes.c_int, i64, ctypes.c_int32, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -256,6 +269,22 @@ def sherry_gemv_f32_batched(descs_dev, count: int, total_blocks: int, stream=Non
     """descs_dev: device uint8 tensor holding a byte copy of prepared f32 descriptors."""
     _check(lib.sherry_gemv_f32_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
            "sherry_gemv_f32_batched")
+
+
+def sherry_gemm_batched_prepare(descs) -> tuple[int, int]:
+    """Fills block_begin of a ctypes array of sherry_gemm_desc; returns
+    (total blocks, largest m)."""
+    total = ctypes.c_int64(0)
+    mm = ctypes.c_int32(0)
+    _check(lib.sherry_gemm_batched_prepare(descs, len(descs), ctypes.byref(total),
+                                           ctypes.byref(mm)), "sherry_gemm_batched_prepare")
+    return int(total.value), int(mm.value)
+
+
+def sherry_gemm_batched(descs_dev, count: int, total_blocks: int, max_m: int, stream=None):
+    """descs_dev: device uint8 tensor holding a byte copy of prepared descriptors."""
+    _check(lib.sherry_gemm_batched(_ptr(descs_dev), count, total_blocks, max_m, _stream(stream)),
+           "sherry_gemm_batched")
 
 
 def sherry_gemv2(w2, x, x_scale, w_scale: float, y, acc, n: int, k: int, stream=None):

@@ -36,8 +36,13 @@ int check_fused(const uint8_t* w, const float* x, const float* x_scale, float* y
   return SHERRY_OK;
 }
 
-// Largest M the VALU decode kernel serves; above it the MFMA kernel runs.
+// Largest M the VALU decode kernel serves, the largest the small-M MFMA
+// kernel accepts, and the largest the automatic choice sends to it (measured
+// on LLaMA-3.2-3B / 8B-scale projections, single launches: the small-M kernel
+// is faster up to 32 tokens, the LDS-tiled MFMA kernel from 64 on).
 constexpr int64_t kGemvMaxM = 4;
+constexpr int64_t kSkinnyMaxM = 64;
+constexpr int64_t kSkinnyAutoMaxM = 32;
 
 int check_product(const uint8_t* w, const int8_t* x, const float* x_scale, float* y,
                   int64_t m, int64_t n, int64_t k, uintptr_t x_align) {
@@ -77,7 +82,8 @@ extern "C" int sherry_quantize_act(const float* x, int64_t m, int64_t k, int8_t*
 
 extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
   if (!shape_ok(m, n, k)) return -SHERRY_E_SHAPE;
-  return m <= kGemvMaxM ? SHERRY_KERNEL_GEMV : SHERRY_KERNEL_MFMA;
+  if (m <= kGemvMaxM) return SHERRY_KERNEL_GEMV;
+  return m <= kSkinnyAutoMaxM ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
 }
 
 extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
@@ -93,6 +99,13 @@ extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_
     if (m > kGemvMaxM) return SHERRY_E_SHAPE;
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
     return launch_gemv_valu(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
+  }
+  if (kernel == SHERRY_KERNEL_SKINNY) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 16);
+    if (st != SHERRY_OK) return st;
+    if (m > kSkinnyMaxM) return SHERRY_E_SHAPE;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_skinny(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
   }
   if (kernel == SHERRY_KERNEL_MFMA) {
     int st = check_product(w, x, x_scale, y, m, n, k, 16);
@@ -195,4 +208,35 @@ extern "C" int sherry_gemv_f32_batched(const sherry_gemv_f32_desc* descs_dev, in
     return SHERRY_E_INVALID;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
   return launch_gemv_f32_batched(descs_dev, count, total_blocks, as_stream(stream));
+}
+
+extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
+                                           int64_t* total_blocks, int32_t* max_m) {
+  if (!descs || !total_blocks || !max_m || count < 1) return SHERRY_E_INVALID;
+  int64_t blocks = 0;
+  int32_t mm = 0;
+  for (int i = 0; i < count; ++i) {
+    sherry_gemm_desc& d = descs[i];
+    int st = check_product(d.w, d.x, d.x_scale, d.y, d.m, d.n, d.k, 16);
+    if (st != SHERRY_OK) return st;
+    if (d.m > kSkinnyMaxM) return SHERRY_E_SHAPE;
+    if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
+    d.block_begin = static_cast<int32_t>(blocks);
+    d.reserved = 0;
+    blocks += skinny_blocks(d.n);
+    if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
+    if (d.m > mm) mm = d.m;
+  }
+  *total_blocks = blocks;
+  *max_m = mm;
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
+                                   int64_t total_blocks, int32_t max_m, void* stream) {
+  if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
+    return SHERRY_E_INVALID;
+  if (max_m < 1 || max_m > kSkinnyMaxM) return SHERRY_E_SHAPE;
+  if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
 }

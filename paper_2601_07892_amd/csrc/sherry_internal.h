@@ -160,6 +160,11 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
                      float w_scale, float* y, int32_t* acc, int64_t m,
                      int64_t n, int64_t k, hipStream_t s);
 
+int skinny_blocks(int64_t n);
+int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
+                  float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);
+int launch_skinny_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                          int max_m, hipStream_t s);
 int launch_gemv_batched(const sherry_gemv_desc* descs, int count,
                         int64_t total_blocks, hipStream_t s);
 int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, float w_scale, float* y,

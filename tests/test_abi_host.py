@@ -168,7 +168,9 @@ def test_gemm_validation_without_launch():
 def test_kernel_choice_by_m():
     for m in (1, 2, 3, 4):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_GEMV
-    for m in (5, 16, 64, 2048):
+    for m in (5, 16, 32):
+        assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_SKINNY
+    for m in (33, 64, 2048):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_MFMA
     assert sh.sherry_gemm_kernel_for(0, 2048, 2048) == -sh.SHERRY_E_SHAPE
 
@@ -232,3 +234,31 @@ def test_fused_validation_without_launch():
         sh.sherry_gemv_f32_batched_prepare(descs)
     assert L.sherry_gemv_f32_batched(None, 1, 1, None) == sh.SHERRY_E_INVALID
     assert L.sherry_gemv_f32_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
+
+
+def test_skinny_validation_without_launch():
+    g = L.sherry_gemm_ex
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 65, 64, 128, sh.SHERRY_KERNEL_SKINNY,
+             None) == sh.SHERRY_E_SHAPE
+    assert g(FAKE, FAKE + 4, FAKE, 1.0, FAKE, None, 16, 64, 128, sh.SHERRY_KERNEL_SKINNY,
+             None) == sh.SHERRY_E_ALIGN
+    cases = [(16, 2048, 2048), (64, 8192, 2048), (1, 70, 132)]
+    descs = (sh.sherry_gemm_desc * len(cases))()
+    for i, (m, n, k) in enumerate(cases):
+        d = descs[i]
+        d.w, d.x, d.x_scale, d.y, d.acc = FAKE, FAKE, FAKE, FAKE, None
+        d.m, d.n, d.k, d.w_scale = m, n, k, 0.02
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    # one workgroup per 8 row tiles: 32 tiles -> 4, 128 -> 16, 2 -> 1
+    assert [d.block_begin for d in descs] == [0, 4, 20] and total == 21 and max_m == 64
+    assert ctypes.sizeof(sh.sherry_gemm_desc) == 64
+    descs[1].m = 65
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemm_batched_prepare(descs)
+    descs[1].m = 64
+    descs[2].x = FAKE + 4
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemm_batched_prepare(descs)
+    assert L.sherry_gemm_batched(FAKE, 1, 1, 65, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 16, None) == sh.SHERRY_E_ALIGN
+    assert L.sherry_gemm_batched(None, 1, 1, 16, None) == sh.SHERRY_E_INVALID

@@ -552,3 +552,95 @@ def test_fused_batched_decode_step_llama_1b(dev):
             assert acc[j] == r
             yr = oracle.epilogue(np.array([[r]], np.int32), sx, sw)[0, 0]
             assert abs(float(yy[j]) - yr) <= RTOL * abs(yr)
+
+
+# ------------------------------------------------- small-M MFMA (M <= 64)
+
+SKINNY_CASES = [(5, 64, 128), (16, 65, 132), (32, 300, 1032), (33, 130, 2048), (64, 512, 1024),
+                (1, 64, 128), (4, 257, 3076), (17, 1000, 2056), (64, 70, 4), (48, 3072, 8192)]
+
+
+@pytest.mark.parametrize("m,n,k", SKINNY_CASES)
+def test_skinny_kernel_parity(dev, m, n, k):
+    # ragged n (partial 64-row tiles and 8-tile workgroups), ragged k (partial
+    # containers, k % 16 != 0 rows, chunk boundaries), 1..64 tokens
+    sh = _sh()
+    _say("skinny", m, n, k)
+    t = synth.ternary_34(n, k, 51, "sk", n, k)
+    q = synth.int8_any(m, k, 51, "sk", m, k)
+    sx = np.abs(synth.activations(1, m, 51, "sks", m)[0]).astype(np.float32) + 0.01
+    sw = synth.weight_scale(51, "sk", n, k)
+    y, acc = _run(dev, t, q, sx, sw, sh.SHERRY_KERNEL_SKINNY, m)
+    acc_ref = oracle.gemm_i32(q, t, threads=8)
+    assert np.array_equal(acc, acc_ref)
+    assert _y_ok(y, oracle.epilogue(acc_ref, sx, sw))
+
+
+def test_skinny_extreme_values(dev):
+    # all activations -128 or 127 and all-ones / all-minus patterns: the
+    # largest |acc| the kernel can meet at this K
+    sh = _sh()
+    m, n, k = 40, 128, 4096
+    q = np.where(synth.int8_any(m, k, 52, "ext") >= 0, 127, -128).astype(np.int8)
+    t = synth.ternary_34(n, k, 52, "ext")
+    y, acc = _run(dev, t, q, np.ones(m, np.float32), 1.0, sh.SHERRY_KERNEL_SKINNY, m)
+    assert np.array_equal(acc, oracle.gemm_i32(q, t, threads=8))
+
+
+def _skinny_batched(dev, cases, seed):
+    sh = _sh()
+    descs = (sh.sherry_gemm_desc * len(cases))()
+    keep = []
+    for i, (m, n, k) in enumerate(cases):
+        t = synth.ternary_34(n, k, seed, "sb", i)
+        q = synth.int8_any(m, k, seed, "sbq", i)
+        sx = np.abs(synth.activations(1, m, seed, "sbs", i)[0]).astype(np.float32) + 0.01
+        sw = synth.weight_scale(seed, "sbw", i)
+        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        qd = torch.from_numpy(q).to(dev)
+        sxd = torch.from_numpy(sx).to(dev)
+        y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+        a = torch.full((m, n), -7, dtype=torch.int32, device=dev)
+        d = descs[i]
+        d.w, d.x, d.x_scale, d.y, d.acc = (w.data_ptr(), qd.data_ptr(), sxd.data_ptr(),
+                                           y.data_ptr(), a.data_ptr())
+        d.n, d.k, d.m, d.w_scale = n, k, m, sw
+        keep.append((t, q, sx, sw, w, qd, sxd, y, a))
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+    sh.sherry_gemm_batched(dd, len(cases), total, max_m)
+    torch.cuda.synchronize()
+    return keep, max_m
+
+
+@pytest.mark.parametrize("big", [False, True])
+def test_skinny_batched_parity(dev, big):
+    _say("skinny batched", big)
+    cases = [(5, 64, 128), (16, 65, 132), (1, 600, 2048), (32, 512, 3072), (8, 130, 1032)]
+    if big:
+        cases += [(64, 300, 2052), (40, 64, 4)]
+    keep, max_m = _skinny_batched(dev, cases, 53)
+    assert max_m == max(c[0] for c in cases)
+    for t, q, sx, sw, w, qd, sxd, y, a in keep:
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a.cpu().numpy(), acc_ref)
+        assert _y_ok(y.cpu().numpy(), oracle.epilogue(acc_ref, sx, sw))
+
+
+@pytest.mark.parametrize("spec_name,m", [("LLAMA_3B", 16), ("STRESS_8B", 64)])
+def test_skinny_batched_model_step_sampled(dev, spec_name, m):
+    # every linear of one layer of the model at M tokens in one grouped
+    # launch (the configurations the benchmark times), sampled outputs
+    _say("skinny step", spec_name, m)
+    spec = getattr(synth, spec_name)
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    keep, _ = _skinny_batched(dev, [(m, lin.n, lin.k) for lin in blk], 54)
+    rng = np.random.default_rng(3)
+    for t, q, sx, sw, w, qd, sxd, y, a in keep:
+        acc = a.cpu().numpy()
+        yy = y.cpu().numpy()
+        for i, j in zip(rng.integers(0, q.shape[0], 40), rng.integers(0, t.shape[0], 40)):
+            r = oracle.dot_i32(q[i], t[j])
+            assert acc[i, j] == r
+            yr = oracle.epilogue(np.array([[r]], np.int32), sx[i:i + 1], sw)[0, 0]
+            assert abs(float(yy[i, j]) - yr) <= RTOL * abs(yr)
