@@ -186,28 +186,52 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
     for (int bb = 0; bb < G::FN; ++bb) acc[a][bb] = v16i{};
 
   const int frow = lane & 31, fhalf = lane >> 5;
-  // MFMAs of one step from a stage: four 32-wide k slices
+  // MFMAs of one step from a stage: four 32-wide k slices.  The fragments of
+  // slice t+1 are read into the other register set before the MFMAs of
+  // slice t are issued, so the LDS latency hides behind those MFMAs.
   auto compute = [&](const int8_t* stage) {
     const int8_t* xs = stage;
     const int8_t* ws = stage + G::LDS_X;
-#pragma unroll
-    for (int t = 0; t < kBK / 32; ++t) {
-      v4i af[G::FM], bf[G::FN];
+    v4i af[2][G::FM], bf[2][G::FN];
+    auto read = [&](int t, int set) {
 #pragma unroll
       for (int a = 0; a < G::FM; ++a) {
         const int row = wr * G::WM + a * 32 + frow;
-        af[a] = *reinterpret_cast<const v4i*>(xs + swz(row, 2 * t + fhalf));
+        af[set][a] = *reinterpret_cast<const v4i*>(xs + swz(row, 2 * t + fhalf));
       }
 #pragma unroll
       for (int bb = 0; bb < G::FN; ++bb) {
         const int row = wc * G::WN + bb * 32 + frow;
-        bf[bb] = *reinterpret_cast<const v4i*>(ws + swz(row, 2 * t + fhalf));
+        bf[set][bb] = *reinterpret_cast<const v4i*>(ws + swz(row, 2 * t + fhalf));
       }
+    };
+    read(0, 0);
+#pragma unroll
+    for (int t = 0; t < kBK / 32; ++t) {
+      if (t + 1 < kBK / 32) read(t + 1, (t + 1) & 1);
 #pragma unroll
       for (int a = 0; a < G::FM; ++a)
 #pragma unroll
         for (int bb = 0; bb < G::FN; ++bb)
-          acc[a][bb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[a], bf[bb], acc[a][bb], 0, 0, 0);
+          acc[a][bb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[t & 1][a], bf[t & 1][bb],
+                                                             acc[a][bb], 0, 0, 0);
+    }
+    // schedule: slice 0's reads, then per slice the next slice's reads
+    // interleaved with this slice's MFMAs (the scheduler would otherwise
+    // reuse one register set and wait on every read)
+    __builtin_amdgcn_sched_group_barrier(0x100, G::FM + G::FN, 0);
+#pragma unroll
+    for (int t = 0; t < kBK / 32; ++t) {
+      if (t + 1 < kBK / 32) {
+#pragma unroll
+        for (int i = 0; i < G::FM + G::FN; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, G::FM * G::FN - (G::FM + G::FN), 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, G::FM * G::FN, 0);
+      }
     }
   };
 
