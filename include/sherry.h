@@ -77,8 +77,7 @@ typedef enum sherry_status {
 #define SHERRY_KERNEL_AUTO 0
 #define SHERRY_KERNEL_GEMV 1 /* VALU decode + dot4 per token, M <= 4         */
 #define SHERRY_KERNEL_MFMA 2 /* decode to int8 tiles in LDS + int8 MFMA      */
-#define SHERRY_KERNEL_SKINNY 3 /* decode in registers + int8 MFMA, M <= 64;
-                                  chosen automatically for 5 <= M <= 32      */
+#define SHERRY_KERNEL_SKINNY 3 /* decode in registers + int8 MFMA, M <= 64   */
 
 /* Static string for a status code (never NULL). */
 const char* sherry_status_str(int status);

@@ -36,13 +36,12 @@ int check_fused(const uint8_t* w, const float* x, const float* x_scale, float* y
   return SHERRY_OK;
 }
 
-// Largest M the VALU decode kernel serves, the largest the small-M MFMA
-// kernel accepts, and the largest the automatic choice sends to it (measured
-// on LLaMA-3.2-3B / 8B-scale projections, single launches: the small-M kernel
-// is faster up to 32 tokens, the LDS-tiled MFMA kernel from 64 on).
+// Largest M the VALU decode kernel serves and the largest the small-M MFMA
+// kernel serves (measured on LLaMA-3.2-3B / 8B-scale projections, single
+// launches: the VALU kernel is faster up to 4 tokens, the small-M kernel up
+// to its limit of 64); above it the LDS-tiled MFMA kernel runs.
 constexpr int64_t kGemvMaxM = 4;
 constexpr int64_t kSkinnyMaxM = 64;
-constexpr int64_t kSkinnyAutoMaxM = 32;
 
 int check_product(const uint8_t* w, const int8_t* x, const float* x_scale, float* y,
                   int64_t m, int64_t n, int64_t k, uintptr_t x_align) {
@@ -83,7 +82,7 @@ extern "C" int sherry_quantize_act(const float* x, int64_t m, int64_t k, int8_t*
 extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
   if (!shape_ok(m, n, k)) return -SHERRY_E_SHAPE;
   if (m <= kGemvMaxM) return SHERRY_KERNEL_GEMV;
-  return m <= kSkinnyAutoMaxM ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
+  return m <= kSkinnyMaxM ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
 }
 
 extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,

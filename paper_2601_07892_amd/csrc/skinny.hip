@@ -113,33 +113,51 @@ __device__ __forceinline__ void sk_lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Workgroup g of problem p (tiles 8g .. 8g+7).  lut and xs are LDS.
-template <int MT>
+// Workgroup g of problem p: tiles T*g .. T*g+T-1 (T = 8/S), each split along
+// K over S waves (wave w: tile w/S, split w%S).  Split s owns units
+// [s*U, min((s+1)*U, C)) with U = ceil(C/S); all waves walk their ranges in
+// lockstep chunks of UPC_S = UPC/S units, and a stage holds, for every
+// token, the S splits' windows side by side.  With S > 1 the partial
+// accumulators meet in LDS (over the stages) and split 0 writes the tile.
+template <int MT, int S>
 __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32_t* lut,
                                          int8_t* xs) {
   using G = SkCfg<MT>;
+  static_assert(S >= 1 && G::UPC % S == 0, "splits divide a chunk");
+  constexpr int T = kSkWaves / S;   // tiles per workgroup
+  constexpr int UPS = G::UPC / S;   // units per split per chunk
+  constexpr int WIN = UPS * kTileK; // K values per split window
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int C = (p.k + kTileK - 1) / kTileK;
   const int R = (p.n + kTileRows - 1) / kTileRows;
-  const int r = g * kSkWaves + wave;
-  const bool live = r < R;
+  const int U = (C + S - 1) / S;    // units per split
+  const int r = g * T + wave / S;
+  const int sp = wave % S;
+  const int u0 = sp * U, u1 = (u0 + U < C) ? u0 + U : C;
+  const bool live = r < R && u0 < u1;
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(p.w) + int64_t(live ? r : 0) * C * kUnitBytes, 0,
-      live ? C * kUnitBytes : 0, kBufferWord3);
-  const int nch = (C + G::UPC - 1) / G::UPC;
+      const_cast<uint8_t*>(p.w) + (int64_t(r < R ? r : 0) * C + (live ? u0 : 0)) * kUnitBytes, 0,
+      live ? (u1 - u0) * kUnitBytes : 0, kBufferWord3);
+  const int nch = (U + UPS - 1) / UPS;
   const bool k16 = (p.k & 15) == 0;
 
   // activation chunk ch -> registers: piece q = tid + threads*v is token
-  // q / (KC/16), 16 bytes at K offset 16 * (q % (KC/16)); zero past m and k
+  // q / (KC/16), 16 bytes at window offset 16 * (q % (KC/16)): split
+  // window s = offset / WIN, K = (s*U + ch*UPS)*128 + offset % WIN; zero past
+  // m, past k and past the split's end
   uint4 sv[G::SPT];
   auto stage_load = [&](int ch) {
 #pragma unroll
     for (int v = 0; v < G::SPT; ++v) {
       const int q = tid + kSkThreads * v;
-      const int tok = q / (G::KC / 16), kk = ch * G::KC + 16 * (q % (G::KC / 16));
+      const int tok = q / (G::KC / 16), o = 16 * (q % (G::KC / 16));
+      const int ws = o / WIN, wo = o % WIN;
+      const int ub = ws * U + ch * UPS;  // first unit of this window
+      const int kk = ub * kTileK + wo;
+      const int kend = (ws * U + U < C ? ws * U + U : C) * kTileK;
       uint4 val = make_uint4(0, 0, 0, 0);
-      if (tok < p.m && kk < p.k) {
+      if (tok < p.m && kk < p.k && kk < kend) {
         const int8_t* src = p.x + int64_t(tok) * p.k + kk;
         if (k16) {
           val = *reinterpret_cast<const uint4*>(as_global(src));
@@ -171,6 +189,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
 
   stage_load(0);
   stage_store(0);
+  if (nch > 1) stage_load(1);
   uint32_t ring[kSkRing][5];
 #pragma unroll
   for (int u = 0; u < kSkRing; ++u) {
@@ -179,26 +198,57 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   }
   sk_lds_barrier();  // stage 0 and the table are ready
 
-  for (int ch = 0; ch < nch; ++ch) {
-    if (ch + 1 < nch) stage_load(ch + 1);
-    const int8_t* xb = xs + (ch & 1) * G::STAGE;
-    for (int i = 0; i < G::UPC; i += kSkRing) {
+  // unit j of the split (relative to u0) lives in chunk j / UPS; at each
+  // chunk boundary the next stage (in registers) is written and the one
+  // after it is loaded
+  const int nunits = nch * UPS;
+  for (int j = 0; j < nunits; j += kSkRing) {
 #pragma unroll
-      for (int u = 0; u < kSkRing; ++u) {
-        const int cc = ch * G::UPC + i + u;
-        if (live && cc < C) sk_container<MT>(ring[u], xb, (i + u) * kTileK, lut, c);
-        __builtin_amdgcn_sched_barrier(0);
-        sk_load_container(ring[u], rs, cc + kSkRing, lane);
-        __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < kSkRing; ++u) {
+      const int jj = j + u;
+      const int ch = jj / UPS;
+      if (jj % UPS == 0 && jj > 0) {
+        stage_store(ch & 1);
+        sk_lds_barrier();
+        if (ch + 1 < nch) stage_load(ch + 1);
       }
+      const int8_t* xb = xs + (ch & 1) * G::STAGE + sp * WIN;
+      if (live && u0 + jj < u1) sk_container<MT>(ring[u], xb, (jj % UPS) * kTileK, lut, c);
+      __builtin_amdgcn_sched_barrier(0);
+      sk_load_container(ring[u], rs, jj + kSkRing, lane);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (ch + 1 < nch) stage_store((ch + 1) & 1);
-    sk_lds_barrier();
   }
 
-  // epilogue: lane holds C[token][row] for row = 32h + lane%32 of the tile
-  // and token = 32tb + 8(e/4) + 4(lane/32) + e%4, e = accumulator element
-  if (!live) return;
+  if constexpr (S > 1) {
+    // partial sums of the S splits of a tile through LDS (the stages are
+    // free now), one token block at a time: [wave][h][element][lane]
+    int32_t* red = reinterpret_cast<int32_t*>(xs);
+    static_assert(kSkWaves * 2 * 16 * 64 * 4 <= 2 * G::STAGE, "reduction fits the stages");
+#pragma unroll
+    for (int tb = 0; tb < MT; ++tb) {
+      sk_lds_barrier();
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) red[((wave * 2 + h) * 16 + e) * 64 + lane] = c[h][tb][e];
+      sk_lds_barrier();
+      if (sp == 0) {
+#pragma unroll
+        for (int q = 1; q < S; ++q)
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              c[h][tb][e] += red[(((wave + q) * 2 + h) * 16 + e) * 64 + lane];
+      }
+    }
+  }
+
+  // epilogue (split 0 of each tile): lane holds C[token][row] for row =
+  // 32h + lane%32 of the tile and token = 32tb + 8(e/4) + 4(lane/32) + e%4,
+  // e = accumulator element
+  if (r >= R || sp != 0) return;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int row = r * kTileRows + 32 * h + (lane & 31);
@@ -218,12 +268,12 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   }
 }
 
-template <int MT>
+template <int MT, int S>
 __global__ __launch_bounds__(kSkThreads) void skinny_kernel(SkProblem p) {
   __shared__ __attribute__((aligned(16))) int8_t lds[kSkLutBytes + 2 * SkCfg<MT>::STAGE];
   uint32_t* lut = reinterpret_cast<uint32_t*>(lds);
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
-  sk_block<MT>(p, blockIdx.x, lut, lds + kSkLutBytes);
+  sk_block<MT, S>(p, blockIdx.x, lut, lds + kSkLutBytes);
 }
 
 template <int MT>
@@ -248,20 +298,49 @@ __global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
   const SkProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m, d.w_scale};
-  sk_block<MT>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
+  sk_block<MT, 1>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
 }
 
 }  // namespace
 
 int skinny_blocks(int64_t n) { return static_cast<int>(ceil_div(ceil_div(n, kTileRows), kSkWaves)); }
 
+// K splits per tile of a lone launch: the smallest power of two (up to a
+// chunk's units) that gives the launch at least kSkMinBlocks workgroups, so
+// that small-N products still spread over many CUs.
+constexpr int64_t kSkMinBlocks = 192;
+
+template <int MT, int S>
+int launch_skinny_s(const SkProblem& p, hipStream_t s) {
+  const int64_t R = ceil_div(p.n, kTileRows);
+  const dim3 grid(static_cast<unsigned>(ceil_div(R, kSkWaves / S))), block(kSkThreads);
+  return launch(skinny_kernel<MT, S>, grid, block, 0, s, p);
+}
+
+template <int MT>
+int launch_skinny_mt(const SkProblem& p, hipStream_t s) {
+  const int64_t R = ceil_div(p.n, kTileRows);
+  const int64_t C = ceil_div(p.k, kTileK);
+  int S = 1;
+  while (S < SkCfg<MT>::UPC && S < kSkWaves && ceil_div(R, kSkWaves / S) < kSkMinBlocks &&
+         C >= 2 * S)
+    S *= 2;
+  switch (S) {
+    case 1: return launch_skinny_s<MT, 1>(p, s);
+    case 2: return launch_skinny_s<MT, 2>(p, s);
+    case 4: return launch_skinny_s<MT, 4>(p, s);
+    default:
+      if constexpr (SkCfg<MT>::UPC >= 8) return launch_skinny_s<MT, 8>(p, s);
+      return launch_skinny_s<MT, 4>(p, s);
+  }
+}
+
 int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
                   float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
   const SkProblem p{w, x, x_scale, y, acc, static_cast<int>(n), static_cast<int>(k),
                     static_cast<int>(m), w_scale};
-  const dim3 grid(static_cast<unsigned>(skinny_blocks(n))), block(kSkThreads);
-  if (m <= 32) return launch(skinny_kernel<1>, grid, block, 0, s, p);
-  return launch(skinny_kernel<2>, grid, block, 0, s, p);
+  if (m <= 32) return launch_skinny_mt<1>(p, s);
+  return launch_skinny_mt<2>(p, s);
 }
 
 int launch_skinny_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,

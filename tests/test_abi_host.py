@@ -168,9 +168,9 @@ def test_gemm_validation_without_launch():
 def test_kernel_choice_by_m():
     for m in (1, 2, 3, 4):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_GEMV
-    for m in (5, 16, 32):
+    for m in (5, 16, 32, 64):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_SKINNY
-    for m in (33, 64, 2048):
+    for m in (65, 2048):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_MFMA
     assert sh.sherry_gemm_kernel_for(0, 2048, 2048) == -sh.SHERRY_E_SHAPE
 

@@ -556,8 +556,13 @@ def test_fused_batched_decode_step_llama_1b(dev):
 
 # ------------------------------------------------- small-M MFMA (M <= 64)
 
+# A lone launch splits K over S = 1, 2, 4 or 8 waves per tile (more splits
+# for fewer tiles, at most half the containers): these cover every S for 32-
+# and 64-token staging, splits that end early or own no container, and the
+# LDS reduction of the partial sums.
 SKINNY_CASES = [(5, 64, 128), (16, 65, 132), (32, 300, 1032), (33, 130, 2048), (64, 512, 1024),
-                (1, 64, 128), (4, 257, 3076), (17, 1000, 2056), (64, 70, 4), (48, 3072, 8192)]
+                (1, 64, 128), (4, 257, 3076), (17, 1000, 2056), (64, 70, 4), (48, 3072, 8192),
+                (40, 100, 384), (20, 200, 896), (9, 16384, 256)]
 
 
 @pytest.mark.parametrize("m,n,k", SKINNY_CASES)
