@@ -36,6 +36,7 @@ sys.path.insert(0, ROOT)
 import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+KERNEL_NAMES = {1: "gemv", 2: "mfma", 3: "skinny"}  # SHERRY_KERNEL_* values
 INT8_PEAK_TOPS = 5000.0
 COPIES = 16  # rotated copies of the weights: 16 x 152 MB = 2.4 GB, ~10x the Infinity Cache
 
@@ -281,7 +282,8 @@ def bench_prefill(sh, torch, dev, spec, m, seed, reps=10):
         tot_ops += ops
         tot_ms += ms
         rows.append({"proj": lin.name, "n": lin.n, "k": lin.k, "us": round(ms * 1e3, 2),
-                     "tops": round(ops / (ms * 1e-3) / 1e12, 1)})
+                     "tops": round(ops / (ms * 1e-3) / 1e12, 1),
+                     "kernel": KERNEL_NAMES[sh.sherry_gemm_kernel_for(m, lin.n, lin.k)]})
         del w, x, q, y
     return {"m": m, "per_layer_us": round(tot_ms * 1e3, 2),
             "tops": round(tot_ops / (tot_ms * 1e-3) / 1e12, 1),
@@ -404,8 +406,7 @@ def bench_shapes(sh, torch, dev, spec, seed, ms, shapes=("q", "gate", "down"), r
             rows.append({"proj": name, "n": lin.n, "k": lin.k, "m": m, "us": round(us, 3),
                          "gbs": round(byts / (us * 1e-6) / 1e9, 1),
                          "tops": round(2.0 * m * lin.n * lin.k / (us * 1e-6) / 1e12, 2),
-                         "kernel": "gemv" if sh.sherry_gemm_kernel_for(m, lin.n, lin.k) ==
-                         sh.SHERRY_KERNEL_GEMV else "mfma"})
+                         "kernel": KERNEL_NAMES[sh.sherry_gemm_kernel_for(m, lin.n, lin.k)]})
             del x, q, sx, y
         del ws, packed
         torch.cuda.empty_cache()

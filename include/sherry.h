@@ -73,11 +73,12 @@ typedef enum sherry_status {
  * quantized row is staged on chip). */
 #define SHERRY_FUSED_MAX_K 32768
 
-/* Kernel selectors for sherry_gemm_ex (the automatic choice is by M). */
+/* Kernel selectors for sherry_gemm_ex (see sherry_gemm_kernel_for for the
+ * automatic choice). */
 #define SHERRY_KERNEL_AUTO 0
 #define SHERRY_KERNEL_GEMV 1 /* VALU decode + dot4 per token, M <= 4         */
 #define SHERRY_KERNEL_MFMA 2 /* decode to int8 tiles in LDS + int8 MFMA      */
-#define SHERRY_KERNEL_SKINNY 3 /* decode in registers + int8 MFMA, M <= 64   */
+#define SHERRY_KERNEL_SKINNY 3 /* decode in registers + int8 MFMA, any M     */
 
 /* Static string for a status code (never NULL). */
 const char* sherry_status_str(int status);
@@ -146,14 +147,14 @@ int sherry_gemm(const uint8_t* w, const int8_t* x, const float* x_scale,
                 int64_t k, void* stream);
 
 /* sherry_gemm with an explicit kernel (SHERRY_KERNEL_*); SHERRY_KERNEL_GEMV
- * requires m <= 4 and SHERRY_KERNEL_SKINNY m <= 64.  Results are
- * bit-identical across kernels. */
+ * requires m <= 4.  Results are bit-identical across kernels. */
 int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
                    float w_scale, float* y, int32_t* acc, int64_t m,
                    int64_t n, int64_t k, int kernel, void* stream);
 
-/* The kernel sherry_gemm picks for this shape (SHERRY_KERNEL_GEMV or
- * SHERRY_KERNEL_MFMA), or -SHERRY_E_SHAPE for an invalid shape. */
+/* The kernel sherry_gemm picks for this shape, or -SHERRY_E_SHAPE for an
+ * invalid shape: SHERRY_KERNEL_GEMV for m <= 4, SHERRY_KERNEL_SKINNY for
+ * 5 <= m <= 512 or k > n, else SHERRY_KERNEL_MFMA. */
 int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k);
 
 /* ---------------------------------------------------------------------- */

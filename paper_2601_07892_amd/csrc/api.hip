@@ -41,7 +41,12 @@ int check_fused(const uint8_t* w, const float* x, const float* x_scale, float* y
 // launches: the VALU kernel is faster up to 4 tokens, the small-M kernel up
 // to its limit of 64); above it the LDS-tiled MFMA kernel runs.
 constexpr int64_t kGemvMaxM = 4;
-constexpr int64_t kSkinnyMaxM = 64;
+// Above this many tokens the LDS-tiled kernel takes products with k <= n
+// (the register-decoded kernel keeps those with k > n): the faster of the two
+// on the LLaMA projection shapes at M = 1024 and 2048.
+constexpr int64_t kSkinnyMaxM = 512;
+// Largest m of one product in a grouped small-M launch (one token block).
+constexpr int64_t kBatchedMaxM = 64;
 
 int check_product(const uint8_t* w, const int8_t* x, const float* x_scale, float* y,
                   int64_t m, int64_t n, int64_t k, uintptr_t x_align) {
@@ -82,7 +87,7 @@ extern "C" int sherry_quantize_act(const float* x, int64_t m, int64_t k, int8_t*
 extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
   if (!shape_ok(m, n, k)) return -SHERRY_E_SHAPE;
   if (m <= kGemvMaxM) return SHERRY_KERNEL_GEMV;
-  return m <= kSkinnyMaxM ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
+  return (m <= kSkinnyMaxM || k > n) ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
 }
 
 extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
@@ -102,7 +107,6 @@ extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_
   if (kernel == SHERRY_KERNEL_SKINNY) {
     int st = check_product(w, x, x_scale, y, m, n, k, 16);
     if (st != SHERRY_OK) return st;
-    if (m > kSkinnyMaxM) return SHERRY_E_SHAPE;
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
     return launch_skinny(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
   }
@@ -218,7 +222,7 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
     sherry_gemm_desc& d = descs[i];
     int st = check_product(d.w, d.x, d.x_scale, d.y, d.m, d.n, d.k, 16);
     if (st != SHERRY_OK) return st;
-    if (d.m > kSkinnyMaxM) return SHERRY_E_SHAPE;
+    if (d.m > kBatchedMaxM) return SHERRY_E_SHAPE;
     if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
     d.reserved = 0;
@@ -235,7 +239,7 @@ extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
                                    int64_t total_blocks, int32_t max_m, void* stream) {
   if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
     return SHERRY_E_INVALID;
-  if (max_m < 1 || max_m > kSkinnyMaxM) return SHERRY_E_SHAPE;
+  if (max_m < 1 || max_m > kBatchedMaxM) return SHERRY_E_SHAPE;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
   return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
 }

@@ -1,11 +1,13 @@
-// Small-M product (a few to 64 tokens; Eq. 2): the weight stream of the
-// decode kernel, with the multiply-accumulate on int8 MFMA.
+// Register-decoded int8-MFMA product (Eq. 2), for any number of tokens:
+// the weight stream of the decode kernel, with the multiply-accumulate on
+// int8 MFMA.  Its first use is small M (a few to 128 tokens), where the
+// weights dominate the traffic; larger M runs as a grid of 128-token blocks.
 //
-// Work mapping.  A workgroup is 8 waves; wave w owns 64-row tile 8*g + w and
-// streams all of its containers in order (no split along K, so no partial
-// sums to combine).  The waves walk K in lockstep chunks: the activations of
-// chunk ch (all tokens, kSkChunk/MT values each) sit in one of two LDS
-// stages while the next chunk is loaded into registers.
+// Work mapping.  A workgroup is 8 waves; wave w owns 64-row tile 8g + w/S and
+// part w%S of its containers along K (S = 1 unless a lone launch has too few
+// tiles to fill the GPU).  The waves walk K in lockstep chunks; the
+// activations of a chunk (every staged token) arrive in LDS by DMA loads,
+// several chunks ahead of their use.
 //
 // Per container (64 rows x 128 weights) a wave decodes its 32 codes per lane
 // through the 32-entry table (lane i = row i), exactly as the decode kernel
@@ -21,23 +23,28 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kSkWaves = 8;
 constexpr int kSkThreads = 64 * kSkWaves;
 constexpr int kSkRing = 4;        // containers per wave in the register ring
 constexpr int kSkLutBytes = 128;  // the code table, at LDS address 0
-// K values per staged chunk and token block count: MT blocks of 32 tokens
-// share 32 KB per stage (chunk = 1024 / MT values, a multiple of the ring)
-template <int MT>
+constexpr int kSkOutside = 0x7FFFFFF0;  // a buffer offset past any range: loads read zero
+// Staging geometry for MT blocks of 32 tokens: a stage holds every staged
+// token's KC = 1024/MT activations (32 KB), filled by LDS-DMA loads of 1 KB
+// per wave instruction; NST stages form a ring, so the loads for chunk ch + NST
+// - 1 are in flight while chunk ch is multiplied.
+template <int MT, int NST>
 struct SkCfg {
-  static constexpr int TOK = 32 * MT;             // staged token rows
-  static constexpr int KC = 1024 / MT;            // K values per chunk
-  static constexpr int ROW = KC + 16;             // LDS row stride (bank skew)
-  static constexpr int UPC = KC / kTileK;         // containers per chunk
-  static constexpr int STAGE = TOK * ROW;
-  static constexpr int SPT = TOK * KC / 16 / kSkThreads;  // 16-byte pieces per thread
-  static_assert(UPC % kSkRing == 0, "chunks hold whole ring turns");
-  static_assert(SPT * 16 * kSkThreads == TOK * KC, "stage split");
+  static constexpr int TOK = 32 * MT;        // staged token rows
+  static constexpr int KC = 1024 / MT;       // K values per chunk (row bytes in a stage)
+  static constexpr int CPR = KC / 16;        // 16-byte pieces per row
+  static constexpr int UPC = KC / kTileK;    // containers per chunk
+  static constexpr int STAGE = TOK * KC;
+  static constexpr int SPT = STAGE / 1024 / kSkWaves;  // DMA instructions per wave per chunk
+  static constexpr int LDS = kSkLutBytes + NST * STAGE;
+  static_assert(SPT * 1024 * kSkWaves == STAGE && CPR >= 16, "stage split");
+  static_assert(NST >= 2 && LDS <= 160 * 1024, "stages fit the LDS");
 };
 
 // One product of a batch (or the whole single-product launch).
@@ -51,6 +58,16 @@ struct SkProblem {
   float w_scale;
 };
 
+// Waits until at most N vector-memory loads of this wave are outstanding
+// (loads complete in issue order); the other counters are left alone.
+template <int N>
+__device__ __forceinline__ void sk_wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // simm16: vmcnt[3:0] at bits 3:0, expcnt 6:4, lgkmcnt 11:8, vmcnt[5:4] at 15:14
+  constexpr int kImm = (N & 15) | (7 << 4) | (15 << 8) | (((N >> 4) & 3) << 14);
+  __builtin_amdgcn_s_waitcnt(static_cast<int16_t>(kImm));
+}
+
 __device__ __forceinline__ void sk_load_container(uint32_t (&d)[5], __amdgpu_buffer_rsrc_t r,
                                                   int c, int lane) {
   const u32x4 h =
@@ -63,47 +80,86 @@ __device__ __forceinline__ void sk_load_container(uint32_t (&d)[5], __amdgpu_buf
                                               kLoadStream);
 }
 
+// One 16-byte LDS-DMA load per lane: lane i's bytes land at dst + 16 i.
+__device__ __forceinline__ void sk_dma(__amdgpu_buffer_rsrc_t r, int8_t* dst, int voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voffset, 0, 0, 0);
+}
+
 template <int j0, int... js>
 __device__ __forceinline__ void sk_offsets(const uint32_t (&d)[5], uint32_t* a4,
                                            std::integer_sequence<int, js...>) {
   ((a4[js] = code_x4<j0 + js>(d)), ...);
 }
 
-// Decodes container d and accumulates its 128 K values against the staged
-// activations xb (row stride ROW, K offset koff) into c[row group][token block].
-template <int MT>
-__device__ __forceinline__ void sk_container(const uint32_t (&d)[5], const int8_t* xb,
-                                             int koff, const uint32_t* lut,
-                                             v16i (&c)[2][MT]) {
-  using G = SkCfg<MT>;
-  const int lane = threadIdx.x & 63;
+// Table lookups of container d's 32 codes (lane i = row i): wv[j] holds the
+// int8x4 weights of K values 4j .. 4j+3 of the lane's row.
+__device__ __forceinline__ void sk_lookup(const uint32_t (&d)[5], const uint32_t* lut,
+                                          uint32_t (&wv)[32]) {
   uint32_t a4[32];
   sk_offsets<0>(d, a4, std::make_integer_sequence<int, 32>{});
-  uint32_t wv[32];
 #pragma unroll
   for (int j = 0; j < 32; ++j)
     wv[j] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + a4[j]);
-  const int8_t* xl = xb + (lane & 31) * G::ROW + koff + 16 * (lane >> 5);
+}
+
+template <int j0, int... is>
+__device__ __forceinline__ void sk_lookup8(const uint32_t (&d)[5], const uint32_t* lut,
+                                           uint32_t (&wv)[32], std::integer_sequence<int, is...>) {
+  ((wv[j0 + is] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) +
+                                                     code_x4<j0 + is>(d))),
+   ...);
+}
+
+// Step s (K values 32s .. 32s+31) of one container: words 8s..8s+3 of wv hold
+// K 32s..32s+15 of this lane's row, 8s+4..8s+7 the next 16; after the swap
+// the first four hold rows 0-31 and the last four rows 32-63, in the operand
+// layout.  Once the step's MFMAs are issued the 8 words take the next
+// container's lookups.
+template <int MT, int s>
+__device__ __forceinline__ void sk_mfma_step(uint32_t (&wv)[32], const uint32_t (&dn)[5],
+                                             const uint32_t* lut, const v4i (&xv)[MT],
+                                             v16i (&c)[2][MT]) {
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    // words 8s..8s+3 hold K 32s..32s+15 of this lane's row, 8s+4..8s+7 the
-    // next 16; after the swap lo = rows 0-31 and hi = rows 32-63 in the
-    // operand layout
-    v4i lo, hi;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const auto r = __builtin_amdgcn_permlane32_swap(wv[8 * s + i], wv[8 * s + 4 + i], false,
-                                                      false);
-      lo[i] = static_cast<int>(r[0]);
-      hi[i] = static_cast<int>(r[1]);
-    }
-#pragma unroll
-    for (int tb = 0; tb < MT; ++tb) {
-      const v4i xv = *reinterpret_cast<const v4i*>(xl + tb * 32 * G::ROW + 32 * s);
-      c[0][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xv, lo, c[0][tb], 0, 0, 0);
-      c[1][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xv, hi, c[1][tb], 0, 0, 0);
-    }
+  for (int i = 0; i < 4; ++i) {
+    const auto r =
+        __builtin_amdgcn_permlane32_swap(wv[8 * s + i], wv[8 * s + 4 + i], false, false);
+    wv[8 * s + i] = r[0];
+    wv[8 * s + 4 + i] = r[1];
   }
+  const v4i wl = {static_cast<int>(wv[8 * s]), static_cast<int>(wv[8 * s + 1]),
+                  static_cast<int>(wv[8 * s + 2]), static_cast<int>(wv[8 * s + 3])};
+  const v4i wh = {static_cast<int>(wv[8 * s + 4]), static_cast<int>(wv[8 * s + 5]),
+                  static_cast<int>(wv[8 * s + 6]), static_cast<int>(wv[8 * s + 7])};
+#pragma unroll
+  for (int tb = 0; tb < MT; ++tb) {
+    c[0][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xv[tb], wl, c[0][tb], 0, 0, 0);
+    c[1][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xv[tb], wh, c[1][tb], 0, 0, 0);
+  }
+  sk_lookup8<8 * s>(dn, lut, wv, std::make_integer_sequence<int, 8>{});
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Accumulates one container's 128 K values (looked-up weights wv) against the
+// staged activations into c[row group][token block], looking up the next
+// container's codes dn into wv on the way.  All of the container's activation
+// fragments are read first (lane l: token row 32tb + l%32 at row base xrow,
+// the 16-byte piece for step s at xrow + lo[s], the stage's swizzle resolved
+// per lane), so only the first step waits for the LDS.
+template <int MT, int NST>
+__device__ __forceinline__ void sk_mfma(uint32_t (&wv)[32], const uint32_t (&dn)[5],
+                                        const uint32_t* lut, const int8_t* xrow,
+                                        const int (&lo)[4], v16i (&c)[2][MT]) {
+  using G = SkCfg<MT, NST>;
+  v4i xv[4][MT];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int tb = 0; tb < MT; ++tb)
+      xv[s][tb] = *reinterpret_cast<const v4i*>(xrow + lo[s] + tb * 32 * G::KC);
+  sk_mfma_step<MT, 0>(wv, dn, lut, xv[0], c);
+  sk_mfma_step<MT, 1>(wv, dn, lut, xv[1], c);
+  sk_mfma_step<MT, 2>(wv, dn, lut, xv[2], c);
+  sk_mfma_step<MT, 3>(wv, dn, lut, xv[3], c);
 }
 
 // Barrier for LDS traffic only (outstanding global loads stay in flight).
@@ -113,25 +169,66 @@ __device__ __forceinline__ void sk_lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Waits for this wave's LDS reads and writes (the other counters are left
+// alone).
+__device__ __forceinline__ void sk_wait_lgkm() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
+
+// Workgroup barrier between stage chunks.  A workgroup-scope release fence
+// would also wait for every DMA still in flight (they write LDS), so the
+// ordering is explicit instead: the caller has waited for its own DMAs of
+// the chunk about to be read (sk_wait_vm), every LDS read of the previous
+// chunk has returned (its results fed MFMAs issued before this point), and
+// the compiler moves no memory access across the barrier.
+__device__ __forceinline__ void sk_stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+}
+
 // Workgroup g of problem p: tiles T*g .. T*g+T-1 (T = 8/S), each split along
 // K over S waves (wave w: tile w/S, split w%S).  Split s owns units
 // [s*U, min((s+1)*U, C)) with U = ceil(C/S); all waves walk their ranges in
-// lockstep chunks of UPC_S = UPC/S units, and a stage holds, for every
-// token, the S splits' windows side by side.  With S > 1 the partial
-// accumulators meet in LDS (over the stages) and split 0 writes the tile.
-template <int MT, int S>
+// lockstep chunks of UPS = UPC/S units, and a stage holds, for every token,
+// the S splits' windows side by side.  With S > 1 the partial accumulators
+// meet in LDS (over the stages) and split 0 writes the tile.
+//
+// Stage layout: token row t at t*KC; its 16-byte piece c (K window offset
+// 16c) at piece c ^ (t & 15), so that the 16 lanes of a read phase (16
+// consecutive tokens, one piece each) hit 16 different bank groups.
+//
+// Load order per container step: two weight loads (the ring), then this
+// step's share of the DMA for the chunk NST - 1 ahead.  Both are issued
+// unconditionally (past the end they read zeros or unused rows), so the
+// number of loads issued after the last DMA of any chunk is fixed and the
+// wait before that chunk's barrier is a constant vmcnt.
+template <int MT, int S, int NST>
 __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32_t* lut,
                                          int8_t* xs) {
-  using G = SkCfg<MT>;
+  using G = SkCfg<MT, NST>;
   static_assert(S >= 1 && G::UPC % S == 0, "splits divide a chunk");
-  constexpr int T = kSkWaves / S;   // tiles per workgroup
-  constexpr int UPS = G::UPC / S;   // units per split per chunk
-  constexpr int WIN = UPS * kTileK; // K values per split window
+  constexpr int T = kSkWaves / S;    // tiles per workgroup
+  constexpr int UPS = G::UPC / S;    // units per split per chunk
+  constexpr int WIN = UPS * kTileK;  // K values per split window
+  constexpr int D = NST - 1;         // chunks between a DMA and its use
+  // DMA instructions at each container position of a chunk
+  constexpr int PER = UPS >= G::SPT ? 1 : G::SPT / UPS;
+  constexpr int PL = UPS >= G::SPT ? G::SPT - 1 : UPS - 1;  // position of the last
+  // loads issued after chunk ch's last DMA when chunk ch is reached: steady
+  // state, and chunks 1..D-1 (whose DMAs the prologue issued)
+  constexpr int NSTEADY = 2 * (UPS - 1 - PL) + (D - 1) * (2 * UPS + G::SPT);
+  constexpr int NPRO = (D - 1) * G::SPT + 2 * kSkRing;
+  static_assert(G::SPT % PER == 0 && PER * (PL + 1) == G::SPT, "DMA spread");
+  static_assert(NPRO + 2 * (D - 1) * UPS < 64 && NSTEADY < 64, "vmcnt range");
+
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int C = (p.k + kTileK - 1) / kTileK;
   const int R = (p.n + kTileRows - 1) / kTileRows;
-  const int U = (C + S - 1) / S;    // units per split
+  const int U = (C + S - 1) / S;     // units per split
   const int r = g * T + wave / S;
   const int sp = wave % S;
   const int u0 = sp * U, u1 = (u0 + U < C) ? u0 + U : C;
@@ -140,45 +237,58 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
       const_cast<uint8_t*>(p.w) + (int64_t(r < R ? r : 0) * C + (live ? u0 : 0)) * kUnitBytes, 0,
       live ? (u1 - u0) * kUnitBytes : 0, kBufferWord3);
   const int nch = (U + UPS - 1) / UPS;
-  const bool k16 = (p.k & 15) == 0;
+  // the activations of the staged tokens; rows past m read zeros
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int8_t*>(p.x), 0, p.m * p.k, kBufferWord3);
 
-  // activation chunk ch -> registers: piece q = tid + threads*v is token
-  // q / (KC/16), 16 bytes at window offset 16 * (q % (KC/16)): split
-  // window s = offset / WIN, K = (s*U + ch*UPS)*128 + offset % WIN; zero past
-  // m, past k and past the split's end
-  uint4 sv[G::SPT];
-  auto stage_load = [&](int ch) {
+  // DMA instruction i of this wave fills 1 KB block i*8 + wave of a stage:
+  // lane slot q = 64 * block + lane is token q / CPR, swizzled piece q % CPR,
+  // i.e. window ws = o / WIN at offset wo = o % WIN.  Its K offset at chunk ch
+  // is kb + ch*WIN with kb = ws*U*128 + wo; pieces past the end of their
+  // split's range or past k are loaded from an offset outside the buffer,
+  // so they arrive as zeros (lim = K values left in the lane's window).
+  int dvo[G::SPT], lim[G::SPT];
 #pragma unroll
-    for (int v = 0; v < G::SPT; ++v) {
-      const int q = tid + kSkThreads * v;
-      const int tok = q / (G::KC / 16), o = 16 * (q % (G::KC / 16));
-      const int ws = o / WIN, wo = o % WIN;
-      const int ub = ws * U + ch * UPS;  // first unit of this window
-      const int kk = ub * kTileK + wo;
-      const int kend = (ws * U + U < C ? ws * U + U : C) * kTileK;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (tok < p.m && kk < p.k && kk < kend) {
-        const int8_t* src = p.x + int64_t(tok) * p.k + kk;
-        if (k16) {
-          val = *reinterpret_cast<const uint4*>(as_global(src));
-        } else {
-          uint32_t t4[4] = {0, 0, 0, 0};
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (kk + 4 * e < p.k) t4[e] = *reinterpret_cast<const uint32_t*>(as_global(src + 4 * e));
-          val = make_uint4(t4[0], t4[1], t4[2], t4[3]);
-        }
-      }
-      sv[v] = val;
-    }
+  for (int i = 0; i < G::SPT; ++i) {
+    const int q = 64 * (i * kSkWaves + wave) + lane;
+    const int t = q / G::CPR;
+    const int o = 16 * ((q % G::CPR) ^ (t & 15));
+    const int ws = o / WIN;
+    const int kb = ws * U * kTileK + o % WIN;
+    const int kend = ((ws + 1) * U < C ? (ws + 1) * U * kTileK : p.k);
+    dvo[i] = t * p.k + kb;
+    lim[i] = (kend < p.k ? kend : p.k) - kb;
+  }
+  int8_t* const xw = xs + 1024 * wave;  // + stage + 8 KB per instruction
+  auto dma = [&](int ch, int i, int voff, int left) {
+    sk_dma(rx, xw + (ch % NST) * G::STAGE + i * 1024 * kSkWaves,
+           ch * WIN < left ? voff + ch * WIN : kSkOutside);
   };
-  auto stage_store = [&](int buf) {
+
+  // reader: token row lane%32 (plus 32tb), piece (8b + 2s + lane/32) ^ (lane & 15)
+  // for window piece base 8b
+  const int sw = lane & 15;
+  int lo[4];
 #pragma unroll
-    for (int v = 0; v < G::SPT; ++v) {
-      const int q = tid + kSkThreads * v;
-      const int tok = q / (G::KC / 16), kc = q % (G::KC / 16);
-      *reinterpret_cast<uint4*>(xs + buf * G::STAGE + tok * G::ROW + 16 * kc) = sv[v];
+  for (int s = 0; s < 4; ++s) lo[s] = 16 * ((2 * s + (lane >> 5)) ^ (sw & 7));
+  const int8_t* xlane = xs + (lane & 31) * G::KC;
+
+  // A row length k that is not a multiple of 16 leaves, in the 16-byte piece
+  // that holds K = k, bytes of the next token's row: they are cleared in the
+  // stage once that piece has landed (chunk chl).
+  const int kr = p.k & 15;
+  const int sl = (C - 1) / U, jl = (C - 1) - sl * U;
+  const int chl = kr ? jl / UPS : -1;
+  auto clear_tail = [&]() {
+    const int o = sl * WIN + (jl % UPS) * kTileK + ((p.k & ~15) - (C - 1) * kTileK);
+    const int nd = (16 - kr) / 4;  // dwords to clear per token row
+    int8_t* st = xs + (chl % NST) * G::STAGE;
+    for (int e = tid; e < G::TOK * nd; e += kSkThreads) {
+      const int t = e / nd, b = kr + 4 * (e % nd);
+      *reinterpret_cast<uint32_t*>(st + t * G::KC + 16 * ((o / 16) ^ (t & 15)) + b) = 0;
     }
+    sk_wait_lgkm();
+    sk_stage_barrier();
   };
 
   v16i c[2][MT];
@@ -187,44 +297,72 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
 #pragma unroll
     for (int tb = 0; tb < MT; ++tb) c[h][tb] = v16i{};
 
-  stage_load(0);
-  stage_store(0);
-  if (nch > 1) stage_load(1);
+#pragma unroll
+  for (int ch = 0; ch < D; ++ch)
+#pragma unroll
+    for (int i = 0; i < G::SPT; ++i) dma(ch, i, dvo[i], lim[i]);
+  __builtin_amdgcn_sched_barrier(0);
   uint32_t ring[kSkRing][5];
 #pragma unroll
   for (int u = 0; u < kSkRing; ++u) {
     sk_load_container(ring[u], rs, u, lane);
     __builtin_amdgcn_sched_barrier(0);
   }
-  sk_lds_barrier();  // stage 0 and the table are ready
+  sk_wait_vm<NPRO>();
+  sk_wait_lgkm();
+  sk_stage_barrier();  // chunk 0 and the table are ready
+  if (chl == 0) clear_tail();
 
-  // unit j of the split (relative to u0) lives in chunk j / UPS; at each
-  // chunk boundary the next stage (in registers) is written and the one
-  // after it is loaded
-  const int nunits = nch * UPS;
+  // Software pipeline: step jj multiplies container jj (weights looked up in
+  // the previous step) and looks up container jj + 1, so the table reads and
+  // field extraction overlap the MFMAs.  Units past the split's end multiply
+  // zero activations; waves past the last tile compute values never stored.
+  uint32_t wv[32];
+  sk_lookup(ring[0], lut, wv);
+  const int nunits = nch * UPS;  // unit j of the split lives in chunk j / UPS
   for (int j = 0; j < nunits; j += kSkRing) {
 #pragma unroll
     for (int u = 0; u < kSkRing; ++u) {
       const int jj = j + u;
-      const int ch = jj / UPS;
-      if (jj % UPS == 0 && jj > 0) {
-        stage_store(ch & 1);
-        sk_lds_barrier();
-        if (ch + 1 < nch) stage_load(ch + 1);
+      const int ch = jj / UPS, pos = jj % UPS;
+      if (pos == 0 && jj > 0) {
+        if (ch >= D) {
+          sk_wait_vm<NSTEADY>();
+        } else {
+          // chunk ch < D: its DMA went out in the prologue
+          if constexpr (D > 1) {
+            if (ch == 1) sk_wait_vm<NPRO + 2 * UPS < 64 ? NPRO + 2 * UPS : 63>();
+            if constexpr (D > 2)
+              if (ch == 2) sk_wait_vm<NPRO + 4 * UPS < 64 ? NPRO + 4 * UPS : 63>();
+          }
+        }
+        sk_stage_barrier();
+        if (ch == chl) clear_tail();
       }
-      const int8_t* xb = xs + (ch & 1) * G::STAGE + sp * WIN;
-      if (live && u0 + jj < u1) sk_container<MT>(ring[u], xb, (jj % UPS) * kTileK, lut, c);
       __builtin_amdgcn_sched_barrier(0);
-      sk_load_container(ring[u], rs, jj + kSkRing, lane);
+      sk_load_container(ring[u], rs, jj + kSkRing, lane);  // container jj's codes are used
+      __builtin_amdgcn_sched_barrier(0);
+      const int wb = sp * WIN / 16 + 8 * pos;  // window piece base (multiple of 8)
+      const int8_t* xrow = xlane + (ch % NST) * G::STAGE + 128 * ((wb >> 3) ^ (sw >> 3));
+      sk_mfma<MT, NST>(wv, ring[(u + 1) % kSkRing], lut, xrow, lo, c);
+      __builtin_amdgcn_sched_barrier(0);
+      if (pos <= PL) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+          const int id = pos * PER + i;
+          dma(ch + D, id, dvo[id], lim[id]);
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+  sk_wait_vm<0>();  // no DMA may land in the LDS after this point
 
   if constexpr (S > 1) {
     // partial sums of the S splits of a tile through LDS (the stages are
     // free now), one token block at a time: [wave][h][element][lane]
     int32_t* red = reinterpret_cast<int32_t*>(xs);
-    static_assert(kSkWaves * 2 * 16 * 64 * 4 <= 2 * G::STAGE, "reduction fits the stages");
+    static_assert(kSkWaves * 2 * 16 * 64 * 4 <= NST * G::STAGE, "reduction fits the stages");
 #pragma unroll
     for (int tb = 0; tb < MT; ++tb) {
       sk_lds_barrier();
@@ -268,18 +406,32 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   }
 }
 
+// Stages per token-block count (one workgroup per CU either way: the
+// registers of the pipelined loop exceed 128 per lane).
+template <int MT>
+constexpr int kSkStages = 4;
+
+// grid: x = groups of 8/S tiles, y = blocks of 32*MT tokens
 template <int MT, int S>
 __global__ __launch_bounds__(kSkThreads) void skinny_kernel(SkProblem p) {
-  __shared__ __attribute__((aligned(16))) int8_t lds[kSkLutBytes + 2 * SkCfg<MT>::STAGE];
+  constexpr int NST = kSkStages<MT>;
+  __shared__ __attribute__((aligned(16))) int8_t lds[SkCfg<MT, NST>::LDS];
   uint32_t* lut = reinterpret_cast<uint32_t*>(lds);
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
-  sk_block<MT, S>(p, blockIdx.x, lut, lds + kSkLutBytes);
+  const int t0 = blockIdx.y * SkCfg<MT, NST>::TOK;
+  p.x += int64_t(t0) * p.k;
+  p.x_scale += t0;
+  p.y += int64_t(t0) * p.n;
+  if (p.acc) p.acc += int64_t(t0) * p.n;
+  p.m = (p.m - t0 < SkCfg<MT, NST>::TOK) ? p.m - t0 : SkCfg<MT, NST>::TOK;
+  sk_block<MT, S, NST>(p, blockIdx.x, lut, lds + kSkLutBytes);
 }
 
 template <int MT>
 __global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
     const sherry_gemm_desc* __restrict__ descs, int count) {
-  __shared__ __attribute__((aligned(16))) int8_t lds[kSkLutBytes + 2 * SkCfg<MT>::STAGE];
+  constexpr int NST = kSkStages<MT>;
+  __shared__ __attribute__((aligned(16))) int8_t lds[SkCfg<MT, NST>::LDS];
   uint32_t* lut = reinterpret_cast<uint32_t*>(lds);
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
@@ -298,7 +450,7 @@ __global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
   const SkProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m, d.w_scale};
-  sk_block<MT, 1>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
+  sk_block<MT, 1, NST>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
 }
 
 }  // namespace
@@ -310,28 +462,47 @@ int skinny_blocks(int64_t n) { return static_cast<int>(ceil_div(ceil_div(n, kTil
 // that small-N products still spread over many CUs.
 constexpr int64_t kSkMinBlocks = 192;
 
+// Token blocks beyond the grid's y limit go to further launches.
+constexpr int64_t kSkMaxGridY = 32768;
+
 template <int MT, int S>
 int launch_skinny_s(const SkProblem& p, hipStream_t s) {
   const int64_t R = ceil_div(p.n, kTileRows);
-  const dim3 grid(static_cast<unsigned>(ceil_div(R, kSkWaves / S))), block(kSkThreads);
-  return launch(skinny_kernel<MT, S>, grid, block, 0, s, p);
+  const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT>>::TOK);
+  for (int64_t b0 = 0; b0 < TB; b0 += kSkMaxGridY) {
+    const int64_t nb = TB - b0 < kSkMaxGridY ? TB - b0 : kSkMaxGridY;
+    const int64_t t0 = b0 * SkCfg<MT, kSkStages<MT>>::TOK;
+    SkProblem q = p;
+    q.x += t0 * p.k;
+    q.x_scale += t0;
+    q.y += t0 * p.n;
+    if (q.acc) q.acc += t0 * p.n;
+    q.m = static_cast<int>(p.m - t0);
+    const dim3 grid(static_cast<unsigned>(ceil_div(R, kSkWaves / S)), static_cast<unsigned>(nb));
+    const int rc = launch(skinny_kernel<MT, S>, grid, dim3(kSkThreads), 0, s, q);
+    if (rc != SHERRY_OK) return rc;
+  }
+  return SHERRY_OK;
 }
 
 template <int MT>
 int launch_skinny_mt(const SkProblem& p, hipStream_t s) {
   const int64_t R = ceil_div(p.n, kTileRows);
   const int64_t C = ceil_div(p.k, kTileK);
+  const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT>>::TOK);
   int S = 1;
-  while (S < SkCfg<MT>::UPC && S < kSkWaves && ceil_div(R, kSkWaves / S) < kSkMinBlocks &&
+  while (S < SkCfg<MT, kSkStages<MT>>::UPC && S < kSkWaves && ceil_div(R, kSkWaves / S) * TB < kSkMinBlocks &&
          C >= 2 * S)
     S *= 2;
   switch (S) {
     case 1: return launch_skinny_s<MT, 1>(p, s);
     case 2: return launch_skinny_s<MT, 2>(p, s);
-    case 4: return launch_skinny_s<MT, 4>(p, s);
+    case 4:
+      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 4) return launch_skinny_s<MT, 4>(p, s);
+      return launch_skinny_s<MT, 2>(p, s);
     default:
-      if constexpr (SkCfg<MT>::UPC >= 8) return launch_skinny_s<MT, 8>(p, s);
-      return launch_skinny_s<MT, 4>(p, s);
+      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 8) return launch_skinny_s<MT, 8>(p, s);
+      return launch_skinny_s<MT, 2>(p, s);
   }
 }
 

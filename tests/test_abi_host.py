@@ -168,10 +168,13 @@ def test_gemm_validation_without_launch():
 def test_kernel_choice_by_m():
     for m in (1, 2, 3, 4):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_GEMV
-    for m in (5, 16, 32, 64):
+    for m in (5, 16, 32, 64, 65, 512):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_SKINNY
-    for m in (65, 2048):
+    for m in (513, 2048):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_MFMA
+        assert sh.sherry_gemm_kernel_for(m, 8192, 2048) == sh.SHERRY_KERNEL_MFMA
+        # a longer K than N (down projections) stays register-decoded
+        assert sh.sherry_gemm_kernel_for(m, 2048, 8192) == sh.SHERRY_KERNEL_SKINNY
     assert sh.sherry_gemm_kernel_for(0, 2048, 2048) == -sh.SHERRY_E_SHAPE
 
 
@@ -238,7 +241,7 @@ def test_fused_validation_without_launch():
 
 def test_skinny_validation_without_launch():
     g = L.sherry_gemm_ex
-    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 65, 64, 128, sh.SHERRY_KERNEL_SKINNY,
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 0, 64, 128, sh.SHERRY_KERNEL_SKINNY,
              None) == sh.SHERRY_E_SHAPE
     assert g(FAKE, FAKE + 4, FAKE, 1.0, FAKE, None, 16, 64, 128, sh.SHERRY_KERNEL_SKINNY,
              None) == sh.SHERRY_E_ALIGN
@@ -252,6 +255,7 @@ def test_skinny_validation_without_launch():
     # one workgroup per 8 row tiles: 32 tiles -> 4, 128 -> 16, 2 -> 1
     assert [d.block_begin for d in descs] == [0, 4, 20] and total == 21 and max_m == 64
     assert ctypes.sizeof(sh.sherry_gemm_desc) == 64
+    # a grouped launch stages at most one 64-token block per product
     descs[1].m = 65
     with pytest.raises(sh.SherryError):
         sh.sherry_gemm_batched_prepare(descs)

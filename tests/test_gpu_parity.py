@@ -195,16 +195,18 @@ def test_mfma_large_tile_config(dev):
 PREFILL_3B = [("q", 3072, 3072), ("k", 1024, 3072), ("gate", 8192, 3072), ("down", 3072, 8192)]
 
 
+@pytest.mark.parametrize("kernel", ["MFMA", "SKINNY"])
 @pytest.mark.parametrize("name,n,k", PREFILL_3B)
-def test_mfma_prefill_shapes_sampled(dev, name, n, k):
+def test_prefill_shapes_sampled(dev, name, n, k, kernel):
+    # both MFMA paths (LDS-tiled and register-decoded) at M = 2048
     sh = _sh()
     m = 2048
-    _say("mfma-prefill", name, m, n, k)
+    _say("prefill", kernel, name, m, n, k)
     t = synth.ternary_34(n, k, 35, "pf", name)
     x = synth.activations(m, k, 35, "pfx", name, outlier_frac=0.01)
     q, sx = oracle.quantize_act(x)
     sw = synth.weight_scale(35, "pfs", name)
-    y, acc = _run(dev, t, q, sx, sw, sh.SHERRY_KERNEL_MFMA, m)
+    y, acc = _run(dev, t, q, sx, sw, getattr(sh, "SHERRY_KERNEL_" + kernel), m)
     rng = np.random.default_rng(1)
     ii, jj = rng.integers(0, m, 1500), rng.integers(0, n, 1500)
     # corners of the output too (first/last rows and columns of tiles)
@@ -554,15 +556,19 @@ def test_fused_batched_decode_step_llama_1b(dev):
             assert abs(float(yy[j]) - yr) <= RTOL * abs(yr)
 
 
-# ------------------------------------------------- small-M MFMA (M <= 64)
+# ------------------------------------- register-decoded MFMA (small M first)
 
 # A lone launch splits K over S = 1, 2, 4 or 8 waves per tile (more splits
 # for fewer tiles, at most half the containers): these cover every S for 32-
 # and 64-token staging, splits that end early or own no container, and the
-# LDS reduction of the partial sums.
+# LDS reduction of the partial sums.  Above 64 tokens the launch stages
+# 64-token blocks along a second grid dimension: ragged last blocks, a single
+# block, and many blocks.
 SKINNY_CASES = [(5, 64, 128), (16, 65, 132), (32, 300, 1032), (33, 130, 2048), (64, 512, 1024),
                 (1, 64, 128), (4, 257, 3076), (17, 1000, 2056), (64, 70, 4), (48, 3072, 8192),
-                (40, 100, 384), (20, 200, 896), (9, 16384, 256)]
+                (40, 100, 384), (20, 200, 896), (9, 16384, 256),
+                (65, 64, 128), (128, 130, 1032), (129, 520, 2052), (300, 64, 388),
+                (700, 1100, 1536), (2048, 96, 256), (257, 4096, 1024)]
 
 
 @pytest.mark.parametrize("m,n,k", SKINNY_CASES)
