@@ -86,6 +86,14 @@ def lib():
         L.oracle_epilogue.restype = None
         L.oracle_ternarize.argtypes = [ctypes.POINTER(ctypes.c_float), i64, i64, i8p]
         L.oracle_ternarize.restype = ctypes.c_double
+        L.oracle_ternarize_rows.argtypes = [ctypes.POINTER(ctypes.c_float), i64, i64, i8p,
+                                            ctypes.POINTER(ctypes.c_double)]
+        L.oracle_ternarize_rows.restype = None
+        L.oracle_epilogue_rows.argtypes = [ctypes.POINTER(ctypes.c_int32),
+                                           ctypes.POINTER(ctypes.c_float),
+                                           ctypes.POINTER(ctypes.c_float), i64, i64,
+                                           ctypes.POINTER(ctypes.c_double)]
+        L.oracle_epilogue_rows.restype = None
         L.oracle_packed2_bytes.argtypes = [i64, i64]
         L.oracle_packed2_bytes.restype = i64
         L.oracle_pack2.argtypes = [i8p, i64, i64, u8p]
@@ -217,6 +225,19 @@ def epilogue(acc: np.ndarray, sx: np.ndarray, sw: float) -> np.ndarray:
     return y
 
 
+def epilogue_rows(acc: np.ndarray, sx: np.ndarray, sw: np.ndarray) -> np.ndarray:
+    """Per-output-channel scales ([T alpha]_ij = T_ij alpha_j): y = acc*sx[m]*sw[n]."""
+    acc = np.ascontiguousarray(acc, dtype=np.int32)
+    sx = np.ascontiguousarray(sx, dtype=np.float32)
+    sw = np.ascontiguousarray(sw, dtype=np.float32)
+    m, n = acc.shape
+    assert sx.shape == (m,) and sw.shape == (n,)
+    y = np.zeros((m, n), dtype=np.float64)
+    lib().oracle_epilogue_rows(_p(acc, ctypes.c_int32), _p(sx, ctypes.c_float),
+                               _p(sw, ctypes.c_float), m, n, _p(y, ctypes.c_double))
+    return y
+
+
 # ---- (vi) Sparse-AbsMean ternarizer (Eq. 4, Eq. 5) -------------------------
 
 def ternarize(w: np.ndarray):
@@ -226,6 +247,17 @@ def ternarize(w: np.ndarray):
     t = np.zeros((n, k), dtype=np.int8)
     alpha = lib().oracle_ternarize(_p(w, ctypes.c_float), n, k, _p(t, ctypes.c_int8))
     return t, float(alpha)
+
+
+def ternarize_rows(w: np.ndarray):
+    """fp32 [n][k] -> (int8 T [n][k], fp64 alpha [n]): Eq. 5 per output channel."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    n, k = w.shape
+    t = np.zeros((n, k), dtype=np.int8)
+    alpha = np.zeros(n, dtype=np.float64)
+    lib().oracle_ternarize_rows(_p(w, ctypes.c_float), n, k, _p(t, ctypes.c_int8),
+                                _p(alpha, ctypes.c_double))
+    return t, alpha
 
 
 # ---- (vii) 2-bit layout ----------------------------------------------------

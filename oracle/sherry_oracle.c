@@ -28,9 +28,12 @@
  *  (iv)  product       -- Eq. 2, Y = X T alpha, with T in {-1,0,1} satisfying
  *                         the 3:4 constraint of Eq. 3.  Plain dense integer
  *                         triple loop on the UNPACKED T; never reads a code.
- *  (v)   epilogue      -- Eq. 2 scaling, y = acc * sx * sw, in fp64.
+ *  (v)   epilogue      -- Eq. 2 scaling, y = acc * sx * sw, in fp64; also
+ *                         with one sw per output channel ([T alpha]_ij =
+ *                         T_ij alpha_j, the footnote to Eq. 2).
  *  (vi)  ternarizer    -- Eq. 4 (Sparse-AbsMean) and Eq. 5 (alpha), with a
- *                         per-tensor alpha.
+ *                         per-tensor alpha, or one alpha per output channel
+ *                         as Eq. 5 states it.
  *  (vii) 2-bit codec   -- the "2-bit strategy" of Sec. 2.3 (one ternary
  *                         weight per 2 bits), used only as a bytes-moved
  *                         comparison; layout is this project's own.
@@ -285,6 +288,14 @@ void oracle_epilogue(const int32_t* acc, const float* sx, float sw, int64_t m,
       y[mm * n + nn] = (double)acc[mm * n + nn] * (double)sx[mm] * (double)sw;
 }
 
+/* Per-output-channel scales: y = acc * sx[m] * sw[n]. */
+void oracle_epilogue_rows(const int32_t* acc, const float* sx, const float* sw,
+                          int64_t m, int64_t n, double* y) {
+  for (int64_t mm = 0; mm < m; ++mm)
+    for (int64_t nn = 0; nn < n; ++nn)
+      y[mm * n + nn] = (double)acc[mm * n + nn] * (double)sx[mm] * (double)sw[nn];
+}
+
 /* ------------------------------------------------------------------------ */
 /* (vi) Sparse-AbsMean ternarizer, Eq. 4 and Eq. 5 (per-tensor alpha)       */
 /* Ties for the smallest |W| go to the lowest position; a kept weight equal */
@@ -314,6 +325,33 @@ double oracle_ternarize(const float* w, int64_t n, int64_t k, int8_t* t) {
     }
   }
   return kept ? kept_abs / (double)kept : 0.0;
+}
+
+/* Eq. 5 as the paper states it: one alpha per output channel (row of T),
+ * the mean |W| over that row's kept weights, summed in fp64 in ascending K
+ * order.  T is the same as oracle_ternarize's. */
+void oracle_ternarize_rows(const float* w, int64_t n, int64_t k, int8_t* t,
+                           double* alpha) {
+  for (int64_t row = 0; row < n; ++row) {
+    double kept_abs = 0.0;
+    int64_t kept = 0;
+    for (int64_t b = 0; b < k / 4; ++b) {
+      const float* wb = w + row * k + 4 * b;
+      int amin = 0;
+      for (int p = 1; p < 4; ++p)
+        if (fabs((double)wb[p]) < fabs((double)wb[amin])) amin = p;
+      for (int p = 0; p < 4; ++p) {
+        int8_t v = 0;
+        if (p != amin) {
+          v = (wb[p] < 0.0f) ? -1 : 1;
+          kept_abs += fabs((double)wb[p]);
+          ++kept;
+        }
+        t[row * k + 4 * b + p] = v;
+      }
+    }
+    alpha[row] = kept ? kept_abs / (double)kept : 0.0;
+  }
 }
 
 /* ------------------------------------------------------------------------ */

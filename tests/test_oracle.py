@@ -301,6 +301,43 @@ def test_ternarizer_alpha_is_least_squares():
     assert np.isclose(alpha, sol, rtol=1e-12)
 
 
+def test_ternarizer_rows_alpha_is_per_channel_least_squares():
+    # Eq. 5 per output channel: alpha_j = <W_j, T_j> / <T_j, T_j>, i.e. the
+    # least-squares scale of row j given its 3:4 pattern; the pattern is the
+    # per-tensor ternarizer's, and with equal kept counts per row the
+    # per-tensor alpha is the mean of the per-row ones.
+    w = synth.dense_weights(7, 96, 12, "alpha_rows")
+    w[3] *= 25.0  # rows of very different magnitude
+    t, alpha = oracle.ternarize_rows(w)
+    t0, alpha0 = oracle.ternarize(w)
+    assert np.array_equal(t, t0)
+    for j in range(7):
+        tj = t[j].astype(np.float64)
+        sol = np.linalg.lstsq(tj[:, None], w[j].astype(np.float64), rcond=None)[0][0]
+        assert np.isclose(alpha[j], sol, rtol=1e-12)
+    assert np.isclose(alpha.mean(), alpha0, rtol=1e-12)
+    assert alpha[3] > 10 * np.delete(alpha, 3).max()
+
+
+def test_epilogue_rows_is_dequantized_product():
+    # [T alpha]_ij = T_ij alpha_j (footnote to Eq. 2): the per-channel result
+    # equals the product of the dequantized operands, (q * sx) @ (T * sw)^T,
+    # computed in the other order; with one sw for every channel it is the
+    # per-tensor epilogue.
+    rng = np.random.default_rng(13)
+    q = rng.integers(-127, 128, (5, 64)).astype(np.int8)
+    t = synth.ternary_34(9, 64, 13, "epr")
+    sx = (rng.random(5) + 0.01).astype(np.float32)
+    sw = (rng.random(9) * 0.05 + 0.001).astype(np.float32)
+    acc = oracle.gemm_i32(q, t)
+    y = oracle.epilogue_rows(acc, sx, sw)
+    ref = (q.astype(np.float64) * sx.astype(np.float64)[:, None]) @ \
+        (t.astype(np.float64) * sw.astype(np.float64)[:, None]).T
+    assert np.allclose(y, ref, rtol=1e-12, atol=0)
+    y1 = oracle.epilogue_rows(acc, sx, np.full(9, sw[0], np.float32))
+    assert np.array_equal(y1, oracle.epilogue(acc, sx, float(sw[0])))
+
+
 def test_ternarizer_ties_and_zeros():
     w = np.array([[0.5, -0.5, 0.5, -0.5, 0.0, 0.0, 1.0, -2.0]], np.float32)
     t, _ = oracle.ternarize(w)
