@@ -112,6 +112,22 @@ int sherry_pack(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
 int sherry_unpack(const uint8_t* packed, size_t packed_bytes, int64_t n,
                   int64_t k, int8_t* t_out);
 
+/* Sparse-AbsMean ternarization and packing on the GPU (Eq. 4, Eq. 5), the
+ * step that turns full-precision weights into the packed layout.
+ * w: device, fp32 [n][k] row-major (row = output channel, blocks of 4 along
+ * k), 16-byte aligned, finite values.  In each block of 4 the smallest |w|
+ * becomes 0 (ties: the lowest position) and the other three their sign (+1
+ * for a kept zero).  packed: device, packed_bytes >= sherry_packed_bytes(n,
+ * k), 16-byte aligned; receives exactly the bytes sherry_pack writes for that
+ * ternary matrix.  alpha: device, fp32 [n], 4-byte aligned, or NULL;
+ * receives Eq. 5 per output channel, the mean |w| over the row's kept
+ * weights, summed in fp64 (the summation order differs from a sequential
+ * sum, so the fp32 result can differ from one by a unit in the last place).
+ * Enqueued on stream; returns SHERRY_E_SHAPE / _BUFSIZE / _ALIGN /
+ * _INVALID before enqueuing anything. */
+int sherry_ternarize_pack(const float* w, int64_t n, int64_t k, uint8_t* packed,
+                          size_t packed_bytes, float* alpha, void* stream);
+
 /* ---------------------------------------------------------------------- */
 /* Activation quantization (the integer inputs of the online phase).       */
 /* ---------------------------------------------------------------------- */
@@ -156,6 +172,16 @@ int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
  * invalid shape: SHERRY_KERNEL_GEMV for m <= 4, SHERRY_KERNEL_SKINNY for
  * 5 <= m <= 512 or k > n, else SHERRY_KERNEL_MFMA. */
 int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k);
+
+/* sherry_gemm_ex with one weight scale per output channel: the footnote to
+ * Eq. 2 scales column j of T by alpha_j, and Eq. 5 gives one alpha per
+ * output channel.  w_scales: device, fp32 [n], 4-byte aligned (for example
+ * the alpha that sherry_ternarize_pack writes).  y[i][j] = float(acc[i][j]) *
+ * (x_scale[i] * w_scales[j]); the int32 acc is the same as sherry_gemm_ex's.
+ * SHERRY_E_INVALID if w_scales is NULL. */
+int sherry_gemm_channel(const uint8_t* w, const int8_t* x, const float* x_scale,
+                        const float* w_scales, float* y, int32_t* acc, int64_t m,
+                        int64_t n, int64_t k, int kernel, void* stream);
 
 /* ---------------------------------------------------------------------- */
 /* Grouped M = 1 products: many independent GEMVs in one launch.           */
@@ -231,6 +257,12 @@ int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
 int sherry_gemv_f32(const uint8_t* w, const float* x, float* x_scale,
                     float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
                     void* stream);
+
+/* sherry_gemv_f32 with one weight scale per output channel (w_scales as in
+ * sherry_gemm_channel). */
+int sherry_gemv_f32_channel(const uint8_t* w, const float* x, float* x_scale,
+                            const float* w_scales, float* y, int32_t* acc,
+                            int64_t n, int64_t k, void* stream);
 
 typedef struct sherry_gemv_f32_desc {
   const uint8_t* w;      /* device, packed n x k, 16-byte aligned          */

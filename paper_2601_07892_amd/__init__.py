@@ -37,6 +37,7 @@ EXPORTS = [
     "sherry_packed2_bytes", "sherry_pack2", "sherry_gemv2", "sherry_stream_read",
     "sherry_stream_read_groups", "sherry_gemv_f32", "sherry_gemv_f32_batched_prepare",
     "sherry_gemv_f32_batched", "sherry_gemm_batched_prepare", "sherry_gemm_batched",
+    "sherry_gemm_channel", "sherry_gemv_f32_channel", "sherry_ternarize_pack",
 ]
 
 
@@ -114,6 +115,10 @@ def _load():
         "sherry_gemm_batched_prepare": ([ctypes.POINTER(sherry_gemm_desc), ctypes.c_int, i64p,
                                          ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
         "sherry_gemm_batched": ([vp, ctypes.c_int, i64, ctypes.c_int32, vp], ctypes.c_int),
+        "sherry_gemm_channel": ([vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp],
+                                ctypes.c_int),
+        "sherry_gemv_f32_channel": ([vp, vp, vp, vp, vp, vp, i64, i64, vp], ctypes.c_int),
+        "sherry_ternarize_pack": ([vp, i64, i64, vp, ctypes.c_size_t, vp, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -233,6 +238,22 @@ def sherry_gemm_ex(w, x, x_scale, w_scale: float, y, acc, m: int, n: int, k: int
            "sherry_gemm_ex")
 
 
+def sherry_gemm_channel(w, x, x_scale, w_scales, y, acc, m: int, n: int, k: int,
+                        kernel: int = SHERRY_KERNEL_AUTO, stream=None):
+    """sherry_gemm_ex with one weight scale per output channel (w_scales: fp32 [n])."""
+    _check(lib.sherry_gemm_channel(_ptr(w), _ptr(x), _ptr(x_scale), _ptr(w_scales), _ptr(y),
+                                   _ptr(acc), m, n, k, int(kernel), _stream(stream)),
+           "sherry_gemm_channel")
+
+
+def sherry_ternarize_pack(w, n: int, k: int, packed, alpha=None, stream=None):
+    """Sparse-AbsMean ternarization + packing of device fp32 w [n][k] into the
+    device byte tensor packed; per-channel alpha into the fp32 [n] tensor alpha."""
+    nbytes = packed.numel() * packed.element_size()
+    _check(lib.sherry_ternarize_pack(_ptr(w), n, k, _ptr(packed), nbytes, _ptr(alpha),
+                                     _stream(stream)), "sherry_ternarize_pack")
+
+
 def sherry_gemm_kernel_for(m: int, n: int, k: int) -> int:
     return int(lib.sherry_gemm_kernel_for(m, n, k))
 
@@ -255,6 +276,13 @@ def sherry_gemv_f32(w, x, x_scale, w_scale: float, y, acc, n: int, k: int, strea
     """Quantizes the fp32 activation row x and multiplies, in one launch."""
     _check(lib.sherry_gemv_f32(_ptr(w), _ptr(x), _ptr(x_scale), float(w_scale), _ptr(y),
                                _ptr(acc), n, k, _stream(stream)), "sherry_gemv_f32")
+
+
+def sherry_gemv_f32_channel(w, x, x_scale, w_scales, y, acc, n: int, k: int, stream=None):
+    """sherry_gemv_f32 with one weight scale per output channel."""
+    _check(lib.sherry_gemv_f32_channel(_ptr(w), _ptr(x), _ptr(x_scale), _ptr(w_scales), _ptr(y),
+                                       _ptr(acc), n, k, _stream(stream)),
+           "sherry_gemv_f32_channel")
 
 
 def sherry_gemv_f32_batched_prepare(descs) -> int:

@@ -90,9 +90,10 @@ extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
   return (m <= kSkinnyMaxM || k > n) ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
 }
 
-extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
-                              float w_scale, float* y, int32_t* acc, int64_t m, int64_t n,
-                              int64_t k, int kernel, void* stream) {
+namespace {
+// Product on the chosen kernel (kernel already resolved from AUTO).
+int gemm_dispatch(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws, float* y,
+                  int32_t* acc, int64_t m, int64_t n, int64_t k, int kernel, void* stream) {
   if (kernel == SHERRY_KERNEL_AUTO) {
     const int kk = sherry_gemm_kernel_for(m, n, k);
     kernel = kk < 0 ? SHERRY_KERNEL_GEMV : kk;
@@ -102,21 +103,36 @@ extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_
     if (st != SHERRY_OK) return st;
     if (m > kGemvMaxM) return SHERRY_E_SHAPE;
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
-    return launch_gemv_valu(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
+    return launch_gemv_valu(w, x, x_scale, ws, y, acc, m, n, k, as_stream(stream));
   }
   if (kernel == SHERRY_KERNEL_SKINNY) {
     int st = check_product(w, x, x_scale, y, m, n, k, 16);
     if (st != SHERRY_OK) return st;
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
-    return launch_skinny(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
+    return launch_skinny(w, x, x_scale, ws, y, acc, m, n, k, as_stream(stream));
   }
   if (kernel == SHERRY_KERNEL_MFMA) {
     int st = check_product(w, x, x_scale, y, m, n, k, 16);
     if (st != SHERRY_OK) return st;
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
-    return launch_gemm_mfma(w, x, x_scale, w_scale, y, acc, m, n, k, as_stream(stream));
+    return launch_gemm_mfma(w, x, x_scale, ws, y, acc, m, n, k, as_stream(stream));
   }
   return SHERRY_E_INVALID;
+}
+}  // namespace
+
+extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
+                              float w_scale, float* y, int32_t* acc, int64_t m, int64_t n,
+                              int64_t k, int kernel, void* stream) {
+  return gemm_dispatch(w, x, x_scale, WScale{nullptr, w_scale}, y, acc, m, n, k, kernel, stream);
+}
+
+extern "C" int sherry_gemm_channel(const uint8_t* w, const int8_t* x, const float* x_scale,
+                                   const float* w_scales, float* y, int32_t* acc, int64_t m,
+                                   int64_t n, int64_t k, int kernel, void* stream) {
+  if (!w_scales) return SHERRY_E_INVALID;
+  if (!aligned(w_scales, 4)) return SHERRY_E_ALIGN;
+  return gemm_dispatch(w, x, x_scale, WScale{w_scales, 0.0f}, y, acc, m, n, k, kernel, stream);
 }
 
 extern "C" int sherry_gemm(const uint8_t* w, const int8_t* x, const float* x_scale,
@@ -186,7 +202,19 @@ extern "C" int sherry_gemv_f32(const uint8_t* w, const float* x, float* x_scale,
                                float* y, int32_t* acc, int64_t n, int64_t k, void* stream) {
   int st = check_fused(w, x, x_scale, y, acc, n, k);
   if (st != SHERRY_OK) return st;
-  return launch_gemv_f32(w, x, x_scale, w_scale, y, acc, n, k, as_stream(stream));
+  return launch_gemv_f32(w, x, x_scale, WScale{nullptr, w_scale}, y, acc, n, k,
+                         as_stream(stream));
+}
+
+extern "C" int sherry_gemv_f32_channel(const uint8_t* w, const float* x, float* x_scale,
+                                       const float* w_scales, float* y, int32_t* acc, int64_t n,
+                                       int64_t k, void* stream) {
+  int st = check_fused(w, x, x_scale, y, acc, n, k);
+  if (st != SHERRY_OK) return st;
+  if (!w_scales) return SHERRY_E_INVALID;
+  if (!aligned(w_scales, 4)) return SHERRY_E_ALIGN;
+  return launch_gemv_f32(w, x, x_scale, WScale{w_scales, 0.0f}, y, acc, n, k,
+                         as_stream(stream));
 }
 
 extern "C" int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int count,
@@ -242,4 +270,15 @@ extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
   if (max_m < 1 || max_m > kBatchedMaxM) return SHERRY_E_SHAPE;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
   return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
+}
+
+extern "C" int sherry_ternarize_pack(const float* w, int64_t n, int64_t k, uint8_t* packed,
+                                     size_t packed_bytes, float* alpha, void* stream) {
+  if (!w || !packed) return SHERRY_E_INVALID;
+  const size_t need = sherry_packed_bytes(n, k);
+  if (need == 0) return SHERRY_E_SHAPE;
+  if (packed_bytes < need) return SHERRY_E_BUFSIZE;
+  if (!aligned(w, 16) || !aligned(packed, 16) || (alpha && !aligned(alpha, 4)))
+    return SHERRY_E_ALIGN;
+  return launch_ternarize_pack(w, n, k, packed, alpha, as_stream(stream));
 }

@@ -76,7 +76,7 @@ __device__ __forceinline__ void decode_codes(const uint32_t (&d)[5], const uint3
 template <class G, bool kFullK>
 __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
     const uint8_t* __restrict__ w, const int8_t* __restrict__ x,
-    const float* __restrict__ x_scale, float w_scale, float* __restrict__ y,
+    const float* __restrict__ x_scale, WScale ws, float* __restrict__ y,
     int32_t* __restrict__ acc_out, int64_t M, int64_t N, int64_t K, int MT, int NT) {
   // LDS: the 32-entry code table at address 0 (table reads then need no base
   // in their address), then the two stages
@@ -282,13 +282,13 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
     for (int r = 0; r < 16; ++r) {
       const int64_t gm = m0 + wr * G::WM + a * 32 + 8 * (r >> 2) + 4 * fhalf + (r & 3);
       if (gm >= M) continue;
-      const float s = x_scale[gm] * w_scale;
+      const float sx = x_scale[gm];
 #pragma unroll
       for (int bb = 0; bb < G::FN; ++bb) {
         const int64_t gn = n0 + wc * G::WN + bb * 32 + frow;
         if (gn >= N) continue;
         const int32_t v = acc[a][bb][r];
-        y[gm * N + gn] = static_cast<float>(v) * s;
+        y[gm * N + gn] = static_cast<float>(v) * (sx * ws.at(gn));
         if (acc_out) acc_out[gm * N + gn] = v;
       }
     }
@@ -296,15 +296,15 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
 }
 
 template <class G>
-int launch_cfg(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
+int launch_cfg(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
   const int MT = static_cast<int>(ceil_div(m, G::BM));
   const int NT = static_cast<int>(ceil_div(n, G::BN));
   const dim3 grid(static_cast<unsigned>(MT) * NT), block(G::THREADS);
   if (k % kBK == 0)
-    return launch(gemm_kernel<G, true>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, m, n,
+    return launch(gemm_kernel<G, true>, grid, block, 0, s, w, x, x_scale, ws, y, acc, m, n,
                   k, MT, NT);
-  return launch(gemm_kernel<G, false>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, m, n, k,
+  return launch(gemm_kernel<G, false>, grid, block, 0, s, w, x, x_scale, ws, y, acc, m, n, k,
                 MT, NT);
 }
 
@@ -333,13 +333,13 @@ int gemm_config_for(int64_t m, int64_t n) {
   return cm <= cs ? 2 : 1;
 }
 
-int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
+int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                      float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
   switch (gemm_config_for(m, n)) {
-    case 0: return launch_cfg<CfgSkinny>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
-    case 1: return launch_cfg<CfgSmall>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
-    case 2: return launch_cfg<CfgMid>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
-    default: return launch_cfg<CfgLarge>(w, x, x_scale, w_scale, y, acc, m, n, k, s);
+    case 0: return launch_cfg<CfgSkinny>(w, x, x_scale, ws, y, acc, m, n, k, s);
+    case 1: return launch_cfg<CfgSmall>(w, x, x_scale, ws, y, acc, m, n, k, s);
+    case 2: return launch_cfg<CfgMid>(w, x, x_scale, ws, y, acc, m, n, k, s);
+    default: return launch_cfg<CfgLarge>(w, x, x_scale, ws, y, acc, m, n, k, s);
   }
 }
 

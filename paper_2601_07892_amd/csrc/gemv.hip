@@ -196,7 +196,7 @@ __device__ __forceinline__ void ring_run(uint32_t (&ring)[kRing][5], __amdgpu_bu
 // LDS; the caller has filled lut.
 template <int M, class X, class Prelude>
 __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Prelude prelude,
-                                           float w_scale, float* y, int32_t* acc_out, int64_t n,
+                                           WScale ws, float* y, int32_t* acc_out, int64_t n,
                                            int k, int g, int S, const uint32_t* lut,
                                            int32_t* red) {
   const int lane = threadIdx.x & 63;
@@ -238,7 +238,7 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
     if (r2 >= R || row >= n) continue;
     int32_t a = 0;
     for (int p = 0; p < S; ++p) a += red[((lt2 * S + p) * M + m) * 64 + i];
-    const float s = sx[m] * w_scale;
+    const float s = sx[m] * ws.at(row);
     as_global_mut(y)[m * n + row] = static_cast<float>(a) * s;
     if (acc_out) as_global_mut(acc_out)[m * n + row] = a;
   }
@@ -262,13 +262,13 @@ __device__ __forceinline__ void fill_lut(uint32_t* lut) {
 template <int M>
 __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(
     const uint8_t* __restrict__ w, const int8_t* __restrict__ x,
-    const float* __restrict__ x_scale, float w_scale, float* __restrict__ y,
+    const float* __restrict__ x_scale, WScale ws, float* __restrict__ y,
     int32_t* __restrict__ acc, int64_t n, int64_t k, int split) {
   __shared__ uint32_t lut[32];
   __shared__ int32_t red[kGemvWaves * M * 64];
   fill_lut(lut);
   gemv_block<M>(w, XFromSgpr<M>{as_const(reinterpret_cast<const int32_t*>(x)), static_cast<int>(k)},
-                ReadScales<M>{x_scale}, w_scale, y, acc, n, static_cast<int>(k), blockIdx.x, split,
+                ReadScales<M>{x_scale}, ws, y, acc, n, static_cast<int>(k), blockIdx.x, split,
                 lut, red);
 }
 
@@ -297,7 +297,8 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
   const int k = static_cast<int>(d.k);
   const int S = gemv_split(static_cast<int>((k + kTileK - 1) / kTileK));
   gemv_block<1>(d.w, XFromSgpr<1>{as_const(reinterpret_cast<const int32_t*>(d.x)), k},
-                ReadScales<1>{d.x_scale}, d.w_scale, d.y, d.acc, d.n, k, blk - d.block_begin, S,
+                ReadScales<1>{d.x_scale}, WScale{nullptr, d.w_scale}, d.y, d.acc, d.n, k,
+                blk - d.block_begin, S,
                 lut, red);
 }
 
@@ -387,33 +388,33 @@ struct QuantizeRow {
 // Fused product of one block: the row length picks the quantizer (rows up
 // to 2048 and 8192 values from registers, longer ones in two passes).
 __device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, float* x_scale,
-                                            bool write_scale, float w_scale, float* y,
+                                            bool write_scale, WScale ws, float* y,
                                             int32_t* acc, int64_t n, int k, int g, int S,
                                             const uint32_t* lut, int32_t* red, float* part,
                                             int8_t* xq) {
   const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
   if (kp <= 4 * kGemvThreads) {
     gemv_block<1>(w, XFromLds{xq}, QuantizeRow<1>{x, k, kp, xq, part, x_scale, write_scale},
-                  w_scale, y, acc, n, k, g, S, lut, red);
+                  ws, y, acc, n, k, g, S, lut, red);
   } else if (kp <= 16 * kGemvThreads) {
     gemv_block<1>(w, XFromLds{xq}, QuantizeRow<4>{x, k, kp, xq, part, x_scale, write_scale},
-                  w_scale, y, acc, n, k, g, S, lut, red);
+                  ws, y, acc, n, k, g, S, lut, red);
   } else {
     gemv_block<1>(w, XFromLds{xq}, QuantizeRow<0>{x, k, kp, xq, part, x_scale, write_scale},
-                  w_scale, y, acc, n, k, g, S, lut, red);
+                  ws, y, acc, n, k, g, S, lut, red);
   }
 }
 
 __global__ __launch_bounds__(kGemvThreads) void gemv_f32_kernel(
     const uint8_t* __restrict__ w, const float* __restrict__ x, float* __restrict__ x_scale,
-    float w_scale, float* __restrict__ y, int32_t* __restrict__ acc, int64_t n, int64_t k,
+    WScale ws, float* __restrict__ y, int32_t* __restrict__ acc, int64_t n, int64_t k,
     int split) {
   __shared__ uint32_t lut[32];
   __shared__ int32_t red[kGemvWaves * 64];
   __shared__ float part[kGemvWaves];
   __shared__ __attribute__((aligned(16))) int8_t xq[kFusedMaxK];
   fill_lut(lut);
-  fused_block(w, x, x_scale, blockIdx.x == 0, w_scale, y, acc, n, static_cast<int>(k), blockIdx.x,
+  fused_block(w, x, x_scale, blockIdx.x == 0, ws, y, acc, n, static_cast<int>(k), blockIdx.x,
               split, lut, red, part, xq);
 }
 
@@ -440,13 +441,14 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
   const int k = static_cast<int>(d.k);
   const int C = (k + kTileK - 1) / kTileK;
   const int S = gemv_split(C, kFusedTarget);
-  fused_block(d.w, d.x, d.x_scale, blk == d.block_begin, d.w_scale, d.y, d.acc, d.n, k,
+  fused_block(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{nullptr, d.w_scale}, d.y, d.acc,
+              d.n, k,
               blk - d.block_begin, S, lut, red, part, xq);
 }
 
 }  // namespace
 
-int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
+int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                      float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
   const int64_t R = ceil_div(n, kTileRows);
   const int C = static_cast<int>(ceil_div(k, kTileK));
@@ -456,10 +458,10 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale, fl
   const dim3 grid(static_cast<unsigned>(ceil_div(R * S, kGemvWaves)));
   const dim3 block(kGemvThreads);
   switch (m) {
-    case 1: return launch(gemv_kernel<1>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, n, k, S);
-    case 2: return launch(gemv_kernel<2>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, n, k, S);
-    case 3: return launch(gemv_kernel<3>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, n, k, S);
-    case 4: return launch(gemv_kernel<4>, grid, block, 0, s, w, x, x_scale, w_scale, y, acc, n, k, S);
+    case 1: return launch(gemv_kernel<1>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+    case 2: return launch(gemv_kernel<2>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+    case 3: return launch(gemv_kernel<3>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+    case 4: return launch(gemv_kernel<4>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
     default: return SHERRY_E_SHAPE;
   }
 }
@@ -470,13 +472,13 @@ int launch_gemv_batched(const sherry_gemv_desc* descs, int count, int64_t total_
                 dim3(kGemvThreads), 0, s, descs, count);
 }
 
-int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, float w_scale, float* y,
+int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, WScale ws, float* y,
                     int32_t* acc, int64_t n, int64_t k, hipStream_t s) {
   const int64_t R = ceil_div(n, kTileRows);
   const int C = static_cast<int>(ceil_div(k, kTileK));
   const int S = (R * gemv_split(C, kFusedTarget) >= 4096) ? gemv_split(C, kFusedTarget) : kGemvWaves;
   return launch(gemv_f32_kernel, dim3(static_cast<unsigned>(ceil_div(R * S, kGemvWaves))),
-                dim3(kGemvThreads), 0, s, w, x, x_scale, w_scale, y, acc, n, k, S);
+                dim3(kGemvThreads), 0, s, w, x, x_scale, ws, y, acc, n, k, S);
 }
 
 int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_t total_blocks,

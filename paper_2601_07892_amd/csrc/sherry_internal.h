@@ -151,23 +151,33 @@ __device__ __forceinline__ SHERRY_GLOBAL T* as_global_mut(T* p) {
   return (SHERRY_GLOBAL T*)(p);
 }
 
+// Weight scale of output row n: one per tensor, or, when rows is set, one
+// per output channel ([T alpha]_ij = T_ij alpha_j, the footnote to Eq. 2).
+struct WScale {
+  const float* rows;
+  float tensor;
+  __device__ __forceinline__ float at(int64_t n) const {
+    return rows ? as_global(rows)[n] : tensor;
+  }
+};
+
 // ---- host-side launchers (each returns a sherry_status) -------------------
 
 int launch_quantize(const float* x, int64_t m, int64_t k, int8_t* q,
                     float* x_scale, hipStream_t s);
 
 int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
-                     float w_scale, float* y, int32_t* acc, int64_t m,
+                     WScale ws, float* y, int32_t* acc, int64_t m,
                      int64_t n, int64_t k, hipStream_t s);
 
 int skinny_blocks(int64_t n);
-int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
+int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                   float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);
 int launch_skinny_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
                           int max_m, hipStream_t s);
 int launch_gemv_batched(const sherry_gemv_desc* descs, int count,
                         int64_t total_blocks, hipStream_t s);
-int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, float w_scale, float* y,
+int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, WScale ws, float* y,
                     int32_t* acc, int64_t n, int64_t k, hipStream_t s);
 int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_t total_blocks,
                             hipStream_t s);
@@ -176,7 +186,7 @@ int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_
 // 1 small (128 x 128), 2 mid (128 x 256), 3 large (256 x 256).
 int gemm_config_for(int64_t m, int64_t n);
 int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale,
-                     float w_scale, float* y, int32_t* acc, int64_t m,
+                     WScale ws, float* y, int32_t* acc, int64_t m,
                      int64_t n, int64_t k, hipStream_t s);
 
 int launch_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,
@@ -185,6 +195,9 @@ int launch_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,
 
 int launch_stream_read(const void* src, size_t bytes, uint32_t* sink,
                        hipStream_t s);
+
+int launch_ternarize_pack(const float* w, int64_t n, int64_t k, uint8_t* out, float* alpha,
+                          hipStream_t s);
 int64_t stream_read_groups(size_t bytes);
 
 // Records the HIP error of the calling thread's last failed library call

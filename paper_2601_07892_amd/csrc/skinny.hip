@@ -55,7 +55,7 @@ struct SkProblem {
   float* y;
   int32_t* acc;
   int n, k, m;
-  float w_scale;
+  WScale ws;
 };
 
 // Waits until at most N vector-memory loads of this wave are outstanding
@@ -398,7 +398,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
         const int tok = 32 * tb + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if (tok >= p.m) continue;
         const int32_t v = c[h][tb][e];
-        const float s = as_global(p.x_scale)[tok] * p.w_scale;
+        const float s = as_global(p.x_scale)[tok] * p.ws.at(row);
         as_global_mut(p.y)[int64_t(tok) * p.n + row] = static_cast<float>(v) * s;
         if (p.acc) as_global_mut(p.acc)[int64_t(tok) * p.n + row] = v;
       }
@@ -449,7 +449,7 @@ __global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
   }
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
-  const SkProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m, d.w_scale};
+  const SkProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m, WScale{nullptr, d.w_scale}};
   sk_block<MT, 1, NST>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
 }
 
@@ -506,10 +506,10 @@ int launch_skinny_mt(const SkProblem& p, hipStream_t s) {
   }
 }
 
-int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, float w_scale,
+int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                   float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
   const SkProblem p{w, x, x_scale, y, acc, static_cast<int>(n), static_cast<int>(k),
-                    static_cast<int>(m), w_scale};
+                    static_cast<int>(m), ws};
   if (m <= 32) return launch_skinny_mt<1>(p, s);
   return launch_skinny_mt<2>(p, s);
 }

@@ -266,3 +266,27 @@ def test_skinny_validation_without_launch():
     assert L.sherry_gemm_batched(FAKE, 1, 1, 65, None) == sh.SHERRY_E_SHAPE
     assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 16, None) == sh.SHERRY_E_ALIGN
     assert L.sherry_gemm_batched(None, 1, 1, 16, None) == sh.SHERRY_E_INVALID
+
+
+def test_channel_and_ternarize_validation_without_launch():
+    # per-channel products need a scale vector; ternarize-pack checks shape,
+    # buffer size and alignment before anything is enqueued
+    g = L.sherry_gemm_channel
+    assert g(FAKE, FAKE, FAKE, None, FAKE, None, 16, 64, 128, sh.SHERRY_KERNEL_SKINNY,
+             None) == sh.SHERRY_E_INVALID
+    assert g(FAKE, FAKE, FAKE, FAKE + 2, FAKE, None, 16, 64, 128, sh.SHERRY_KERNEL_SKINNY,
+             None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 5, 64, 128, sh.SHERRY_KERNEL_GEMV,
+             None) == sh.SHERRY_E_SHAPE
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, 64, 130, sh.SHERRY_KERNEL_AUTO,
+             None) == sh.SHERRY_E_SHAPE
+    f = L.sherry_gemv_f32_channel
+    assert f(FAKE, FAKE, FAKE, None, FAKE, None, 64, 128, None) == sh.SHERRY_E_INVALID
+    assert f(FAKE, FAKE, FAKE, FAKE + 1, FAKE, None, 64, 128, None) == sh.SHERRY_E_ALIGN
+    t = L.sherry_ternarize_pack
+    need = sh.sherry_packed_bytes(70, 132)
+    assert t(None, 70, 132, FAKE, need, None, None) == sh.SHERRY_E_INVALID
+    assert t(FAKE, 70, 130, FAKE, need, None, None) == sh.SHERRY_E_SHAPE
+    assert t(FAKE, 70, 132, FAKE, need - 1, None, None) == sh.SHERRY_E_BUFSIZE
+    assert t(FAKE + 4, 70, 132, FAKE, need, None, None) == sh.SHERRY_E_ALIGN
+    assert t(FAKE, 70, 132, FAKE, need, FAKE + 2, None) == sh.SHERRY_E_ALIGN

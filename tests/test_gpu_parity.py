@@ -655,3 +655,129 @@ def test_skinny_batched_model_step_sampled(dev, spec_name, m):
             assert acc[i, j] == r
             yr = oracle.epilogue(np.array([[r]], np.int32), sx[i:i + 1], sw)[0, 0]
             assert abs(float(yy[i, j]) - yr) <= RTOL * abs(yr)
+
+
+# ------------------------------------- per-channel scales (Eq. 5 per row)
+
+def _channel_scales(n, seed):
+    rng = np.random.default_rng(seed)
+    return (rng.random(n) * 0.05 + 0.001).astype(np.float32)
+
+
+# every kernel (GEMV up to 4 tokens, register-decoded, LDS-tiled) with ragged
+# n and k: int32 acc as the per-tensor path, y scaled per output channel
+CHANNEL_CASES = [(1, 70, 132, "GEMV"), (4, 600, 2048, "GEMV"), (9, 130, 1028, "SKINNY"),
+                 (100, 257, 388, "SKINNY"), (33, 300, 1032, "MFMA"), (300, 520, 2052, "MFMA")]
+
+
+@pytest.mark.parametrize("m,n,k,kernel", CHANNEL_CASES)
+def test_gemm_channel_parity(dev, m, n, k, kernel):
+    sh = _sh()
+    _say("channel", kernel, m, n, k)
+    t = synth.ternary_34(n, k, 61, "ch", n, k)
+    q = synth.int8_any(m, k, 61, "chq", m, k)
+    sx = np.abs(synth.activations(1, m, 61, "chs", m)[0]).astype(np.float32) + 0.01
+    sw = _channel_scales(n, 61)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+    acc = torch.full((m, n), -7, dtype=torch.int32, device=dev)
+    sh.sherry_gemm_channel(w, torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev),
+                           torch.from_numpy(sw).to(dev), y, acc, m, n, k,
+                           getattr(sh, "SHERRY_KERNEL_" + kernel))
+    torch.cuda.synchronize()
+    acc_ref = oracle.gemm_i32(q, t, threads=8)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref)
+    assert _y_ok(y.cpu().numpy(), oracle.epilogue_rows(acc_ref, sx, sw))
+
+
+@pytest.mark.parametrize("n,k", [(70, 132), (3072, 8192)])
+def test_gemv_f32_channel_parity(dev, n, k):
+    sh = _sh()
+    _say("f32 channel", n, k)
+    t = synth.ternary_34(n, k, 62, "fch", n, k)
+    x = synth.activations(1, k, 62, "fchx", n, k, outlier_frac=0.01)
+    sw = _channel_scales(n, 62)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    xs = torch.empty(1, dtype=torch.float32, device=dev)
+    y = torch.full((1, n), float("nan"), dtype=torch.float32, device=dev)
+    acc = torch.full((1, n), -7, dtype=torch.int32, device=dev)
+    sh.sherry_gemv_f32_channel(w, torch.from_numpy(x[0]).to(dev), xs, torch.from_numpy(sw).to(dev),
+                               y, acc, n, k)
+    torch.cuda.synchronize()
+    q, sx = oracle.quantize_act(x)
+    assert np.array_equal(xs.cpu().numpy(), sx)
+    acc_ref = oracle.gemm_i32(q, t, threads=8)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref)
+    assert _y_ok(y.cpu().numpy(), oracle.epilogue_rows(acc_ref, sx, sw))
+
+
+# --------------------------------- Sparse-AbsMean ternarize + pack (Eq. 4-5)
+
+def _weights_with_ties(n, k, seed):
+    w = synth.dense_weights(n, k, seed, "tp", n, k)
+    rng = np.random.default_rng(seed)
+    nb = k // 4
+    for _ in range(max(1, n * nb // 50)):
+        row, b = rng.integers(0, n), rng.integers(0, nb)
+        kind = rng.integers(0, 4)
+        blk = w[row, 4 * b:4 * b + 4]
+        if kind == 0:      # tie for the smallest magnitude
+            blk[:] = [0.5, -0.25, 0.25, -0.5]
+        elif kind == 1:    # zeros, also among the kept weights
+            blk[:] = [0.0, 0.0, -0.0, 0.3]
+        elif kind == 2:    # all equal magnitudes
+            blk[:] = [-0.1, 0.1, -0.1, 0.1]
+        else:              # negative zero kept as +1
+            blk[:] = [-0.0, 1.0, -2.0, 3.0]
+    return w
+
+
+def _ulp_close(a, b):
+    a = np.asarray(a, np.float32)
+    b = np.asarray(b, np.float32)
+    return bool(np.all(np.abs(a.astype(np.float64) - b.astype(np.float64)) <=
+                       np.spacing(np.maximum(np.abs(a), np.abs(b)))))
+
+
+@pytest.mark.parametrize("n,k", [(1, 4), (63, 128), (64, 132), (70, 1028), (130, 260),
+                                 (512, 4096), (8192, 3072)])
+def test_ternarize_pack_parity(dev, n, k):
+    # packed bytes identical to packing the oracle's ternary matrix (padding
+    # included); per-channel alpha within one fp32 unit of the oracle's fp64
+    # mean (the summation order differs)
+    sh = _sh()
+    _say("ternarize_pack", n, k)
+    w = _weights_with_ties(n, k, 63)
+    t_ref, alpha_ref = oracle.ternarize_rows(w)
+    packed_ref = oracle.pack(t_ref)
+    wd = torch.from_numpy(w).to(dev)
+    packed = torch.full((sh.sherry_packed_bytes(n, k),), 0xA5, dtype=torch.uint8, device=dev)
+    alpha = torch.full((n,), float("nan"), dtype=torch.float32, device=dev)
+    sh.sherry_ternarize_pack(wd, n, k, packed, alpha)
+    torch.cuda.synchronize()
+    assert np.array_equal(packed.cpu().numpy(), packed_ref)
+    assert _ulp_close(alpha.cpu().numpy(), alpha_ref.astype(np.float32))
+
+
+def test_ternarize_pack_then_channel_product(dev):
+    # fp32 weights -> GPU ternarize+pack -> per-channel product with the GPU
+    # alpha, against the oracle chain (ternarize_rows, quantize_act, gemm,
+    # epilogue_rows with the same alpha)
+    sh = _sh()
+    m, n, k = 16, 3072, 3072
+    _say("ternarize -> channel product", m, n, k)
+    w = synth.dense_weights(n, k, 64, "tpc")
+    x = synth.activations(m, k, 64, "tpcx", outlier_frac=0.01)
+    packed = torch.empty((sh.sherry_packed_bytes(n, k),), dtype=torch.uint8, device=dev)
+    alpha = torch.empty((n,), dtype=torch.float32, device=dev)
+    sh.sherry_ternarize_pack(torch.from_numpy(w).to(dev), n, k, packed, alpha)
+    q, sx = oracle.quantize_act(x)
+    y = torch.empty((m, n), dtype=torch.float32, device=dev)
+    acc = torch.empty((m, n), dtype=torch.int32, device=dev)
+    sh.sherry_gemm_channel(packed, torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev),
+                           alpha, y, acc, m, n, k)
+    torch.cuda.synchronize()
+    t_ref, _ = oracle.ternarize_rows(w)
+    acc_ref = oracle.gemm_i32(q, t_ref, threads=8)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref)
+    assert _y_ok(y.cpu().numpy(), oracle.epilogue_rows(acc_ref, sx, alpha.cpu().numpy()))
