@@ -80,6 +80,9 @@ class DecodeStep:
         self.ks = sorted({lin.k for _, lin in self.lins})
         self.x_host = {kk: synth.activations(sum(1 for _, l in self.lins if l.k == kk), kk, seed,
                                              "x", kk) for kk in self.ks}
+        self.channel_scales = [
+            torch.from_numpy((np.random.default_rng([seed, i]).random(lin.n) * 0.04 + 0.01)
+                             .astype(np.float32)).to(dev) for i, (_, lin) in enumerate(self.lins)]
         self.copies = []
         for c in range(copies):
             w = [torch.from_numpy(p).to(dev) for p in host_packed]
@@ -112,8 +115,12 @@ class DecodeStep:
                 f.n, f.k, f.w_scale = d.n, d.k, d.w_scale
             ftotal = sh.sherry_gemv_f32_batched_prepare(fdescs)
             fdev = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
+            # the same step with one weight scale per output channel (Eq. 5)
+            for i in range(self.count):
+                fdescs[i].w_scales = self.channel_scales[i].data_ptr()
+            fdev_ch = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
             self.copies.append(dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total,
-                                    fdescs=fdev, ftotal=ftotal))
+                                    fdescs=fdev, ftotal=ftotal, fdescs_ch=fdev_ch))
         torch.cuda.synchronize()
         self.total_blocks = self.copies[0]["total"]
         self.weight_bytes = sum(sh.sherry_packed_bytes(l.n, l.k) for _, l in self.lins)
@@ -143,6 +150,10 @@ class DecodeStep:
         cp = self.copies[c]
         self.sh.sherry_gemv_f32_batched(cp["fdescs"], self.count, cp["ftotal"])
 
+    def fused_channel(self, c):
+        cp = self.copies[c]
+        self.sh.sherry_gemv_f32_batched(cp["fdescs_ch"], self.count, cp["ftotal"])
+
 
 def _events(torch):
     return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -161,21 +172,53 @@ def settle(run, torch, seconds=0.02):
         torch.cuda.synchronize()
 
 
-def bench_fused(step: DecodeStep, torch, steps, warmup):
-    """ms per decode step (one fused launch), back to back after a heat-up."""
+def bench_fused(step: DecodeStep, torch, steps, warmup, channel=False):
+    """ms per decode step (one fused launch), back to back after a heat-up;
+    channel=True runs the step with per-channel weight scales."""
     ncp = len(step.copies)
+    run = step.fused_channel if channel else step.fused
     heat(step.sh, torch, step.dev)
-    settle(lambda i: step.fused(i % ncp), torch)
+    settle(lambda i: run(i % ncp), torch)
     for i in range(warmup):
-        step.fused(i % ncp)
+        run(i % ncp)
     start, stop = _events(torch)
     torch.cuda.synchronize()
     start.record()
     for i in range(steps):
-        step.fused(i % ncp)
+        run(i % ncp)
     stop.record()
     torch.cuda.synchronize()
     return start.elapsed_time(stop) / steps
+
+
+def bench_ternarize(sh, torch, dev, seed, shapes=(("llama-3.2-3b gate", 8192, 3072),
+                                                  ("stress-8b down", 4096, 14336)), reps=10):
+    """GB/s of the GPU Sparse-AbsMean ternarize + pack (fp32 W read, packed
+    layout and per-channel alpha written), over rotated weight copies."""
+    rows = []
+    for name, n, k in shapes:
+        w0 = torch.from_numpy(synth.dense_weights(n, k, seed, "tp", name)).to(dev)
+        ncp = max(2, -(-600_000_000 // (4 * n * k)))  # > 600 MB, past the Infinity Cache
+        ws = [w0.clone() for _ in range(ncp)]
+        packed = torch.empty(sh.sherry_packed_bytes(n, k), dtype=torch.uint8, device=dev)
+        alpha = torch.empty(n, dtype=torch.float32, device=dev)
+        for i in range(2):
+            sh.sherry_ternarize_pack(ws[i % ncp], n, k, packed, alpha)
+        start, stop = _events(torch)
+        torch.cuda.synchronize()
+        start.record()
+        for i in range(reps):
+            sh.sherry_ternarize_pack(ws[i % ncp], n, k, packed, alpha)
+        stop.record()
+        torch.cuda.synchronize()
+        us = start.elapsed_time(stop) / reps * 1e3
+        nbytes = 4 * n * k + sh.sherry_packed_bytes(n, k) + 4 * n
+        rows.append({"shape": name, "n": n, "k": k, "us": round(us, 2), "bytes": nbytes,
+                     "gbs": round(nbytes / us / 1e3, 1),
+                     "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)})
+        del ws, w0, packed, alpha
+        torch.cuda.empty_cache()
+    return rows
 
 
 def bench_unfused(step: DecodeStep, torch, steps, warmup):
@@ -575,6 +618,16 @@ def main():
                     "int8_product_bytes": step.gemv_bytes},
     }
     if not args.no_extra:
+        ms_ch = bench_fused(step, torch, args.steps, args.warmup, channel=True)
+        ch_bytes = step.fused_bytes + sum(4 * lin.n for _, lin in step.lins)
+        out["per_channel_decode_step"] = {
+            "step_us": round(ms_ch * 1e3, 2), "bytes_per_step": ch_bytes,
+            "gbs": round(ch_bytes / (ms_ch * 1e-3) / 1e9, 1),
+            "time_vs_per_tensor": round(ms_ch / ms_step, 4)}
+        log("decode step, per-channel scales: %.2f us" % (ms_ch * 1e3))
+        out["ternarize_pack"] = bench_ternarize(sh, torch, dev, args.seed)
+        for r in out["ternarize_pack"]:
+            log("ternarize+pack %s: %.1f us, %.0f GB/s" % (r["shape"], r["us"], r["gbs"]))
         try:
             out["hbm_read_ceiling_gbs"] = round(bench_stream_ceiling(sh, torch, dev), 1)
         except Exception as e:  # pragma: no cover

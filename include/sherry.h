@@ -193,7 +193,9 @@ typedef struct sherry_gemv_desc {
   const float* x_scale;  /* device, fp32 [1]                               */
   float* y;              /* device, fp32 [n]                               */
   int32_t* acc;          /* device, int32 [n] or NULL                      */
-  int64_t n, k;
+  const float* w_scales; /* device, fp32 [n] per-channel scales, or NULL   */
+                         /* for the per-tensor w_scale                     */
+  int32_t n, k;
   float w_scale;
   int32_t block_begin;   /* written by sherry_gemv_batched_prepare         */
 } sherry_gemv_desc;
@@ -224,6 +226,7 @@ typedef struct sherry_gemm_desc {
   const float* x_scale;  /* device, fp32 [m]                               */
   float* y;              /* device, fp32 [m][n]                            */
   int32_t* acc;          /* device, int32 [m][n] or NULL                   */
+  const float* w_scales; /* device, fp32 [n] per-channel scales, or NULL   */
   int32_t n, k, m;       /* 1 <= m <= 64                                   */
   float w_scale;
   int32_t block_begin;   /* written by sherry_gemm_batched_prepare         */
@@ -270,7 +273,8 @@ typedef struct sherry_gemv_f32_desc {
   float* x_scale;        /* device, fp32 [1] output, or NULL               */
   float* y;              /* device, fp32 [n]                               */
   int32_t* acc;          /* device, int32 [n] or NULL                      */
-  int64_t n, k;          /* k <= SHERRY_FUSED_MAX_K                        */
+  const float* w_scales; /* device, fp32 [n] per-channel scales, or NULL   */
+  int32_t n, k;          /* k <= SHERRY_FUSED_MAX_K                        */
   float w_scale;
   int32_t block_begin;   /* written by sherry_gemv_f32_batched_prepare     */
 } sherry_gemv_f32_desc;

@@ -90,6 +90,11 @@ extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
   return (m <= kSkinnyMaxM || k > n) ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
 }
 
+// The descriptor layouts are part of the ABI (Python and C callers build them).
+static_assert(sizeof(sherry_gemv_desc) == 64, "sherry_gemv_desc layout");
+static_assert(sizeof(sherry_gemv_f32_desc) == 64, "sherry_gemv_f32_desc layout");
+static_assert(sizeof(sherry_gemm_desc) == 72, "sherry_gemm_desc layout");
+
 namespace {
 // Product on the chosen kernel (kernel already resolved from AUTO).
 int gemm_dispatch(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws, float* y,
@@ -163,7 +168,8 @@ extern "C" int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
     sherry_gemv_desc& d = descs[i];
     int st = check_product(d.w, d.x, d.x_scale, d.y, 1, d.n, d.k, 4);
     if (st != SHERRY_OK) return st;
-    if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
+    if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)))
+      return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
     blocks += gemv_blocks(d.n, d.k, kGemvTarget);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
@@ -225,6 +231,7 @@ extern "C" int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int 
     sherry_gemv_f32_desc& d = descs[i];
     int st = check_fused(d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k);
     if (st != SHERRY_OK) return st;
+    if (d.w_scales && !aligned(d.w_scales, 4)) return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
     blocks += gemv_blocks(d.n, d.k, kFusedTarget);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
@@ -251,7 +258,8 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
     int st = check_product(d.w, d.x, d.x_scale, d.y, d.m, d.n, d.k, 16);
     if (st != SHERRY_OK) return st;
     if (d.m > kBatchedMaxM) return SHERRY_E_SHAPE;
-    if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
+    if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)))
+      return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
     d.reserved = 0;
     blocks += skinny_blocks(d.n);

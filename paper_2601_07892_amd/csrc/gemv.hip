@@ -221,6 +221,15 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
   prelude.issue();
   float sx[M];
   prelude.finish(sx);
+  // a per-channel scale for this thread's first output is loaded now, so
+  // its latency hides behind the stream instead of ending the workgroup
+  float sw0 = ws.tensor;
+  if (ws.rows && static_cast<int>(threadIdx.x) < tpb * M * 64) {
+    const int r0 = g * tpb + static_cast<int>(threadIdx.x >> 6) / M;
+    const int64_t row0 = int64_t(r0) * kTileRows + (threadIdx.x & 63);
+    if (r0 < R && row0 < n) sw0 = as_global(ws.rows)[row0];
+  }
+  __builtin_amdgcn_sched_barrier(0);
   uint32_t ring[kRing][5];
   ring_fill(ring, range);
   ring_run<M>(ring, range, c0, c1, xsrc, lut, acc);
@@ -238,7 +247,7 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
     if (r2 >= R || row >= n) continue;
     int32_t a = 0;
     for (int p = 0; p < S; ++p) a += red[((lt2 * S + p) * M + m) * 64 + i];
-    const float s = sx[m] * ws.at(row);
+    const float s = sx[m] * (t == static_cast<int>(threadIdx.x) ? sw0 : ws.at(row));
     as_global_mut(y)[m * n + row] = static_cast<float>(a) * s;
     if (acc_out) as_global_mut(acc_out)[m * n + row] = a;
   }
@@ -297,7 +306,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
   const int k = static_cast<int>(d.k);
   const int S = gemv_split(static_cast<int>((k + kTileK - 1) / kTileK));
   gemv_block<1>(d.w, XFromSgpr<1>{as_const(reinterpret_cast<const int32_t*>(d.x)), k},
-                ReadScales<1>{d.x_scale}, WScale{nullptr, d.w_scale}, d.y, d.acc, d.n, k,
+                ReadScales<1>{d.x_scale}, WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k,
                 blk - d.block_begin, S,
                 lut, red);
 }
@@ -441,7 +450,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
   const int k = static_cast<int>(d.k);
   const int C = (k + kTileK - 1) / kTileK;
   const int S = gemv_split(C, kFusedTarget);
-  fused_block(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{nullptr, d.w_scale}, d.y, d.acc,
+  fused_block(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{d.w_scales, d.w_scale}, d.y, d.acc,
               d.n, k,
               blk - d.block_begin, S, lut, red, part, xq);
 }

@@ -449,7 +449,7 @@ __global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
   }
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
-  const SkProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m, WScale{nullptr, d.w_scale}};
+  const SkProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m, WScale{d.w_scales, d.w_scale}};
   sk_block<MT, 1, NST>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
 }
 

@@ -3,13 +3,13 @@
 // channel out, with the same bytes as sherry_pack applied to the ternary
 // matrix of Eq. 4.
 //
-// Work mapping.  A workgroup owns one 64-row tile; lane i of every wave is
-// row i, so a wave turns one unit (64 rows x 128 weights) into its 16-byte
-// head and 4-byte tail per lane directly, and the eight waves take the
-// tile's units in turn.  Each lane reads its row's 128 values as 32 16-byte
-// loads (one block of 4 per load); the 64 rows of a load are 64 cache lines,
-// each used by 8 consecutive loads.  The kept magnitudes of each row are
-// summed in fp64 per wave and the eight partial sums are added in wave order.
+// Work mapping.  A workgroup owns RW rows (64, 32 or 16) of one 64-row tile
+// and all of their units; lane l of a wave is row l % RW and unit slot l / RW,
+// so a lane turns one row of one unit (128 weights) into its 16-byte head
+// and 4-byte tail directly.  Each lane reads its 128 values as 32 16-byte
+// loads (one block of 4 per load).  Fewer rows per workgroup give small-N
+// matrices more workgroups.  The kept magnitudes are summed in fp64 per
+// lane and the partial sums of each row are added in a fixed order.
 #include "sherry_internal.h"
 
 namespace sherry {
@@ -65,33 +65,39 @@ __device__ __forceinline__ void tp_unit(const float* row_w, bool in, int64_t b0,
       ...);
 }
 
+template <int RW>
 __global__ __launch_bounds__(kTpThreads) void ternarize_pack_kernel(
     const float* __restrict__ w, int64_t n, int64_t k, uint8_t* __restrict__ out,
     float* __restrict__ alpha) {
+  constexpr int SLOTS = 64 / RW;  // units in flight per wave
   __shared__ double red[kTpWaves * 64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t r = blockIdx.x;
-  const int64_t row = r * kTileRows + lane;
+  const int64_t r = blockIdx.x / SLOTS;           // tile
+  const int ri = (blockIdx.x % SLOTS) * RW + lane % RW;  // row within the tile
+  const int64_t row = r * kTileRows + ri;
   const int64_t C = (k + kTileK - 1) / kTileK, nb = k / 4;
   const bool in = row < n;
   const float* row_w = w + (in ? row : 0) * k;
   double kept = 0.0;
-  for (int64_t c = wave; c < C; c += kTpWaves) {
+  for (int64_t c = wave * SLOTS + lane / RW; c < C; c += kTpWaves * SLOTS) {
     uint32_t d[5] = {0, 0, 0, 0, 0};
     tp_unit(row_w, in, c * 32, nb, d, kept, std::make_integer_sequence<int, 32>{});
     uint8_t* unit = out + (r * C + c) * kUnitBytes;
-    *reinterpret_cast<uint4*>(as_global_mut(unit + 16 * lane)) = make_uint4(d[0], d[1], d[2], d[3]);
-    *reinterpret_cast<uint32_t*>(as_global_mut(unit + kHeadBytes + 4 * lane)) = d[4];
+    *reinterpret_cast<uint4*>(as_global_mut(unit + 16 * ri)) = make_uint4(d[0], d[1], d[2], d[3]);
+    *reinterpret_cast<uint32_t*>(as_global_mut(unit + kHeadBytes + 4 * ri)) = d[4];
   }
   red[wave * 64 + lane] = kept;
   __syncthreads();
-  if (wave == 0 && in && alpha) {
-    double s = 0.0;
-#pragma unroll
-    for (int q = 0; q < kTpWaves; ++q) s += red[q * 64 + lane];
-    // Eq. 5: mean |W| over the row's kept weights (three per block)
-    as_global_mut(alpha)[row] = static_cast<float>(s / static_cast<double>(3 * nb));
+  if (threadIdx.x < RW) {
+    const int64_t arow = r * kTileRows + (blockIdx.x % SLOTS) * RW + threadIdx.x;
+    if (arow < n && alpha) {
+      double s = 0.0;
+      for (int q = 0; q < kTpWaves * SLOTS; ++q)  // wave-major, then slot
+        s += red[(q / SLOTS) * 64 + (q % SLOTS) * RW + threadIdx.x];
+      // Eq. 5: mean |W| over the row's kept weights (three per block)
+      as_global_mut(alpha)[arow] = static_cast<float>(s / static_cast<double>(3 * nb));
+    }
   }
 }
 
@@ -99,8 +105,17 @@ __global__ __launch_bounds__(kTpThreads) void ternarize_pack_kernel(
 
 int launch_ternarize_pack(const float* w, int64_t n, int64_t k, uint8_t* out, float* alpha,
                           hipStream_t s) {
-  return launch(ternarize_pack_kernel, dim3(static_cast<unsigned>(ceil_div(n, kTileRows))),
-                dim3(kTpThreads), 0, s, w, n, k, out, alpha);
+  const int64_t R = ceil_div(n, kTileRows);
+  const dim3 block(kTpThreads);
+  // rows per workgroup: whole tiles when there are enough of them
+  if (R >= 256)
+    return launch(ternarize_pack_kernel<64>, dim3(static_cast<unsigned>(R)), block, 0, s, w, n,
+                  k, out, alpha);
+  if (R >= 128)
+    return launch(ternarize_pack_kernel<32>, dim3(static_cast<unsigned>(2 * R)), block, 0, s, w,
+                  n, k, out, alpha);
+  return launch(ternarize_pack_kernel<16>, dim3(static_cast<unsigned>(4 * R)), block, 0, s, w, n,
+                k, out, alpha);
 }
 
 }  // namespace sherry

@@ -254,7 +254,7 @@ def test_skinny_validation_without_launch():
     total, max_m = sh.sherry_gemm_batched_prepare(descs)
     # one workgroup per 8 row tiles: 32 tiles -> 4, 128 -> 16, 2 -> 1
     assert [d.block_begin for d in descs] == [0, 4, 20] and total == 21 and max_m == 64
-    assert ctypes.sizeof(sh.sherry_gemm_desc) == 64
+    assert ctypes.sizeof(sh.sherry_gemm_desc) == 72
     # a grouped launch stages at most one 64-token block per product
     descs[1].m = 65
     with pytest.raises(sh.SherryError):

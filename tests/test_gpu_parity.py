@@ -343,7 +343,27 @@ def test_guard_bands_and_determinism(dev):
 
 # ---------------------------------------------------------- batched decode
 
-def _batched(dev, shapes, seed, want_acc=True):
+def _epi(acc, sx, sw):
+    """Oracle epilogue for a per-tensor (float) or per-channel (array) scale."""
+    if np.ndim(sw):
+        return oracle.epilogue_rows(acc, sx, sw)
+    return oracle.epilogue(acc, sx, sw)
+
+
+def _desc_scale(d, dev, keep, n, seed, i, channel):
+    """Per-tensor scale, or (channel and even i) a per-channel vector in
+    d.w_scales; returns what the oracle epilogue takes."""
+    if channel and i % 2 == 0:
+        sw = _channel_scales(n, seed * 1000 + i)
+        swd = torch.from_numpy(sw).to(dev)
+        keep.append(swd)
+        d.w_scales = swd.data_ptr()
+        d.w_scale = float("nan")  # unused
+        return sw
+    return None
+
+
+def _batched(dev, shapes, seed, want_acc=True, channel=False):
     sh = _sh()
     descs = (sh.sherry_gemv_desc * len(shapes))()
     keep, refs = [], []
@@ -362,6 +382,8 @@ def _batched(dev, shapes, seed, want_acc=True):
         d.w, d.x, d.x_scale, d.y = w.data_ptr(), qd.data_ptr(), sxd.data_ptr(), y.data_ptr()
         d.acc = a.data_ptr() if want_acc else None
         d.n, d.k, d.w_scale = n, k, sw
+        swc = _desc_scale(d, dev, keep, n, seed, i, channel)
+        sw = sw if swc is None else swc
         refs.append((t, q, sx, sw, y, a))
     total = sh.sherry_gemv_batched_prepare(descs)
     ddev = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
@@ -377,6 +399,16 @@ def test_batched_gemv_parity(dev):
         acc_ref = oracle.gemm_i32(q, t, threads=8)
         assert np.array_equal(a.cpu().numpy(), acc_ref[0])
         assert _y_ok(y.cpu().numpy(), oracle.epilogue(acc_ref, sx, sw)[0])
+
+
+def test_batched_gemv_channel_scales(dev):
+    # per-channel scales in half of the descriptors of one grouped launch
+    _say("batched channel scales")
+    shapes = [(64, 128), (65, 132), (2048, 2048), (512, 2048), (300, 8192), (1, 4), (70, 1032)]
+    for t, q, sx, sw, y, a in _batched(dev, shapes, 47, channel=True):
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a.cpu().numpy(), acc_ref[0])
+        assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw)[0])
 
 
 def test_batched_split_paths(dev):
@@ -503,10 +535,10 @@ def test_fused_gemv_zero_row_and_no_outputs(dev):
     assert _y_ok(y.cpu().numpy(), y_ref[0])
 
 
-def _fused_batched(dev, shapes, seed, with_scale=True):
+def _fused_batched(dev, shapes, seed, with_scale=True, channel=False):
     sh = _sh()
     descs = (sh.sherry_gemv_f32_desc * len(shapes))()
-    keep = []
+    keep, hold = [], []
     for i, (n, k) in enumerate(shapes):
         t = synth.ternary_34(n, k, seed, "fb", i)
         x = synth.activations(1, k, seed, "fbx", i, outlier_frac=0.01)
@@ -520,7 +552,8 @@ def _fused_batched(dev, shapes, seed, with_scale=True):
         d.w, d.x, d.y, d.acc = w.data_ptr(), xd.data_ptr(), y.data_ptr(), a.data_ptr()
         d.x_scale = sxd.data_ptr() if with_scale else None
         d.n, d.k, d.w_scale = n, k, sw
-        keep.append((t, x, sw, w, xd, sxd, y, a))
+        swc = _desc_scale(d, dev, hold, n, seed, i, channel)
+        keep.append((t, x, sw if swc is None else swc, w, xd, sxd, y, a))
     total = sh.sherry_gemv_f32_batched_prepare(descs)
     dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
     sh.sherry_gemv_f32_batched(dd, len(shapes), total)
@@ -537,6 +570,17 @@ def test_fused_batched_parity(dev):
         assert sxd.cpu().numpy()[0] == sx_ref[0]
         assert np.array_equal(a.cpu().numpy(), acc_ref[0])
         assert _y_ok(y.cpu().numpy(), y_ref[0])
+
+
+def test_fused_batched_channel_scales(dev):
+    _say("fused batched channel scales")
+    shapes = [(64, 128), (65, 132), (2048, 2048), (300, 8192), (1, 4), (100, 8196)]
+    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 51, channel=True):
+        q, sx = oracle.quantize_act(x)
+        assert sxd.cpu().numpy()[0] == sx[0]
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a.cpu().numpy(), acc_ref[0])
+        assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw)[0])
 
 
 def test_fused_batched_decode_step_llama_1b(dev):
@@ -598,10 +642,10 @@ def test_skinny_extreme_values(dev):
     assert np.array_equal(acc, oracle.gemm_i32(q, t, threads=8))
 
 
-def _skinny_batched(dev, cases, seed):
+def _skinny_batched(dev, cases, seed, channel=False):
     sh = _sh()
     descs = (sh.sherry_gemm_desc * len(cases))()
-    keep = []
+    keep, hold = [], []
     for i, (m, n, k) in enumerate(cases):
         t = synth.ternary_34(n, k, seed, "sb", i)
         q = synth.int8_any(m, k, seed, "sbq", i)
@@ -616,12 +660,23 @@ def _skinny_batched(dev, cases, seed):
         d.w, d.x, d.x_scale, d.y, d.acc = (w.data_ptr(), qd.data_ptr(), sxd.data_ptr(),
                                            y.data_ptr(), a.data_ptr())
         d.n, d.k, d.m, d.w_scale = n, k, m, sw
-        keep.append((t, q, sx, sw, w, qd, sxd, y, a))
+        swc = _desc_scale(d, dev, hold, n, seed, i, channel)
+        keep.append((t, q, sx, sw if swc is None else swc, w, qd, sxd, y, a))
     total, max_m = sh.sherry_gemm_batched_prepare(descs)
     dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
     sh.sherry_gemm_batched(dd, len(cases), total, max_m)
     torch.cuda.synchronize()
     return keep, max_m
+
+
+def test_skinny_batched_channel_scales(dev):
+    _say("skinny batched channel scales")
+    cases = [(5, 64, 128), (16, 65, 132), (1, 600, 2048), (32, 512, 3072), (64, 300, 2052)]
+    keep, _ = _skinny_batched(dev, cases, 55, channel=True)
+    for t, q, sx, sw, w, qd, sxd, y, a in keep:
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a.cpu().numpy(), acc_ref)
+        assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw))
 
 
 @pytest.mark.parametrize("big", [False, True])
