@@ -537,9 +537,11 @@ def main():
                     help="rotated weight copies (working set = copies x 152 MB)")
     ap.add_argument("--no-extra", action="store_true", help="skip the M=2048 GEMM and ceiling")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--only", choices=["decode", "product"], default=None,
-                    help="run only the timed decode steps, or only the back-to-back "
-                         "product launches (for profiler runs)")
+    ap.add_argument("--only", choices=["decode", "product", "prefill", "grouped", "ternarize"],
+                    default=None,
+                    help="run only one part (for profiler runs): the timed decode steps, the "
+                         "back-to-back product launches, the M=2048 LLaMA-3.2-3B layer, the "
+                         "grouped small-M steps, or ternarize + pack")
     ap.add_argument("--product-launches", type=int, default=1000,
                     help="back-to-back grouped product launches timed for the roofline")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -569,6 +571,20 @@ def main():
         return
     if args.only:
         args.no_extra = args.no_cpu = True
+    if args.only == "prefill":
+        r = bench_prefill(sh, torch, dev, synth.LLAMA_3B, 2048, args.seed)
+        print(json.dumps({"prefill_m2048_llama-3.2-3b": r}), flush=True)
+        return
+    if args.only == "grouped":
+        rows = [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2)
+                for mm in (4, 16)]
+        rows.append(bench_model_step_m(sh, torch, dev, synth.STRESS_8B, args.seed, 64, 1))
+        print(json.dumps({"decode_small_m_grouped": rows}), flush=True)
+        return
+    if args.only == "ternarize":
+        print(json.dumps({"ternarize_pack": bench_ternarize(sh, torch, dev, args.seed)}),
+              flush=True)
+        return
 
     step = DecodeStep(sh, torch, dev, synth.LLAMA_1B, args.seed, copies=args.copies)
     if args.only == "product":
