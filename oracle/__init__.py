@@ -238,6 +238,42 @@ def epilogue_rows(acc: np.ndarray, sx: np.ndarray, sw: np.ndarray) -> np.ndarray
     return y
 
 
+GROUP = 128  # weights per scale group along K (the paper's group size 128)
+
+
+def product_groups(x: np.ndarray, t: np.ndarray, sx: np.ndarray, s_groups: np.ndarray,
+                   threads: int = 1):
+    """Per-group weight scales (group size 128 along K, the paper's default
+    granularity): y[m][n] = sx[m] * sum_g acc_g[m][n] * s[n][g], where acc_g
+    is the exact integer product over K values [128 g, 128 g + 128).  fp64.
+
+    Returns (y, mag, acc): mag[m][n] = sx[m] * sum_g |acc_g * s[n][g]| (the
+    scale of the rounding error of any fp32 summation order) and acc the
+    int32 sum over all groups."""
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    t = np.ascontiguousarray(t, dtype=np.int8)
+    if x.ndim == 1:
+        x = x[None, :]
+    m, k = x.shape
+    n = t.shape[0]
+    g_count = (k + GROUP - 1) // GROUP
+    s_groups = np.asarray(s_groups, dtype=np.float32)
+    if s_groups.shape != (n, g_count):
+        raise OracleError("group scales must be [n][ceil(k/128)]")
+    sx = np.asarray(sx, dtype=np.float32).astype(np.float64)
+    y = np.zeros((m, n), dtype=np.float64)
+    mag = np.zeros((m, n), dtype=np.float64)
+    acc = np.zeros((m, n), dtype=np.int64)
+    for g in range(g_count):
+        lo, hi = g * GROUP, min(k, (g + 1) * GROUP)
+        a = gemm_i32(x[:, lo:hi], t[:, lo:hi], threads=threads).astype(np.float64)
+        term = a * s_groups[:, g].astype(np.float64)[None, :]
+        y += term
+        mag += np.abs(term)
+        acc += a.astype(np.int64)
+    return y * sx[:, None], mag * sx[:, None], acc.astype(np.int32)
+
+
 # ---- (vi) Sparse-AbsMean ternarizer (Eq. 4, Eq. 5) -------------------------
 
 def ternarize(w: np.ndarray):

@@ -338,6 +338,34 @@ def test_epilogue_rows_is_dequantized_product():
     assert np.array_equal(y1, oracle.epilogue(acc, sx, float(sw[0])))
 
 
+def test_product_groups_pins():
+    # per-group scales (group 128 along K): (1) equal scales across a row's
+    # groups give the per-channel product; (2) the dequantized operands
+    # multiplied in the other order give the same y; (3) a scale in one group
+    # only isolates that K slice (catches an off-by-one in the grouping)
+    rng = np.random.default_rng(21)
+    m, n, k = 3, 7, 300  # three groups, the last one partial (44 values)
+    q = rng.integers(-127, 128, (m, k)).astype(np.int8)
+    t = synth.ternary_34(n, k, 21, "grp")
+    sx = (rng.random(m) + 0.01).astype(np.float32)
+    s = (rng.random((n, 3)) * 0.05 + 0.001).astype(np.float32)
+    y, mag, acc = oracle.product_groups(q, t, sx, s)
+    assert np.array_equal(acc, oracle.gemm_i32(q, t))
+    ch = np.repeat(s[:, :1], 3, axis=1)
+    y1, _, _ = oracle.product_groups(q, t, sx, ch)
+    assert np.allclose(y1, oracle.epilogue_rows(oracle.gemm_i32(q, t), sx, s[:, 0]),
+                       rtol=1e-12, atol=0)
+    s_exp = np.repeat(s.astype(np.float64), 128, axis=1)[:, :k]
+    ref = (q.astype(np.float64) * sx.astype(np.float64)[:, None]) @ \
+        (t.astype(np.float64) * s_exp).T
+    assert np.allclose(y, ref, rtol=1e-12, atol=0)
+    assert np.all(mag >= np.abs(y) * (1 - 1e-12))
+    one = np.zeros_like(s)
+    one[:, 2] = 1.0
+    y2, _, _ = oracle.product_groups(q, t, np.ones(m, np.float32), one)
+    assert np.array_equal(y2, oracle.gemm_i32(q[:, 256:], t[:, 256:]).astype(np.float64))
+
+
 def test_ternarizer_ties_and_zeros():
     w = np.array([[0.5, -0.5, 0.5, -0.5, 0.0, 0.0, 1.0, -2.0]], np.float32)
     t, _ = oracle.ternarize(w)
