@@ -183,6 +183,23 @@ int sherry_gemm_channel(const uint8_t* w, const int8_t* x, const float* x_scale,
                         const float* w_scales, float* y, int32_t* acc, int64_t m,
                         int64_t n, int64_t k, int kernel, void* stream);
 
+/* Per-group weight scales, group size 128 along k (the paper's default
+ * granularity, Sec. 4.1; one scale per output channel and group).
+ * w_group_scales: device, fp32 [n][ceil(k/128)] row-major, 4-byte aligned.
+ * y[i][j] = x_scale[i] * sum_g float(acc_g[i][j]) * w_group_scales[j][g],
+ * where acc_g is the exact int32 product over k in [128g, 128g + 128); the
+ * sum runs in fp32 in ascending g within each part of the kernel's split of
+ * k, and the parts are added in order (so y is within (G + 4) * 2^-24 of
+ * x_scale * sum_g |acc_g * scale| of the exact value, G = ceil(k/128)).
+ * acc, if not NULL, receives sum_g acc_g (the unscaled int32 product).
+ * kernel: SHERRY_KERNEL_AUTO (GEMV for m <= 4, else register-decoded),
+ * SHERRY_KERNEL_GEMV (m <= 4) or SHERRY_KERNEL_SKINNY; the LDS-tiled kernel
+ * has no per-group epilogue (SHERRY_E_INVALID).  SHERRY_E_INVALID if
+ * w_group_scales is NULL. */
+int sherry_gemm_group(const uint8_t* w, const int8_t* x, const float* x_scale,
+                      const float* w_group_scales, float* y, int32_t* acc, int64_t m,
+                      int64_t n, int64_t k, int kernel, void* stream);
+
 /* ---------------------------------------------------------------------- */
 /* Grouped M = 1 products: many independent GEMVs in one launch.           */
 /* ---------------------------------------------------------------------- */
@@ -266,6 +283,12 @@ int sherry_gemv_f32(const uint8_t* w, const float* x, float* x_scale,
 int sherry_gemv_f32_channel(const uint8_t* w, const float* x, float* x_scale,
                             const float* w_scales, float* y, int32_t* acc,
                             int64_t n, int64_t k, void* stream);
+
+/* sherry_gemv_f32 with per-group weight scales (w_group_scales and the
+ * result as in sherry_gemm_group). */
+int sherry_gemv_f32_group(const uint8_t* w, const float* x, float* x_scale,
+                          const float* w_group_scales, float* y, int32_t* acc,
+                          int64_t n, int64_t k, void* stream);
 
 typedef struct sherry_gemv_f32_desc {
   const uint8_t* w;      /* device, packed n x k, 16-byte aligned          */

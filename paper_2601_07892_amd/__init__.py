@@ -38,6 +38,7 @@ EXPORTS = [
     "sherry_stream_read_groups", "sherry_gemv_f32", "sherry_gemv_f32_batched_prepare",
     "sherry_gemv_f32_batched", "sherry_gemm_batched_prepare", "sherry_gemm_batched",
     "sherry_gemm_channel", "sherry_gemv_f32_channel", "sherry_ternarize_pack",
+    "sherry_gemm_group", "sherry_gemv_f32_group",
 ]
 
 
@@ -121,6 +122,9 @@ def _load():
                                 ctypes.c_int),
         "sherry_gemv_f32_channel": ([vp, vp, vp, vp, vp, vp, i64, i64, vp], ctypes.c_int),
         "sherry_ternarize_pack": ([vp, i64, i64, vp, ctypes.c_size_t, vp, vp], ctypes.c_int),
+        "sherry_gemm_group": ([vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp],
+                              ctypes.c_int),
+        "sherry_gemv_f32_group": ([vp, vp, vp, vp, vp, vp, i64, i64, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -246,6 +250,21 @@ def sherry_gemm_channel(w, x, x_scale, w_scales, y, acc, m: int, n: int, k: int,
     _check(lib.sherry_gemm_channel(_ptr(w), _ptr(x), _ptr(x_scale), _ptr(w_scales), _ptr(y),
                                    _ptr(acc), m, n, k, int(kernel), _stream(stream)),
            "sherry_gemm_channel")
+
+
+def sherry_gemm_group(w, x, x_scale, w_group_scales, y, acc, m: int, n: int, k: int,
+                      kernel: int = SHERRY_KERNEL_AUTO, stream=None):
+    """Product with per-group weight scales (fp32 [n][ceil(k/128)])."""
+    _check(lib.sherry_gemm_group(_ptr(w), _ptr(x), _ptr(x_scale), _ptr(w_group_scales), _ptr(y),
+                                 _ptr(acc), m, n, k, int(kernel), _stream(stream)),
+           "sherry_gemm_group")
+
+
+def sherry_gemv_f32_group(w, x, x_scale, w_group_scales, y, acc, n: int, k: int, stream=None):
+    """Fused quantization + M = 1 product with per-group weight scales."""
+    _check(lib.sherry_gemv_f32_group(_ptr(w), _ptr(x), _ptr(x_scale), _ptr(w_group_scales),
+                                     _ptr(y), _ptr(acc), n, k, _stream(stream)),
+           "sherry_gemv_f32_group")
 
 
 def sherry_ternarize_pack(w, n: int, k: int, packed, alpha=None, stream=None):

@@ -132,6 +132,29 @@ extern "C" int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_
   return gemm_dispatch(w, x, x_scale, WScale{nullptr, w_scale}, y, acc, m, n, k, kernel, stream);
 }
 
+extern "C" int sherry_gemm_group(const uint8_t* w, const int8_t* x, const float* x_scale,
+                                 const float* w_group_scales, float* y, int32_t* acc, int64_t m,
+                                 int64_t n, int64_t k, int kernel, void* stream) {
+  if (!w_group_scales) return SHERRY_E_INVALID;
+  if (!aligned(w_group_scales, 4)) return SHERRY_E_ALIGN;
+  if (kernel == SHERRY_KERNEL_AUTO) kernel = m <= kGemvMaxM ? SHERRY_KERNEL_GEMV : SHERRY_KERNEL_SKINNY;
+  if (kernel == SHERRY_KERNEL_GEMV) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 4);
+    if (st != SHERRY_OK) return st;
+    if (m > kGemvMaxM) return SHERRY_E_SHAPE;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_gemv_group(w, x, x_scale, w_group_scales, y, acc, m, n, k, as_stream(stream));
+  }
+  if (kernel == SHERRY_KERNEL_SKINNY) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 16);
+    if (st != SHERRY_OK) return st;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_skinny_group(w, x, x_scale, w_group_scales, y, acc, m, n, k,
+                               as_stream(stream));
+  }
+  return SHERRY_E_INVALID;  // the LDS-tiled kernel has no per-group epilogue
+}
+
 extern "C" int sherry_gemm_channel(const uint8_t* w, const int8_t* x, const float* x_scale,
                                    const float* w_scales, float* y, int32_t* acc, int64_t m,
                                    int64_t n, int64_t k, int kernel, void* stream) {
@@ -221,6 +244,16 @@ extern "C" int sherry_gemv_f32_channel(const uint8_t* w, const float* x, float* 
   if (!aligned(w_scales, 4)) return SHERRY_E_ALIGN;
   return launch_gemv_f32(w, x, x_scale, WScale{w_scales, 0.0f}, y, acc, n, k,
                          as_stream(stream));
+}
+
+extern "C" int sherry_gemv_f32_group(const uint8_t* w, const float* x, float* x_scale,
+                                     const float* w_group_scales, float* y, int32_t* acc,
+                                     int64_t n, int64_t k, void* stream) {
+  int st = check_fused(w, x, x_scale, y, acc, n, k);
+  if (st != SHERRY_OK) return st;
+  if (!w_group_scales) return SHERRY_E_INVALID;
+  if (!aligned(w_group_scales, 4)) return SHERRY_E_ALIGN;
+  return launch_gemv_f32_group(w, x, x_scale, w_group_scales, y, acc, n, k, as_stream(stream));
 }
 
 extern "C" int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int count,

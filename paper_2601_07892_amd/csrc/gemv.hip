@@ -190,15 +190,64 @@ __device__ __forceinline__ void ring_run(uint32_t (&ring)[kRing][5], __amdgpu_bu
   }
 }
 
+// Per-group scales (one per output row and 128 weights along K, i.e. per
+// container): the same ring, plus one 4-byte scale per lane and container
+// loaded with it through a resource over the tile's rows of the [n][G] scale
+// matrix.  Each container's int32 sum is scaled into an fp32 accumulator
+// (ascending container order) and also added to the int32 total.
+__device__ __forceinline__ float load_group_scale(__amdgpu_buffer_rsrc_t gr, int G, int c,
+                                                  int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(gr, 4 * (lane * G + c), 0, 0));
+}
+
+template <int M, class X>
+__device__ __forceinline__ void ring_run_groups(uint32_t (&ring)[kRing][5],
+                                                __amdgpu_buffer_rsrc_t r,
+                                                __amdgpu_buffer_rsrc_t gr, int G, int c0, int c1,
+                                                const X& xsrc, const uint32_t* lut,
+                                                int32_t (&acc)[M], float (&accf)[M]) {
+  const int lane = threadIdx.x & 63;
+  const int n = c1 - c0;
+  float gring[kRing];
+#pragma unroll
+  for (int u = 0; u < kRing; ++u) gring[u] = load_group_scale(gr, G, c0 + u, lane);
+  for (int i = 0; i < n; i += kRing) {
+#pragma unroll
+    for (int u = 0; u < kRing; ++u) {
+      if (i + u < n) {
+        int32_t a[M];
+#pragma unroll
+        for (int m = 0; m < M; ++m) a[m] = 0;
+        xsrc.dot(ring[u], c0 + i + u, lut, a);
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          accf[m] = __builtin_fmaf(static_cast<float>(a[m]), gring[u], accf[m]);
+          acc[m] += a[m];
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      load_container(ring[u], r, i + u + kRing, lane);
+      gring[u] = load_group_scale(gr, G, c0 + i + u + kRing, lane);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
 // One workgroup of a product: block g of a problem whose tiles are split
 // over S waves each.  prelude.issue() then prelude.finish(sx) run before the
 // weight stream; finish yields the tokens' activation scales sx[m].  lut and red are
 // LDS; the caller has filled lut.
-template <int M, class X, class Prelude>
+//
+// With kGrp the weights carry per-group scales gs ([n][ceil(k/128)] fp32):
+// y = sx * sum over containers of float(acc_c) * gs[row][c], summed in fp32
+// in container order per wave and then over the S waves in order; redf is
+// LDS for the fp32 partial sums.
+template <int M, bool kGrp = false, class X, class Prelude>
 __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Prelude prelude,
                                            WScale ws, float* y, int32_t* acc_out, int64_t n,
                                            int k, int g, int S, const uint32_t* lut,
-                                           int32_t* red) {
+                                           int32_t* red, const float* gs = nullptr,
+                                           float* redf = nullptr) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int C = (k + kTileK - 1) / kTileK;
@@ -232,10 +281,26 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
   __builtin_amdgcn_sched_barrier(0);
   uint32_t ring[kRing][5];
   ring_fill(ring, range);
-  ring_run<M>(ring, range, c0, c1, xsrc, lut, acc);
+  float accf[M];
+  if constexpr (kGrp) {
+    // scale rows of this wave's tile (rows past n read zero)
+    const int rows = (r < R) ? static_cast<int>(n - int64_t(r) * kTileRows) : 0;
+    const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(gs) + int64_t(r < R ? r : 0) * kTileRows * C, 0,
+        (rows < kTileRows ? rows : kTileRows) * C * 4, kBufferWord3);
+#pragma unroll
+    for (int m = 0; m < M; ++m) accf[m] = 0.0f;
+    ring_run_groups<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
+  } else {
+    ring_run<M>(ring, range, c0, c1, xsrc, lut, acc);
+  }
 
 #pragma unroll
   for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + lane] = acc[m];
+  if constexpr (kGrp) {
+#pragma unroll
+    for (int m = 0; m < M; ++m) redf[(wave * M + m) * 64 + lane] = accf[m];
+  }
   __syncthreads();
   // thread t -> (tile lt2, token m, row i); the S waves of a tile are adjacent
   for (int t = threadIdx.x; t < tpb * M * 64; t += kGemvThreads) {
@@ -247,8 +312,14 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
     if (r2 >= R || row >= n) continue;
     int32_t a = 0;
     for (int p = 0; p < S; ++p) a += red[((lt2 * S + p) * M + m) * 64 + i];
-    const float s = sx[m] * (t == static_cast<int>(threadIdx.x) ? sw0 : ws.at(row));
-    as_global_mut(y)[m * n + row] = static_cast<float>(a) * s;
+    if constexpr (kGrp) {
+      float f = 0.0f;
+      for (int p = 0; p < S; ++p) f += redf[((lt2 * S + p) * M + m) * 64 + i];
+      as_global_mut(y)[m * n + row] = f * sx[m];
+    } else {
+      const float s = sx[m] * (t == static_cast<int>(threadIdx.x) ? sw0 : ws.at(row));
+      as_global_mut(y)[m * n + row] = static_cast<float>(a) * s;
+    }
     if (acc_out) as_global_mut(acc_out)[m * n + row] = a;
   }
 }
@@ -279,6 +350,22 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(
   gemv_block<M>(w, XFromSgpr<M>{as_const(reinterpret_cast<const int32_t*>(x)), static_cast<int>(k)},
                 ReadScales<M>{x_scale}, ws, y, acc, n, static_cast<int>(k), blockIdx.x, split,
                 lut, red);
+}
+
+template <int M>
+__global__ __launch_bounds__(kGemvThreads) void gemv_group_kernel(
+    const uint8_t* __restrict__ w, const int8_t* __restrict__ x,
+    const float* __restrict__ x_scale, const float* __restrict__ gs, float* __restrict__ y,
+    int32_t* __restrict__ acc, int64_t n, int64_t k, int split) {
+  __shared__ uint32_t lut[32];
+  __shared__ int32_t red[kGemvWaves * M * 64];
+  __shared__ float redf[kGemvWaves * M * 64];
+  fill_lut(lut);
+  gemv_block<M, true>(w,
+                      XFromSgpr<M>{as_const(reinterpret_cast<const int32_t*>(x)),
+                                   static_cast<int>(k)},
+                      ReadScales<M>{x_scale}, WScale{nullptr, 0.0f}, y, acc, n,
+                      static_cast<int>(k), blockIdx.x, split, lut, red, gs, redf);
 }
 
 __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
@@ -396,21 +483,26 @@ struct QuantizeRow {
 
 // Fused product of one block: the row length picks the quantizer (rows up
 // to 2048 and 8192 values from registers, longer ones in two passes).
+template <bool kGrp = false>
 __device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, float* x_scale,
                                             bool write_scale, WScale ws, float* y,
                                             int32_t* acc, int64_t n, int k, int g, int S,
                                             const uint32_t* lut, int32_t* red, float* part,
-                                            int8_t* xq) {
+                                            int8_t* xq, const float* gs = nullptr,
+                                            float* redf = nullptr) {
   const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
   if (kp <= 4 * kGemvThreads) {
-    gemv_block<1>(w, XFromLds{xq}, QuantizeRow<1>{x, k, kp, xq, part, x_scale, write_scale},
-                  ws, y, acc, n, k, g, S, lut, red);
+    gemv_block<1, kGrp>(w, XFromLds{xq},
+                        QuantizeRow<1>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
+                        n, k, g, S, lut, red, gs, redf);
   } else if (kp <= 16 * kGemvThreads) {
-    gemv_block<1>(w, XFromLds{xq}, QuantizeRow<4>{x, k, kp, xq, part, x_scale, write_scale},
-                  ws, y, acc, n, k, g, S, lut, red);
+    gemv_block<1, kGrp>(w, XFromLds{xq},
+                        QuantizeRow<4>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
+                        n, k, g, S, lut, red, gs, redf);
   } else {
-    gemv_block<1>(w, XFromLds{xq}, QuantizeRow<0>{x, k, kp, xq, part, x_scale, write_scale},
-                  ws, y, acc, n, k, g, S, lut, red);
+    gemv_block<1, kGrp>(w, XFromLds{xq},
+                        QuantizeRow<0>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
+                        n, k, g, S, lut, red, gs, redf);
   }
 }
 
@@ -425,6 +517,20 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_kernel(
   fill_lut(lut);
   fused_block(w, x, x_scale, blockIdx.x == 0, ws, y, acc, n, static_cast<int>(k), blockIdx.x,
               split, lut, red, part, xq);
+}
+
+__global__ __launch_bounds__(kGemvThreads) void gemv_f32_group_kernel(
+    const uint8_t* __restrict__ w, const float* __restrict__ x, float* __restrict__ x_scale,
+    const float* __restrict__ gs, float* __restrict__ y, int32_t* __restrict__ acc, int64_t n,
+    int64_t k, int split) {
+  __shared__ uint32_t lut[32];
+  __shared__ int32_t red[kGemvWaves * 64];
+  __shared__ float redf[kGemvWaves * 64];
+  __shared__ float part[kGemvWaves];
+  __shared__ __attribute__((aligned(16))) int8_t xq[kFusedMaxK];
+  fill_lut(lut);
+  fused_block<true>(w, x, x_scale, blockIdx.x == 0, WScale{nullptr, 0.0f}, y, acc, n,
+                    static_cast<int>(k), blockIdx.x, split, lut, red, part, xq, gs, redf);
 }
 
 __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
@@ -473,6 +579,31 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale, WS
     case 4: return launch(gemv_kernel<4>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
     default: return SHERRY_E_SHAPE;
   }
+}
+
+int launch_gemv_group(const uint8_t* w, const int8_t* x, const float* x_scale, const float* gs,
+                      float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
+  const int64_t R = ceil_div(n, kTileRows);
+  const int C = static_cast<int>(ceil_div(k, kTileK));
+  const int S = (R * gemv_split(C) >= 4096) ? gemv_split(C) : kGemvWaves;
+  const dim3 grid(static_cast<unsigned>(ceil_div(R * S, kGemvWaves)));
+  const dim3 block(kGemvThreads);
+  switch (m) {
+    case 1: return launch(gemv_group_kernel<1>, grid, block, 0, s, w, x, x_scale, gs, y, acc, n, k, S);
+    case 2: return launch(gemv_group_kernel<2>, grid, block, 0, s, w, x, x_scale, gs, y, acc, n, k, S);
+    case 3: return launch(gemv_group_kernel<3>, grid, block, 0, s, w, x, x_scale, gs, y, acc, n, k, S);
+    case 4: return launch(gemv_group_kernel<4>, grid, block, 0, s, w, x, x_scale, gs, y, acc, n, k, S);
+    default: return SHERRY_E_SHAPE;
+  }
+}
+
+int launch_gemv_f32_group(const uint8_t* w, const float* x, float* x_scale, const float* gs,
+                          float* y, int32_t* acc, int64_t n, int64_t k, hipStream_t s) {
+  const int64_t R = ceil_div(n, kTileRows);
+  const int C = static_cast<int>(ceil_div(k, kTileK));
+  const int S = (R * gemv_split(C, kFusedTarget) >= 4096) ? gemv_split(C, kFusedTarget) : kGemvWaves;
+  return launch(gemv_f32_group_kernel, dim3(static_cast<unsigned>(ceil_div(R * S, kGemvWaves))),
+                dim3(kGemvThreads), 0, s, w, x, x_scale, gs, y, acc, n, k, S);
 }
 
 int launch_gemv_batched(const sherry_gemv_desc* descs, int count, int64_t total_blocks,

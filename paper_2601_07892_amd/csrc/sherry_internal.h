@@ -181,6 +181,14 @@ int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, WScale ws,
                     int32_t* acc, int64_t n, int64_t k, hipStream_t s);
 int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_t total_blocks,
                             hipStream_t s);
+// Per-group weight scales gs: fp32 [n][ceil(k/128)] (one per 128 weights of
+// a row).
+int launch_gemv_group(const uint8_t* w, const int8_t* x, const float* x_scale, const float* gs,
+                      float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);
+int launch_gemv_f32_group(const uint8_t* w, const float* x, float* x_scale, const float* gs,
+                          float* y, int32_t* acc, int64_t n, int64_t k, hipStream_t s);
+int launch_skinny_group(const uint8_t* w, const int8_t* x, const float* x_scale, const float* gs,
+                        float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);
 
 // MFMA tile configuration chosen for an m x n product: 0 skinny (32 x 256),
 // 1 small (128 x 128), 2 mid (128 x 256), 3 large (256 x 256).

@@ -56,6 +56,7 @@ struct SkProblem {
   int32_t* acc;
   int n, k, m;
   WScale ws;
+  const float* gs;  // per-group scales [n][ceil(k/128)] (grouped kernels only)
 };
 
 // Waits until at most N vector-memory loads of this wave are outstanding
@@ -205,7 +206,13 @@ __device__ __forceinline__ void sk_stage_barrier() {
 // unconditionally (past the end they read zeros or unused rows), so the
 // number of loads issued after the last DMA of any chunk is fixed and the
 // wait before that chunk's barrier is a constant vmcnt.
-template <int MT, int S, int NST>
+//
+// With GR the weights carry per-group scales p.gs (one per row and 128
+// weights, i.e. per unit): after each unit's MFMAs the int32 accumulators
+// are scaled into fp32 ones (unit order) and cleared; two scale loads per
+// unit ride with the weight loads.  (The int32 totals, when asked for, come
+// from a second, unscaled launch.)
+template <int MT, int S, int NST, bool GR = false>
 __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32_t* lut,
                                          int8_t* xs) {
   using G = SkCfg<MT, NST>;
@@ -219,10 +226,15 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   constexpr int PL = UPS >= G::SPT ? G::SPT - 1 : UPS - 1;  // position of the last
   // loads issued after chunk ch's last DMA when chunk ch is reached: steady
   // state, and chunks 1..D-1 (whose DMAs the prologue issued)
-  constexpr int NSTEADY = 2 * (UPS - 1 - PL) + (D - 1) * (2 * UPS + G::SPT);
-  constexpr int NPRO = (D - 1) * G::SPT + 2 * kSkRing;
+  constexpr int LPC = GR ? 4 : 2;  // vector loads per unit besides the DMA
+  constexpr int NSTEADY = LPC * (UPS - 1 - PL) + (D - 1) * (LPC * UPS + G::SPT);
+  constexpr int NPRO = (D - 1) * G::SPT + LPC * kSkRing;
   static_assert(G::SPT % PER == 0 && PER * (PL + 1) == G::SPT, "DMA spread");
-  static_assert(NPRO + 2 * (D - 1) * UPS < 64 && NSTEADY < 64, "vmcnt range");
+  // vmcnt holds at most 63: waiting for fewer outstanding loads than the
+  // count is always safe (the loads complete in order), only stricter
+  constexpr int NSTEADY_W = NSTEADY < 63 ? NSTEADY : 63;
+  constexpr int NPRO_W = NPRO < 63 ? NPRO : 63;
+  static_assert(!GR || MT == 1, "per-group scales use 32-token blocks");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -296,6 +308,30 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   for (int h = 0; h < 2; ++h)
 #pragma unroll
     for (int tb = 0; tb < MT; ++tb) c[h][tb] = v16i{};
+  // per-group: fp32 sums, and the scales of the ring's units for rows
+  // 32h + lane%32 (a resource over the tile's scale rows; rows past n read
+  // zero)
+  typedef float v16f __attribute__((ext_vector_type(16)));
+  v16f cf[2][GR ? MT : 1];
+  float gsr[kSkRing][2];
+  __amdgpu_buffer_rsrc_t grs;
+  if constexpr (GR) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int tb = 0; tb < MT; ++tb) cf[h][tb] = v16f{};
+    const int rows = (r < R) ? p.n - r * kTileRows : 0;
+    grs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(p.gs) + int64_t(r < R ? r : 0) * kTileRows * C, 0,
+        (rows < kTileRows ? rows : kTileRows) * C * 4, kBufferWord3);
+  }
+  auto load_scales = [&](float (&gq)[2], int unit) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      gq[h] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                            grs, 4 * ((32 * h + (lane & 31)) * C + u0 + unit),
+                                            0, 0));
+  };
 
 #pragma unroll
   for (int ch = 0; ch < D; ++ch)
@@ -306,9 +342,10 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
 #pragma unroll
   for (int u = 0; u < kSkRing; ++u) {
     sk_load_container(ring[u], rs, u, lane);
+    if constexpr (GR) load_scales(gsr[u], u);
     __builtin_amdgcn_sched_barrier(0);
   }
-  sk_wait_vm<NPRO>();
+  sk_wait_vm<NPRO_W>();
   sk_wait_lgkm();
   sk_stage_barrier();  // chunk 0 and the table are ready
   if (chl == 0) clear_tail();
@@ -327,13 +364,14 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
       const int ch = jj / UPS, pos = jj % UPS;
       if (pos == 0 && jj > 0) {
         if (ch >= D) {
-          sk_wait_vm<NSTEADY>();
+          sk_wait_vm<NSTEADY_W>();
         } else {
           // chunk ch < D: its DMA went out in the prologue
           if constexpr (D > 1) {
-            if (ch == 1) sk_wait_vm<NPRO + 2 * UPS < 64 ? NPRO + 2 * UPS : 63>();
+            if (ch == 1) sk_wait_vm<NPRO + LPC * UPS < 64 ? NPRO + LPC * UPS : 63>();
             if constexpr (D > 2)
-              if (ch == 2) sk_wait_vm<NPRO + 4 * UPS < 64 ? NPRO + 4 * UPS : 63>();
+              if (ch == 2)
+                sk_wait_vm<NPRO + 2 * LPC * UPS < 64 ? NPRO + 2 * LPC * UPS : 63>();
           }
         }
         sk_stage_barrier();
@@ -346,6 +384,20 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
       const int8_t* xrow = xlane + (ch % NST) * G::STAGE + 128 * ((wb >> 3) ^ (sw >> 3));
       sk_mfma<MT, NST>(wv, ring[(u + 1) % kSkRing], lut, xrow, lo, c);
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (GR) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int tb = 0; tb < MT; ++tb) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              cf[h][tb][e] = __builtin_fmaf(static_cast<float>(c[h][tb][e]), gsr[u][h],
+                                            cf[h][tb][e]);
+            c[h][tb] = v16i{};
+          }
+        load_scales(gsr[u], jj + kSkRing);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if (pos <= PL) {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
@@ -358,7 +410,26 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   }
   sk_wait_vm<0>();  // no DMA may land in the LDS after this point
 
-  if constexpr (S > 1) {
+  if constexpr (S > 1 && GR) {
+    // fp32 partial sums of the S splits, in split order
+    float* redf = reinterpret_cast<float*>(xs);
+    sk_lds_barrier();
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) redf[((wave * 2 + h) * 16 + e) * 64 + lane] = cf[h][0][e];
+    sk_lds_barrier();
+    if (sp == 0) {
+#pragma unroll
+      for (int q = 1; q < S; ++q)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            cf[h][0][e] += redf[(((wave + q) * 2 + h) * 16 + e) * 64 + lane];
+    }
+  }
+  if constexpr (S > 1 && !GR) {
     // partial sums of the S splits of a tile through LDS (the stages are
     // free now), one token block at a time: [wave][h][element][lane]
     int32_t* red = reinterpret_cast<int32_t*>(xs);
@@ -398,9 +469,15 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
         const int tok = 32 * tb + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if (tok >= p.m) continue;
         const int32_t v = c[h][tb][e];
-        const float s = as_global(p.x_scale)[tok] * p.ws.at(row);
-        as_global_mut(p.y)[int64_t(tok) * p.n + row] = static_cast<float>(v) * s;
-        if (p.acc) as_global_mut(p.acc)[int64_t(tok) * p.n + row] = v;
+        if constexpr (GR) {
+          as_global_mut(p.y)[int64_t(tok) * p.n + row] =
+              cf[h][0][e] * as_global(p.x_scale)[tok];
+        } else {
+          const float s = as_global(p.x_scale)[tok] * p.ws.at(row);
+          as_global_mut(p.y)[int64_t(tok) * p.n + row] = static_cast<float>(v) * s;
+        }
+        if constexpr (!GR)
+          if (p.acc) as_global_mut(p.acc)[int64_t(tok) * p.n + row] = v;
       }
     }
   }
@@ -412,7 +489,7 @@ template <int MT>
 constexpr int kSkStages = 4;
 
 // grid: x = groups of 8/S tiles, y = blocks of 32*MT tokens
-template <int MT, int S>
+template <int MT, int S, bool GR = false>
 __global__ __launch_bounds__(kSkThreads) void skinny_kernel(SkProblem p) {
   constexpr int NST = kSkStages<MT>;
   __shared__ __attribute__((aligned(16))) int8_t lds[SkCfg<MT, NST>::LDS];
@@ -424,7 +501,7 @@ __global__ __launch_bounds__(kSkThreads) void skinny_kernel(SkProblem p) {
   p.y += int64_t(t0) * p.n;
   if (p.acc) p.acc += int64_t(t0) * p.n;
   p.m = (p.m - t0 < SkCfg<MT, NST>::TOK) ? p.m - t0 : SkCfg<MT, NST>::TOK;
-  sk_block<MT, S, NST>(p, blockIdx.x, lut, lds + kSkLutBytes);
+  sk_block<MT, S, NST, GR>(p, blockIdx.x, lut, lds + kSkLutBytes);
 }
 
 template <int MT>
@@ -449,7 +526,8 @@ __global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
   }
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
-  const SkProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m, WScale{d.w_scales, d.w_scale}};
+  const SkProblem p{d.w,   d.x,   d.x_scale, d.y, d.acc, d.n, d.k, d.m,
+                    WScale{d.w_scales, d.w_scale}, nullptr};
   sk_block<MT, 1, NST>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
 }
 
@@ -465,7 +543,7 @@ constexpr int64_t kSkMinBlocks = 192;
 // Token blocks beyond the grid's y limit go to further launches.
 constexpr int64_t kSkMaxGridY = 32768;
 
-template <int MT, int S>
+template <int MT, int S, bool GR>
 int launch_skinny_s(const SkProblem& p, hipStream_t s) {
   const int64_t R = ceil_div(p.n, kTileRows);
   const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT>>::TOK);
@@ -479,39 +557,57 @@ int launch_skinny_s(const SkProblem& p, hipStream_t s) {
     if (q.acc) q.acc += t0 * p.n;
     q.m = static_cast<int>(p.m - t0);
     const dim3 grid(static_cast<unsigned>(ceil_div(R, kSkWaves / S)), static_cast<unsigned>(nb));
-    const int rc = launch(skinny_kernel<MT, S>, grid, dim3(kSkThreads), 0, s, q);
+    const int rc = launch(skinny_kernel<MT, S, GR>, grid, dim3(kSkThreads), 0, s, q);
     if (rc != SHERRY_OK) return rc;
   }
   return SHERRY_OK;
 }
 
-template <int MT>
+template <int MT, bool GR = false>
 int launch_skinny_mt(const SkProblem& p, hipStream_t s) {
   const int64_t R = ceil_div(p.n, kTileRows);
   const int64_t C = ceil_div(p.k, kTileK);
   const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT>>::TOK);
-  int S = 1;
+  // the per-group kernel always splits K at least in two (fewer units per
+  // wave keep its registers in bounds)
+  int S = GR ? 2 : 1;
   while (S < SkCfg<MT, kSkStages<MT>>::UPC && S < kSkWaves && ceil_div(R, kSkWaves / S) * TB < kSkMinBlocks &&
          C >= 2 * S)
     S *= 2;
   switch (S) {
-    case 1: return launch_skinny_s<MT, 1>(p, s);
-    case 2: return launch_skinny_s<MT, 2>(p, s);
+    case 1:
+      if constexpr (!GR) return launch_skinny_s<MT, 1, GR>(p, s);
+      return launch_skinny_s<MT, 2, GR>(p, s);
+    case 2: return launch_skinny_s<MT, 2, GR>(p, s);
     case 4:
-      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 4) return launch_skinny_s<MT, 4>(p, s);
-      return launch_skinny_s<MT, 2>(p, s);
+      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 4) return launch_skinny_s<MT, 4, GR>(p, s);
+      return launch_skinny_s<MT, 2, GR>(p, s);
     default:
-      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 8) return launch_skinny_s<MT, 8>(p, s);
-      return launch_skinny_s<MT, 2>(p, s);
+      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 8) return launch_skinny_s<MT, 8, GR>(p, s);
+      return launch_skinny_s<MT, 2, GR>(p, s);
   }
 }
 
 int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                   float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
   const SkProblem p{w, x, x_scale, y, acc, static_cast<int>(n), static_cast<int>(k),
-                    static_cast<int>(m), ws};
+                    static_cast<int>(m), ws, nullptr};
   if (m <= 32) return launch_skinny_mt<1>(p, s);
   return launch_skinny_mt<2>(p, s);
+}
+
+// Per-group scales: 32-token blocks for every M (the fp32 sums and int32
+// totals double the accumulator registers).
+int launch_skinny_group(const uint8_t* w, const int8_t* x, const float* x_scale, const float* gs,
+                        float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
+  if (acc) {
+    // int32 totals from an unscaled launch (its y is overwritten below)
+    const int rc = launch_skinny(w, x, x_scale, WScale{nullptr, 1.0f}, y, acc, m, n, k, s);
+    if (rc != SHERRY_OK) return rc;
+  }
+  const SkProblem p{w, x, x_scale, y, nullptr, static_cast<int>(n), static_cast<int>(k),
+                    static_cast<int>(m), WScale{nullptr, 0.0f}, gs};
+  return launch_skinny_mt<1, true>(p, s);
 }
 
 int launch_skinny_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,

@@ -290,3 +290,18 @@ def test_channel_and_ternarize_validation_without_launch():
     assert t(FAKE, 70, 132, FAKE, need - 1, None, None) == sh.SHERRY_E_BUFSIZE
     assert t(FAKE + 4, 70, 132, FAKE, need, None, None) == sh.SHERRY_E_ALIGN
     assert t(FAKE, 70, 132, FAKE, need, FAKE + 2, None) == sh.SHERRY_E_ALIGN
+
+
+def test_group_validation_without_launch():
+    g = L.sherry_gemm_group
+    assert g(FAKE, FAKE, FAKE, None, FAKE, None, 1, 64, 128, sh.SHERRY_KERNEL_AUTO,
+             None) == sh.SHERRY_E_INVALID
+    assert g(FAKE, FAKE, FAKE, FAKE + 2, FAKE, None, 1, 64, 128, sh.SHERRY_KERNEL_AUTO,
+             None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 16, 64, 128, sh.SHERRY_KERNEL_MFMA,
+             None) == sh.SHERRY_E_INVALID
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 5, 64, 128, sh.SHERRY_KERNEL_GEMV,
+             None) == sh.SHERRY_E_SHAPE
+    f = L.sherry_gemv_f32_group
+    assert f(FAKE, FAKE, FAKE, None, FAKE, None, 64, 128, None) == sh.SHERRY_E_INVALID
+    assert f(FAKE, FAKE, FAKE, FAKE + 1, FAKE, None, 64, 128, None) == sh.SHERRY_E_ALIGN

@@ -836,3 +836,81 @@ def test_ternarize_pack_then_channel_product(dev):
     acc_ref = oracle.gemm_i32(q, t_ref, threads=8)
     assert np.array_equal(acc.cpu().numpy(), acc_ref)
     assert _y_ok(y.cpu().numpy(), oracle.epilogue_rows(acc_ref, sx, alpha.cpu().numpy()))
+
+
+# ------------------------------------ per-group scales (group 128 along K)
+
+def _group_scales(n, k, seed):
+    rng = np.random.default_rng(seed)
+    return (rng.random((n, (k + 127) // 128)) * 0.05 + 0.001).astype(np.float32)
+
+
+def _group_ok(y, y_ref, mag, k):
+    # fp32 summation in any order: |y - y_ref| <= (G + 4) * 2^-24 * mag
+    bound = ((k + 127) // 128 + 4) * 2.0 ** -24 * mag + 1e-30
+    return bool(np.all(np.abs(np.asarray(y, np.float64) - y_ref) <= bound))
+
+
+# GEMV (m <= 4) and the register-decoded kernel (32-token blocks, K split in
+# 2, 4 or 8) with ragged n, a partial last group, and the int32 totals
+GROUP_CASES = [(1, 70, 132, "GEMV"), (4, 600, 2048, "GEMV"), (3, 300, 8196, "GEMV"),
+               (5, 64, 128, "SKINNY"), (33, 130, 1028, "SKINNY"), (100, 257, 3076, "SKINNY"),
+               (17, 3072, 8192, "SKINNY")]
+
+
+@pytest.mark.parametrize("m,n,k,kernel", GROUP_CASES)
+def test_gemm_group_parity(dev, m, n, k, kernel):
+    sh = _sh()
+    _say("group", kernel, m, n, k)
+    t = synth.ternary_34(n, k, 71, "gr", n, k)
+    q = synth.int8_any(m, k, 71, "grq", m, k)
+    sx = np.abs(synth.activations(1, m, 71, "grs", m)[0]).astype(np.float32) + 0.01
+    gs = _group_scales(n, k, 71)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+    acc = torch.full((m, n), -7, dtype=torch.int32, device=dev)
+    sh.sherry_gemm_group(w, torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev),
+                         torch.from_numpy(gs).to(dev), y, acc, m, n, k,
+                         getattr(sh, "SHERRY_KERNEL_" + kernel))
+    torch.cuda.synchronize()
+    y_ref, mag, acc_ref = oracle.product_groups(q, t, sx, gs, threads=8)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref)
+    assert _group_ok(y.cpu().numpy(), y_ref, mag, k)
+
+
+def test_gemm_group_without_acc(dev):
+    sh = _sh()
+    m, n, k = 40, 200, 1024
+    _say("group no acc", m, n, k)
+    t = synth.ternary_34(n, k, 72, "gra")
+    q = synth.int8_any(m, k, 72, "graq")
+    sx = np.full(m, 0.02, np.float32)
+    gs = _group_scales(n, k, 72)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+    sh.sherry_gemm_group(w, torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev),
+                         torch.from_numpy(gs).to(dev), y, None, m, n, k)
+    torch.cuda.synchronize()
+    y_ref, mag, _ = oracle.product_groups(q, t, sx, gs, threads=8)
+    assert _group_ok(y.cpu().numpy(), y_ref, mag, k)
+
+
+@pytest.mark.parametrize("n,k", [(70, 132), (2048, 8192)])
+def test_gemv_f32_group_parity(dev, n, k):
+    sh = _sh()
+    _say("f32 group", n, k)
+    t = synth.ternary_34(n, k, 73, "fgr", n, k)
+    x = synth.activations(1, k, 73, "fgrx", n, k, outlier_frac=0.01)
+    gs = _group_scales(n, k, 73)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    xs = torch.empty(1, dtype=torch.float32, device=dev)
+    y = torch.full((1, n), float("nan"), dtype=torch.float32, device=dev)
+    acc = torch.full((1, n), -7, dtype=torch.int32, device=dev)
+    sh.sherry_gemv_f32_group(w, torch.from_numpy(x[0]).to(dev), xs, torch.from_numpy(gs).to(dev),
+                             y, acc, n, k)
+    torch.cuda.synchronize()
+    q, sx = oracle.quantize_act(x)
+    assert np.array_equal(xs.cpu().numpy(), sx)
+    y_ref, mag, acc_ref = oracle.product_groups(q, t, sx, gs, threads=8)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref)
+    assert _group_ok(y.cpu().numpy(), y_ref, mag, k)
