@@ -456,6 +456,52 @@ def bench_shapes(sh, torch, dev, spec, seed, ms, shapes=("q", "gate", "down"), r
     return rows
 
 
+def bench_scale_granularity(sh, torch, dev, spec, seed, ms=(1, 16), shapes=("q", "gate", "down"),
+                            reps=3):
+    """The same products with one weight scale, one per output channel and
+    one per 128-weight group (M = 1 on the VALU kernel, M = 16 on the
+    register-decoded one), each timed over rotated weight copies from a
+    captured graph.  Bytes count the scale vectors (4N, 4N*K/128)."""
+    blk = {lin.name: lin for lin in synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])}
+    rows = []
+    for name in shapes:
+        lin = blk[name]
+        n, k = lin.n, lin.k
+        t = synth.ternary_34(n, k, seed, "gsk", name)
+        packed = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        nb = packed.numel()
+        ws = [packed.clone() for _ in range(_rotation(nb))]
+        g = (k + 127) // 128
+        rng = np.random.default_rng([seed, n, k])
+        sw_rows = torch.from_numpy((rng.random(n) * 0.04 + 0.01).astype(np.float32)).to(dev)
+        sw_groups = torch.from_numpy((rng.random((n, g)) * 0.04 + 0.01).astype(np.float32)).to(dev)
+        for m in ms:
+            q = torch.from_numpy(synth.int8_any(m, k, seed, "gskx", name, m)).to(dev)
+            sx = torch.full((m,), 0.01, dtype=torch.float32, device=dev)
+            y = torch.empty((m, n), dtype=torch.float32, device=dev)
+            kern = sh.SHERRY_KERNEL_GEMV if m <= 4 else sh.SHERRY_KERNEL_SKINNY
+            base = nb + m * k + 4 * m + 4 * m * n
+            runs = {
+                "tensor": (lambda i: sh.sherry_gemm_ex(ws[i % len(ws)], q, sx, 0.02, y, None,
+                                                       m, n, k, kern), base),
+                "channel": (lambda i: sh.sherry_gemm_channel(ws[i % len(ws)], q, sx, sw_rows, y,
+                                                             None, m, n, k, kern), base + 4 * n),
+                "group128": (lambda i: sh.sherry_gemm_group(ws[i % len(ws)], q, sx, sw_groups, y,
+                                                            None, m, n, k, kern),
+                             base + 4 * n * g),
+            }
+            row = {"proj": name, "n": n, "k": k, "m": m, "kernel": KERNEL_NAMES[kern]}
+            for key, (run, byts) in runs.items():
+                us = time_graph(run, reps * len(ws), torch)
+                row[key + "_us"] = round(us, 3)
+                row[key + "_gbs"] = round(byts / (us * 1e-6) / 1e9, 1)
+            rows.append(row)
+            del q, sx, y
+        del ws, packed
+        torch.cuda.empty_cache()
+    return rows
+
+
 def bench_two_bit(sh, torch, dev, spec, seed, shapes=("q", "gate", "down"), reps=3):
     """The same ternary weights as 1.25-bit codes and as the 2-bit reference
     layout, M = 1, each timed over rotated copies (launched from a captured
@@ -641,6 +687,11 @@ def main():
             "gbs": round(ch_bytes / (ms_ch * 1e-3) / 1e9, 1),
             "time_vs_per_tensor": round(ms_ch / ms_step, 4)}
         log("decode step, per-channel scales: %.2f us" % (ms_ch * 1e3))
+        out["scale_granularity_3b"] = bench_scale_granularity(sh, torch, dev, synth.LLAMA_3B,
+                                                              args.seed)
+        for r in out["scale_granularity_3b"]:
+            log("3b %s M=%d: tensor %.2f us, channel %.2f us, group-128 %.2f us" %
+                (r["proj"], r["m"], r["tensor_us"], r["channel_us"], r["group128_us"]))
         out["ternarize_pack"] = bench_ternarize(sh, torch, dev, args.seed)
         for r in out["ternarize_pack"]:
             log("ternarize+pack %s: %.1f us, %.0f GB/s" % (r["shape"], r["us"], r["gbs"]))
