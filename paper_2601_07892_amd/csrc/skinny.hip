@@ -3,11 +3,12 @@
 // int8 MFMA.  Its first use is small M (a few to 128 tokens), where the
 // weights dominate the traffic; larger M runs as a grid of 128-token blocks.
 //
-// Work mapping.  A workgroup is 8 waves; wave w owns 64-row tile 8g + w/S and
-// part w%S of its containers along K (S = 1 unless a lone launch has too few
-// tiles to fill the GPU).  The waves walk K in lockstep chunks; the
-// activations of a chunk (every staged token) arrive in LDS by DMA loads,
-// several chunks ahead of their use.
+// Work mapping.  A workgroup is W = 8 waves; wave w owns 64-row tile
+// (W/S)g + w/S and part w%S of its containers along K (S = 1 unless a lone
+// launch has too few tiles to fill the GPU).
+// The waves walk K in lockstep chunks; the activations of a chunk (every
+// staged token) arrive in LDS by DMA loads, one or three chunks ahead of
+// their use.
 //
 // Per container (64 rows x 128 weights) a wave decodes its 32 codes per lane
 // through the 32-entry table (lane i = row i), exactly as the decode kernel
@@ -25,25 +26,27 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kSkWaves = 8;
-constexpr int kSkThreads = 64 * kSkWaves;
+// Waves per workgroup (lone and grouped launches; kept apart so that each
+// can be tuned on its own).
+constexpr int kSkWavesLone = 8;
+constexpr int kSkWavesGrouped = 8;
 constexpr int kSkRing = 4;        // containers per wave in the register ring
 constexpr int kSkLutBytes = 128;  // the code table, at LDS address 0
 constexpr int kSkOutside = 0x7FFFFFF0;  // a buffer offset past any range: loads read zero
-// Staging geometry for MT blocks of 32 tokens: a stage holds every staged
-// token's KC = 1024/MT activations (32 KB), filled by LDS-DMA loads of 1 KB
-// per wave instruction; NST stages form a ring, so the loads for chunk ch + NST
-// - 1 are in flight while chunk ch is multiplied.
-template <int MT, int NST>
+// Staging geometry for MT blocks of 32 tokens and W waves: a stage holds
+// every staged token's KC = 1024/MT activations (32 KB), filled by LDS-DMA
+// loads of 1 KB per wave instruction; NST stages form a ring, so the loads for
+// chunk ch + NST - 1 are in flight while chunk ch is multiplied.
+template <int MT, int NST, int W>
 struct SkCfg {
   static constexpr int TOK = 32 * MT;        // staged token rows
   static constexpr int KC = 1024 / MT;       // K values per chunk (row bytes in a stage)
   static constexpr int CPR = KC / 16;        // 16-byte pieces per row
   static constexpr int UPC = KC / kTileK;    // containers per chunk
   static constexpr int STAGE = TOK * KC;
-  static constexpr int SPT = STAGE / 1024 / kSkWaves;  // DMA instructions per wave per chunk
+  static constexpr int SPT = STAGE / 1024 / W;  // DMA instructions per wave per chunk
   static constexpr int LDS = kSkLutBytes + NST * STAGE;
-  static_assert(SPT * 1024 * kSkWaves == STAGE && CPR >= 16, "stage split");
+  static_assert(SPT * 1024 * W == STAGE && CPR >= 16, "stage split");
   static_assert(NST >= 2 && LDS <= 160 * 1024, "stages fit the LDS");
 };
 
@@ -150,7 +153,7 @@ template <int MT, int NST>
 __device__ __forceinline__ void sk_mfma(uint32_t (&wv)[32], const uint32_t (&dn)[5],
                                         const uint32_t* lut, const int8_t* xrow,
                                         const int (&lo)[4], v16i (&c)[2][MT]) {
-  using G = SkCfg<MT, NST>;
+  using G = SkCfg<MT, NST, kSkWavesLone>;  // KC only
   v4i xv[4][MT];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
@@ -212,12 +215,12 @@ __device__ __forceinline__ void sk_stage_barrier() {
 // are scaled into fp32 ones (unit order) and cleared; two scale loads per
 // unit ride with the weight loads.  (The int32 totals, when asked for, come
 // from a second, unscaled launch.)
-template <int MT, int S, int NST, bool GR = false>
+template <int MT, int S, int NST, int W, bool GR = false>
 __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32_t* lut,
                                          int8_t* xs) {
-  using G = SkCfg<MT, NST>;
+  using G = SkCfg<MT, NST, W>;
   static_assert(S >= 1 && G::UPC % S == 0, "splits divide a chunk");
-  constexpr int T = kSkWaves / S;    // tiles per workgroup
+  constexpr int T = W / S;           // tiles per workgroup
   constexpr int UPS = G::UPC / S;    // units per split per chunk
   constexpr int WIN = UPS * kTileK;  // K values per split window
   constexpr int D = NST - 1;         // chunks between a DMA and its use
@@ -262,7 +265,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   int dvo[G::SPT], lim[G::SPT];
 #pragma unroll
   for (int i = 0; i < G::SPT; ++i) {
-    const int q = 64 * (i * kSkWaves + wave) + lane;
+    const int q = 64 * (i * W + wave) + lane;
     const int t = q / G::CPR;
     const int o = 16 * ((q % G::CPR) ^ (t & 15));
     const int ws = o / WIN;
@@ -273,7 +276,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   }
   int8_t* const xw = xs + 1024 * wave;  // + stage + 8 KB per instruction
   auto dma = [&](int ch, int i, int voff, int left) {
-    sk_dma(rx, xw + (ch % NST) * G::STAGE + i * 1024 * kSkWaves,
+    sk_dma(rx, xw + (ch % NST) * G::STAGE + i * 1024 * W,
            ch * WIN < left ? voff + ch * WIN : kSkOutside);
   };
 
@@ -295,7 +298,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
     const int o = sl * WIN + (jl % UPS) * kTileK + ((p.k & ~15) - (C - 1) * kTileK);
     const int nd = (16 - kr) / 4;  // dwords to clear per token row
     int8_t* st = xs + (chl % NST) * G::STAGE;
-    for (int e = tid; e < G::TOK * nd; e += kSkThreads) {
+    for (int e = tid; e < G::TOK * nd; e += 64 * W) {
       const int t = e / nd, b = kr + 4 * (e % nd);
       *reinterpret_cast<uint32_t*>(st + t * G::KC + 16 * ((o / 16) ^ (t & 15)) + b) = 0;
     }
@@ -433,7 +436,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
     // partial sums of the S splits of a tile through LDS (the stages are
     // free now), one token block at a time: [wave][h][element][lane]
     int32_t* red = reinterpret_cast<int32_t*>(xs);
-    static_assert(kSkWaves * 2 * 16 * 64 * 4 <= NST * G::STAGE, "reduction fits the stages");
+    static_assert(W * 2 * 16 * 64 * 4 <= NST * G::STAGE, "reduction fits the stages");
 #pragma unroll
     for (int tb = 0; tb < MT; ++tb) {
       sk_lds_barrier();
@@ -483,32 +486,35 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   }
 }
 
-// Stages per token-block count (one workgroup per CU either way: the
-// registers of the pipelined loop exceed 128 per lane).
-template <int MT>
-constexpr int kSkStages = 4;
+// Stage ring depth: two stages (one chunk ahead) for lone 32-token launches,
+// four otherwise (measured).
+template <int MT, bool kGrouped>
+constexpr int kSkStages = (MT == 1 && !kGrouped) ? 2 : 4;
 
-// grid: x = groups of 8/S tiles, y = blocks of 32*MT tokens
+// grid: x = groups of W/S tiles, y = blocks of 32*MT tokens
 template <int MT, int S, bool GR = false>
-__global__ __launch_bounds__(kSkThreads) void skinny_kernel(SkProblem p) {
-  constexpr int NST = kSkStages<MT>;
-  __shared__ __attribute__((aligned(16))) int8_t lds[SkCfg<MT, NST>::LDS];
+__global__ __launch_bounds__(64 * kSkWavesLone) void skinny_kernel(SkProblem p) {
+  constexpr int W = kSkWavesLone;
+  constexpr int NST = kSkStages<MT, false>;
+  using G = SkCfg<MT, NST, W>;
+  __shared__ __attribute__((aligned(16))) int8_t lds[G::LDS];
   uint32_t* lut = reinterpret_cast<uint32_t*>(lds);
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
-  const int t0 = blockIdx.y * SkCfg<MT, NST>::TOK;
+  const int t0 = blockIdx.y * G::TOK;
   p.x += int64_t(t0) * p.k;
   p.x_scale += t0;
   p.y += int64_t(t0) * p.n;
   if (p.acc) p.acc += int64_t(t0) * p.n;
-  p.m = (p.m - t0 < SkCfg<MT, NST>::TOK) ? p.m - t0 : SkCfg<MT, NST>::TOK;
-  sk_block<MT, S, NST, GR>(p, blockIdx.x, lut, lds + kSkLutBytes);
+  p.m = (p.m - t0 < G::TOK) ? p.m - t0 : G::TOK;
+  sk_block<MT, S, NST, W, GR>(p, blockIdx.x, lut, lds + kSkLutBytes);
 }
 
 template <int MT>
-__global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
+__global__ __launch_bounds__(64 * kSkWavesGrouped) void skinny_batched_kernel(
     const sherry_gemm_desc* __restrict__ descs, int count) {
-  constexpr int NST = kSkStages<MT>;
-  __shared__ __attribute__((aligned(16))) int8_t lds[SkCfg<MT, NST>::LDS];
+  constexpr int W = kSkWavesGrouped;
+  constexpr int NST = kSkStages<MT, true>;
+  __shared__ __attribute__((aligned(16))) int8_t lds[SkCfg<MT, NST, W>::LDS];
   uint32_t* lut = reinterpret_cast<uint32_t*>(lds);
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
@@ -528,12 +534,15 @@ __global__ __launch_bounds__(kSkThreads) void skinny_batched_kernel(
   const sherry_gemm_desc& d = descs[lo];
   const SkProblem p{d.w,   d.x,   d.x_scale, d.y, d.acc, d.n, d.k, d.m,
                     WScale{d.w_scales, d.w_scale}, nullptr};
-  sk_block<MT, 1, NST>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
+  sk_block<MT, 1, NST, W>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
 }
 
 }  // namespace
 
-int skinny_blocks(int64_t n) { return static_cast<int>(ceil_div(ceil_div(n, kTileRows), kSkWaves)); }
+// Workgroups of one product in a grouped launch.
+int skinny_blocks(int64_t n) {
+  return static_cast<int>(ceil_div(ceil_div(n, kTileRows), kSkWavesGrouped));
+}
 
 // K splits per tile of a lone launch: the smallest power of two (up to a
 // chunk's units) that gives the launch at least kSkMinBlocks workgroups, so
@@ -546,18 +555,19 @@ constexpr int64_t kSkMaxGridY = 32768;
 template <int MT, int S, bool GR>
 int launch_skinny_s(const SkProblem& p, hipStream_t s) {
   const int64_t R = ceil_div(p.n, kTileRows);
-  const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT>>::TOK);
+  const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT, false>, kSkWavesLone>::TOK);
   for (int64_t b0 = 0; b0 < TB; b0 += kSkMaxGridY) {
     const int64_t nb = TB - b0 < kSkMaxGridY ? TB - b0 : kSkMaxGridY;
-    const int64_t t0 = b0 * SkCfg<MT, kSkStages<MT>>::TOK;
+    const int64_t t0 = b0 * SkCfg<MT, kSkStages<MT, false>, kSkWavesLone>::TOK;
     SkProblem q = p;
     q.x += t0 * p.k;
     q.x_scale += t0;
     q.y += t0 * p.n;
     if (q.acc) q.acc += t0 * p.n;
     q.m = static_cast<int>(p.m - t0);
-    const dim3 grid(static_cast<unsigned>(ceil_div(R, kSkWaves / S)), static_cast<unsigned>(nb));
-    const int rc = launch(skinny_kernel<MT, S, GR>, grid, dim3(kSkThreads), 0, s, q);
+    const dim3 grid(static_cast<unsigned>(ceil_div(R, kSkWavesLone / S)),
+                    static_cast<unsigned>(nb));
+    const int rc = launch(skinny_kernel<MT, S, GR>, grid, dim3(64 * kSkWavesLone), 0, s, q);
     if (rc != SHERRY_OK) return rc;
   }
   return SHERRY_OK;
@@ -567,11 +577,12 @@ template <int MT, bool GR = false>
 int launch_skinny_mt(const SkProblem& p, hipStream_t s) {
   const int64_t R = ceil_div(p.n, kTileRows);
   const int64_t C = ceil_div(p.k, kTileK);
-  const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT>>::TOK);
+  const int64_t TB = ceil_div(p.m, SkCfg<MT, kSkStages<MT, false>, kSkWavesLone>::TOK);
   // the per-group kernel always splits K at least in two (fewer units per
   // wave keep its registers in bounds)
   int S = GR ? 2 : 1;
-  while (S < SkCfg<MT, kSkStages<MT>>::UPC && S < kSkWaves && ceil_div(R, kSkWaves / S) * TB < kSkMinBlocks &&
+  while (S < SkCfg<MT, kSkStages<MT, false>, kSkWavesLone>::UPC && S < kSkWavesLone &&
+         ceil_div(R, kSkWavesLone / S) * TB < kSkMinBlocks &&
          C >= 2 * S)
     S *= 2;
   switch (S) {
@@ -580,10 +591,10 @@ int launch_skinny_mt(const SkProblem& p, hipStream_t s) {
       return launch_skinny_s<MT, 2, GR>(p, s);
     case 2: return launch_skinny_s<MT, 2, GR>(p, s);
     case 4:
-      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 4) return launch_skinny_s<MT, 4, GR>(p, s);
+      if constexpr (SkCfg<MT, kSkStages<MT, false>, kSkWavesLone>::UPC >= 4) return launch_skinny_s<MT, 4, GR>(p, s);
       return launch_skinny_s<MT, 2, GR>(p, s);
     default:
-      if constexpr (SkCfg<MT, kSkStages<MT>>::UPC >= 8) return launch_skinny_s<MT, 8, GR>(p, s);
+      if constexpr (SkCfg<MT, kSkStages<MT, false>, kSkWavesLone>::UPC >= 8) return launch_skinny_s<MT, 8, GR>(p, s);
       return launch_skinny_s<MT, 2, GR>(p, s);
   }
 }
@@ -612,7 +623,7 @@ int launch_skinny_group(const uint8_t* w, const int8_t* x, const float* x_scale,
 
 int launch_skinny_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
                           int max_m, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(total_blocks)), block(kSkThreads);
+  const dim3 grid(static_cast<unsigned>(total_blocks)), block(64 * kSkWavesGrouped);
   if (max_m <= 32) return launch(skinny_batched_kernel<1>, grid, block, 0, s, descs, count);
   return launch(skinny_batched_kernel<2>, grid, block, 0, s, descs, count);
 }
