@@ -212,6 +212,9 @@ typedef struct sherry_gemv_desc {
   int32_t* acc;          /* device, int32 [n] or NULL                      */
   const float* w_scales; /* device, fp32 [n] per-channel scales, or NULL   */
                          /* for the per-tensor w_scale                     */
+  const float* w_group_scales; /* device, fp32 [n][ceil(k/128)] per-group  */
+                         /* scales (as sherry_gemm_group), or NULL; at     */
+                         /* most one of w_scales and w_group_scales is set */
   int32_t n, k;
   float w_scale;
   int32_t block_begin;   /* written by sherry_gemv_batched_prepare         */
@@ -297,6 +300,8 @@ typedef struct sherry_gemv_f32_desc {
   float* y;              /* device, fp32 [n]                               */
   int32_t* acc;          /* device, int32 [n] or NULL                      */
   const float* w_scales; /* device, fp32 [n] per-channel scales, or NULL   */
+  const float* w_group_scales; /* per-group scales or NULL, as in          */
+                         /* sherry_gemv_desc                               */
   int32_t n, k;          /* k <= SHERRY_FUSED_MAX_K                        */
   float w_scale;
   int32_t block_begin;   /* written by sherry_gemv_f32_batched_prepare     */

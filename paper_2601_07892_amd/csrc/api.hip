@@ -91,8 +91,8 @@ extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
 }
 
 // The descriptor layouts are part of the ABI (Python and C callers build them).
-static_assert(sizeof(sherry_gemv_desc) == 64, "sherry_gemv_desc layout");
-static_assert(sizeof(sherry_gemv_f32_desc) == 64, "sherry_gemv_f32_desc layout");
+static_assert(sizeof(sherry_gemv_desc) == 72, "sherry_gemv_desc layout");
+static_assert(sizeof(sherry_gemv_f32_desc) == 72, "sherry_gemv_f32_desc layout");
 static_assert(sizeof(sherry_gemm_desc) == 72, "sherry_gemm_desc layout");
 
 namespace {
@@ -191,7 +191,9 @@ extern "C" int sherry_gemv_batched_prepare(sherry_gemv_desc* descs, int count,
     sherry_gemv_desc& d = descs[i];
     int st = check_product(d.w, d.x, d.x_scale, d.y, 1, d.n, d.k, 4);
     if (st != SHERRY_OK) return st;
-    if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)))
+    if (d.w_scales && d.w_group_scales) return SHERRY_E_INVALID;
+    if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)) ||
+        (d.w_group_scales && !aligned(d.w_group_scales, 4)))
       return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
     blocks += gemv_blocks(d.n, d.k, kGemvTarget);
@@ -264,7 +266,10 @@ extern "C" int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int 
     sherry_gemv_f32_desc& d = descs[i];
     int st = check_fused(d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k);
     if (st != SHERRY_OK) return st;
-    if (d.w_scales && !aligned(d.w_scales, 4)) return SHERRY_E_ALIGN;
+    if (d.w_scales && d.w_group_scales) return SHERRY_E_INVALID;
+    if ((d.w_scales && !aligned(d.w_scales, 4)) ||
+        (d.w_group_scales && !aligned(d.w_group_scales, 4)))
+      return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
     blocks += gemv_blocks(d.n, d.k, kFusedTarget);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;

@@ -372,6 +372,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
     const sherry_gemv_desc* __restrict__ descs, int count) {
   __shared__ uint32_t lut[32];
   __shared__ int32_t red[kGemvWaves * 64];
+  __shared__ float redf[kGemvWaves * 64];
   fill_lut(lut);
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
   // last descriptor with block_begin <= blk: block_begin strictly increases,
@@ -392,10 +393,14 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
   const sherry_gemv_desc& d = descs[lo];
   const int k = static_cast<int>(d.k);
   const int S = gemv_split(static_cast<int>((k + kTileK - 1) / kTileK));
-  gemv_block<1>(d.w, XFromSgpr<1>{as_const(reinterpret_cast<const int32_t*>(d.x)), k},
-                ReadScales<1>{d.x_scale}, WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k,
-                blk - d.block_begin, S,
-                lut, red);
+  const XFromSgpr<1> xs{as_const(reinterpret_cast<const int32_t*>(d.x)), k};
+  if (d.w_group_scales) {
+    gemv_block<1, true>(d.w, xs, ReadScales<1>{d.x_scale}, WScale{nullptr, 0.0f}, d.y, d.acc,
+                        d.n, k, blk - d.block_begin, S, lut, red, d.w_group_scales, redf);
+  } else {
+    gemv_block<1>(d.w, xs, ReadScales<1>{d.x_scale}, WScale{d.w_scales, d.w_scale}, d.y, d.acc,
+                  d.n, k, blk - d.block_begin, S, lut, red);
+  }
 }
 
 // ---- fused per-token quantization + product (M = 1) ----
@@ -537,6 +542,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
     const sherry_gemv_f32_desc* __restrict__ descs, int count) {
   __shared__ uint32_t lut[32];
   __shared__ int32_t red[kGemvWaves * 64];
+  __shared__ float redf[kGemvWaves * 64];
   __shared__ float part[kGemvWaves];
   __shared__ __attribute__((aligned(16))) int8_t xq[kFusedMaxK];
   fill_lut(lut);
@@ -556,9 +562,14 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
   const int k = static_cast<int>(d.k);
   const int C = (k + kTileK - 1) / kTileK;
   const int S = gemv_split(C, kFusedTarget);
-  fused_block(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{d.w_scales, d.w_scale}, d.y, d.acc,
-              d.n, k,
-              blk - d.block_begin, S, lut, red, part, xq);
+  if (d.w_group_scales) {
+    fused_block<true>(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{nullptr, 0.0f}, d.y,
+                      d.acc, d.n, k, blk - d.block_begin, S, lut, red, part, xq,
+                      d.w_group_scales, redf);
+  } else {
+    fused_block(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{d.w_scales, d.w_scale}, d.y,
+                d.acc, d.n, k, blk - d.block_begin, S, lut, red, part, xq);
+  }
 }
 
 }  // namespace

@@ -197,7 +197,7 @@ def test_batched_prepare():
     # (32 tiles, S=2) 8, (8, S=2) 2, (128, S=2) 32, (32, S=8) 32, (2, S=1) 1
     assert begins == [0, 8, 10, 42, 74]
     assert total == 75
-    assert ctypes.sizeof(sh.sherry_gemv_desc) == 64
+    assert ctypes.sizeof(sh.sherry_gemv_desc) == 72
     descs[3].k = 6
     with pytest.raises(sh.SherryError):
         sh.sherry_gemv_batched_prepare(descs)
@@ -231,7 +231,7 @@ def test_fused_validation_without_launch():
     total = sh.sherry_gemv_f32_batched_prepare(descs)
     # fused workgroups are longer: C/S <= 16 containers per wave
     assert [d.block_begin for d in descs] == [0, 4, 20] and total == 36
-    assert ctypes.sizeof(sh.sherry_gemv_f32_desc) == 64
+    assert ctypes.sizeof(sh.sherry_gemv_f32_desc) == 72
     descs[2].k = 40000
     with pytest.raises(sh.SherryError):
         sh.sherry_gemv_f32_batched_prepare(descs)
@@ -305,3 +305,20 @@ def test_group_validation_without_launch():
     f = L.sherry_gemv_f32_group
     assert f(FAKE, FAKE, FAKE, None, FAKE, None, 64, 128, None) == sh.SHERRY_E_INVALID
     assert f(FAKE, FAKE, FAKE, FAKE + 1, FAKE, None, 64, 128, None) == sh.SHERRY_E_ALIGN
+
+
+def test_batched_scale_fields_validation():
+    # a descriptor takes per-channel or per-group scales, not both
+    for cls, prep in ((sh.sherry_gemv_desc, L.sherry_gemv_batched_prepare),
+                      (sh.sherry_gemv_f32_desc, L.sherry_gemv_f32_batched_prepare)):
+        descs = (cls * 1)()
+        d = descs[0]
+        d.w, d.x, d.x_scale, d.y = FAKE, FAKE, FAKE, FAKE
+        d.n, d.k, d.w_scale = 64, 128, 1.0
+        total = ctypes.c_int64(0)
+        d.w_scales, d.w_group_scales = FAKE, FAKE
+        assert prep(descs, 1, ctypes.byref(total)) == sh.SHERRY_E_INVALID
+        d.w_scales, d.w_group_scales = None, FAKE + 2
+        assert prep(descs, 1, ctypes.byref(total)) == sh.SHERRY_E_ALIGN
+        d.w_group_scales = FAKE
+        assert prep(descs, 1, ctypes.byref(total)) == sh.SHERRY_OK and total.value >= 1

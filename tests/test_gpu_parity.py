@@ -350,9 +350,11 @@ def _epi(acc, sx, sw):
     return oracle.epilogue(acc, sx, sw)
 
 
-def _desc_scale(d, dev, keep, n, seed, i, channel):
+def _desc_scale(d, dev, keep, n, seed, i, channel, k=None):
     """Per-tensor scale, or (channel and even i) a per-channel vector in
-    d.w_scales; returns what the oracle epilogue takes."""
+    d.w_scales, or (channel == "mixed", i % 3 == 1) per-group scales in
+    d.w_group_scales; returns what the oracle epilogue takes (a float, a
+    vector, or ("groups", matrix))."""
     if channel and i % 2 == 0:
         sw = _channel_scales(n, seed * 1000 + i)
         swd = torch.from_numpy(sw).to(dev)
@@ -360,6 +362,13 @@ def _desc_scale(d, dev, keep, n, seed, i, channel):
         d.w_scales = swd.data_ptr()
         d.w_scale = float("nan")  # unused
         return sw
+    if channel == "mixed" and i % 3 == 1:
+        gs = _group_scales(n, k, seed * 1000 + i)
+        gsd = torch.from_numpy(gs).to(dev)
+        keep.append(gsd)
+        d.w_group_scales = gsd.data_ptr()
+        d.w_scale = float("nan")
+        return ("groups", gs)
     return None
 
 
@@ -382,7 +391,7 @@ def _batched(dev, shapes, seed, want_acc=True, channel=False):
         d.w, d.x, d.x_scale, d.y = w.data_ptr(), qd.data_ptr(), sxd.data_ptr(), y.data_ptr()
         d.acc = a.data_ptr() if want_acc else None
         d.n, d.k, d.w_scale = n, k, sw
-        swc = _desc_scale(d, dev, keep, n, seed, i, channel)
+        swc = _desc_scale(d, dev, keep, n, seed, i, channel, k)
         sw = sw if swc is None else swc
         refs.append((t, q, sx, sw, y, a))
     total = sh.sherry_gemv_batched_prepare(descs)
@@ -409,6 +418,26 @@ def test_batched_gemv_channel_scales(dev):
         acc_ref = oracle.gemm_i32(q, t, threads=8)
         assert np.array_equal(a.cpu().numpy(), acc_ref[0])
         assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw)[0])
+
+
+def _check_mixed(q, t, sx, sw, y, a):
+    if isinstance(sw, tuple):
+        y_ref, mag, acc_ref = oracle.product_groups(q, t, sx, sw[1], threads=8)
+        assert np.array_equal(a, acc_ref[0])
+        assert _group_ok(y, y_ref[0], mag[0], t.shape[1])
+    else:
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a, acc_ref[0])
+        assert _y_ok(y, _epi(acc_ref, sx, sw)[0])
+
+
+def test_batched_gemv_mixed_scales(dev):
+    # per-tensor, per-channel and per-group descriptors in one grouped launch
+    _say("batched mixed scales")
+    shapes = [(64, 128), (65, 132), (2048, 2048), (512, 2048), (300, 8192), (1, 4), (70, 1032),
+              (130, 3076)]
+    for t, q, sx, sw, y, a in _batched(dev, shapes, 48, channel="mixed"):
+        _check_mixed(q, t, sx, sw, y.cpu().numpy(), a.cpu().numpy())
 
 
 def test_batched_split_paths(dev):
@@ -552,7 +581,7 @@ def _fused_batched(dev, shapes, seed, with_scale=True, channel=False):
         d.w, d.x, d.y, d.acc = w.data_ptr(), xd.data_ptr(), y.data_ptr(), a.data_ptr()
         d.x_scale = sxd.data_ptr() if with_scale else None
         d.n, d.k, d.w_scale = n, k, sw
-        swc = _desc_scale(d, dev, hold, n, seed, i, channel)
+        swc = _desc_scale(d, dev, hold, n, seed, i, channel, k)
         keep.append((t, x, sw if swc is None else swc, w, xd, sxd, y, a))
     total = sh.sherry_gemv_f32_batched_prepare(descs)
     dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
@@ -581,6 +610,15 @@ def test_fused_batched_channel_scales(dev):
         acc_ref = oracle.gemm_i32(q, t, threads=8)
         assert np.array_equal(a.cpu().numpy(), acc_ref[0])
         assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw)[0])
+
+
+def test_fused_batched_mixed_scales(dev):
+    _say("fused batched mixed scales")
+    shapes = [(64, 128), (65, 132), (2048, 2048), (300, 8192), (1, 4), (100, 8196), (70, 260)]
+    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 52, channel="mixed"):
+        q, sx = oracle.quantize_act(x)
+        assert sxd.cpu().numpy()[0] == sx[0]
+        _check_mixed(q, t, sx, sw, y.cpu().numpy(), a.cpu().numpy())
 
 
 def test_fused_batched_decode_step_llama_1b(dev):
