@@ -446,7 +446,11 @@ struct QuantizeRow {
 #pragma unroll
       for (int e = 0; e < NV; ++e) {
         const int i = threadIdx.x + e * kGemvThreads;
-        v[e] = (i < (k >> 2)) ? x4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+        // every thread loads (a clamped index past the row), so that the
+        // loads issue back to back instead of behind exec-masked branches
+        const int k4 = k >> 2;
+        const float4 t = x4[i < k4 ? i : k4 - 1];
+        v[e] = (i < k4) ? t : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
   }
@@ -487,7 +491,7 @@ struct QuantizeRow {
 };
 
 // Fused product of one block: the row length picks the quantizer (rows up
-// to 2048 and 8192 values from registers, longer ones in two passes).
+// to 2048, 8192 and 16384 values from registers, longer ones in two passes).
 template <bool kGrp = false>
 __device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, float* x_scale,
                                             bool write_scale, WScale ws, float* y,
@@ -503,6 +507,10 @@ __device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, fl
   } else if (kp <= 16 * kGemvThreads) {
     gemv_block<1, kGrp>(w, XFromLds{xq},
                         QuantizeRow<4>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
+                        n, k, g, S, lut, red, gs, redf);
+  } else if (kp <= 32 * kGemvThreads) {
+    gemv_block<1, kGrp>(w, XFromLds{xq},
+                        QuantizeRow<8>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
                         n, k, g, S, lut, red, gs, redf);
   } else {
     gemv_block<1, kGrp>(w, XFromLds{xq},
