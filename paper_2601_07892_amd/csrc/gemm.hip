@@ -274,24 +274,56 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
   }
   compute(smem + (ks & 1) * G::STAGE);
 
-  // ---- epilogue: lane holds C[i][j] with j = lane%32 and
-  //      i = 8*(r/4) + 4*(lane/32) + r%4 for accumulator element r
+  // ---- epilogue, staged through LDS so that every lane stores 16 bytes of
+  // one row and a wave writes whole rows.  Lane holds C[i][j] of fragment
+  // (a, bb) with j = lane%32 and i = 8*(r/4) + 4*(lane/32) + r%4 for
+  // accumulator element r.  Each wave copies one 32-row strip of its block
+  // (32 x WN int32, row stride WN + 8 words, so that the half-waves' rows, 4
+  // apart, use disjoint banks) into its own LDS region and reads it back as
+  // 16-byte row pieces; a wave's LDS accesses run in order, so the strip
+  // needs no barrier of its own.
+  __syncthreads();  // every wave is done reading the stages
+  constexpr int SW = G::WN + 8;
+  static_assert(G::THREADS / 64 * 32 * SW * 4 <= 2 * G::STAGE, "epilogue strips fit in LDS");
+  int32_t* strip = reinterpret_cast<int32_t*>(smem) + wave * 32 * SW;
+  const bool vec = (N % 4 == 0) && (reinterpret_cast<uintptr_t>(y) % 16 == 0) &&
+                   (!acc_out || reinterpret_cast<uintptr_t>(acc_out) % 16 == 0);
+  constexpr int RP = G::WN / 4;  // 16-byte pieces per strip row
 #pragma unroll
   for (int a = 0; a < G::FM; ++a) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t gm = m0 + wr * G::WM + a * 32 + 8 * (r >> 2) + 4 * fhalf + (r & 3);
-      if (gm >= M) continue;
-      const float sx = x_scale[gm];
+    for (int bb = 0; bb < G::FN; ++bb)
 #pragma unroll
-      for (int bb = 0; bb < G::FN; ++bb) {
-        const int64_t gn = n0 + wc * G::WN + bb * 32 + frow;
-        if (gn >= N) continue;
-        const int32_t v = acc[a][bb][r];
-        y[gm * N + gn] = static_cast<float>(v) * (sx * ws.at(gn));
-        if (acc_out) acc_out[gm * N + gn] = v;
+      for (int r = 0; r < 16; ++r)
+        strip[(8 * (r >> 2) + 4 * fhalf + (r & 3)) * SW + bb * 32 + frow] = acc[a][bb][r];
+    __asm__ volatile("" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < 32 * RP / 64; ++i) {
+      const int p = lane + 64 * i;
+      const int row = p / RP, c4 = p % RP;
+      const v4i v = *reinterpret_cast<const v4i*>(strip + row * SW + 4 * c4);
+      const int64_t gm = m0 + wr * G::WM + a * 32 + row;
+      const int64_t gn = n0 + wc * G::WN + 4 * c4;
+      if (gm >= M || gn >= N) continue;
+      const float sx = x_scale[gm];
+      if (vec) {
+        const float4 o = make_float4(static_cast<float>(v.x) * (sx * ws.at(gn)),
+                                     static_cast<float>(v.y) * (sx * ws.at(gn + 1)),
+                                     static_cast<float>(v.z) * (sx * ws.at(gn + 2)),
+                                     static_cast<float>(v.w) * (sx * ws.at(gn + 3)));
+        *reinterpret_cast<float4*>(y + gm * N + gn) = o;
+        if (acc_out) *reinterpret_cast<v4i*>(acc_out + gm * N + gn) = v;
+      } else {
+        const int32_t vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (gn + e >= N) break;
+          y[gm * N + gn + e] = static_cast<float>(vv[e]) * (sx * ws.at(gn + e));
+          if (acc_out) acc_out[gm * N + gn + e] = vv[e];
+        }
       }
     }
+    __asm__ volatile("" ::: "memory");  // the next strip overwrites these reads
   }
 }
 
