@@ -459,29 +459,68 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
 
   // epilogue (split 0 of each tile): lane holds C[token][row] for row =
   // 32h + lane%32 of the tile and token = 32tb + 8(e/4) + 4(lane/32) + e%4,
-  // e = accumulator element
+  // e = accumulator element.  Each 32-token x 32-row block is staged in the
+  // wave's own LDS region (row stride 40 words: the half-waves' tokens, 4
+  // apart, use disjoint banks) and read back as 16-byte pieces of 4 rows, so
+  // that every lane stores 16 bytes and 8 lanes write 128 contiguous bytes;
+  // a wave's LDS accesses run in order, so the region needs no barrier of
+  // its own.
+  sk_lds_barrier();  // every wave is done with the stages and the reduction
   if (r >= R || sp != 0) return;
+  constexpr int SW = 40;
+  static_assert((W / S) * 32 * SW * 4 <= NST * G::STAGE, "epilogue regions fit the stages");
+  int32_t* strip = reinterpret_cast<int32_t*>(xs) + (wave / S) * 32 * SW;
+  const bool vec = (p.n % 4 == 0) && (reinterpret_cast<uintptr_t>(p.y) % 16 == 0) &&
+                   (GR || !p.acc || reinterpret_cast<uintptr_t>(p.acc) % 16 == 0);
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int row = r * kTileRows + 32 * h + (lane & 31);
-    if (row >= p.n) continue;
+  for (int tb = 0; tb < MT; ++tb) {
 #pragma unroll
-    for (int tb = 0; tb < MT; ++tb) {
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int tok = 32 * tb + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (tok >= p.m) continue;
-        const int32_t v = c[h][tb][e];
+        const int tl = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if constexpr (GR) {
-          as_global_mut(p.y)[int64_t(tok) * p.n + row] =
-              cf[h][0][e] * as_global(p.x_scale)[tok];
+          // copy the element out first: a bit cast of a vector element in
+          // place reads element 0
+          const float f = cf[h][0][e];
+          strip[tl * SW + (lane & 31)] = __float_as_int(f);
         } else {
-          const float s = as_global(p.x_scale)[tok] * p.ws.at(row);
-          as_global_mut(p.y)[int64_t(tok) * p.n + row] = static_cast<float>(v) * s;
+          strip[tl * SW + (lane & 31)] = c[h][tb][e];
         }
-        if constexpr (!GR)
-          if (p.acc) as_global_mut(p.acc)[int64_t(tok) * p.n + row] = v;
       }
+      __asm__ volatile("" ::: "memory");
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = lane + 64 * i;
+        const int tl = q >> 3, c4 = q & 7;
+        const v4i v = *reinterpret_cast<const v4i*>(strip + tl * SW + 4 * c4);
+        const int tok = 32 * tb + tl;
+        const int row = r * kTileRows + 32 * h + 4 * c4;
+        if (tok >= p.m || row >= p.n) continue;
+        const float sx = as_global(p.x_scale)[tok];
+        const int32_t vv[4] = {v.x, v.y, v.z, v.w};
+        float o[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if constexpr (GR) o[u] = __int_as_float(vv[u]) * sx;
+          else o[u] = static_cast<float>(vv[u]) * (sx * p.ws.at(row + u));
+        }
+        float* yrow = as_global_mut(p.y) + int64_t(tok) * p.n + row;
+        if (vec) {
+          *reinterpret_cast<float4*>(yrow) = make_float4(o[0], o[1], o[2], o[3]);
+          if constexpr (!GR)
+            if (p.acc) *reinterpret_cast<v4i*>(as_global_mut(p.acc) + int64_t(tok) * p.n + row) = v;
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (row + u >= p.n) break;
+            yrow[u] = o[u];
+            if constexpr (!GR)
+              if (p.acc) as_global_mut(p.acc)[int64_t(tok) * p.n + row + u] = vv[u];
+          }
+        }
+      }
+      __asm__ volatile("" ::: "memory");  // the next block overwrites these reads
     }
   }
 }
