@@ -175,6 +175,13 @@ def test_kernel_choice_by_m():
         assert sh.sherry_gemm_kernel_for(m, 8192, 2048) == sh.SHERRY_KERNEL_MFMA
         # a longer K than N (down projections) stays register-decoded
         assert sh.sherry_gemm_kernel_for(m, 2048, 8192) == sh.SHERRY_KERNEL_SKINNY
+        # so do k >= 3072 shapes up to 2048 tokens
+        assert sh.sherry_gemm_kernel_for(m, 3072, 3072) == sh.SHERRY_KERNEL_SKINNY
+        assert sh.sherry_gemm_kernel_for(m, 14336, 4096) == sh.SHERRY_KERNEL_SKINNY
+        assert sh.sherry_gemm_kernel_for(m, 8192, 3072) == sh.SHERRY_KERNEL_SKINNY
+    assert sh.sherry_gemm_kernel_for(2049, 3072, 3072) == sh.SHERRY_KERNEL_MFMA
+    assert sh.sherry_gemm_kernel_for(4096, 3072, 3072) == sh.SHERRY_KERNEL_MFMA
+    assert sh.sherry_gemm_kernel_for(2048, 3071 + 1, 2048) == sh.SHERRY_KERNEL_MFMA
     assert sh.sherry_gemm_kernel_for(0, 2048, 2048) == -sh.SHERRY_E_SHAPE
 
 
