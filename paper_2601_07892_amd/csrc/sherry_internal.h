@@ -26,12 +26,12 @@ constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Decode kernel work split.  A workgroup has kGemvWaves waves; the
 // containers of a 64-row tile are split among S waves of one workgroup,
 // S = the smallest power of two with C / S <= target, at most kGemvWaves.
-// Short waves keep many workgroups queued behind the resident ones, so a CU
-// that finishes early is refilled instead of idling (target kGemvTarget).
-// The fused quantize + product kernels quantize the activation row once per
-// workgroup, so they use fewer, longer workgroups (kFusedTarget).
+// Up to 16 units per wave (kGemvTarget, kFusedTarget) was measured fastest
+// for grouped decode steps, for both the int8 and the fused quantize +
+// product kernels: shorter waves (more workgroups, more refills) and longer
+// ones (fewer workgroups than the GPU holds) were both slower.
 constexpr int kGemvWaves = 8;
-constexpr int kGemvTarget = 8;
+constexpr int kGemvTarget = 16;
 constexpr int kFusedTarget = 16;
 // Longest activation row of the fused quantize + product kernels (the
 // quantized row is held in LDS); equals SHERRY_FUSED_MAX_K.

@@ -200,10 +200,10 @@ def test_batched_prepare():
     total = sh.sherry_gemv_batched_prepare(descs)
     begins = [d.block_begin for d in descs]
     # 8-wave workgroups; a 64-row tile with C containers is split over the
-    # smallest power of two S <= 8 with C/S <= 8 waves:
-    # (32 tiles, S=2) 8, (8, S=2) 2, (128, S=2) 32, (32, S=8) 32, (2, S=1) 1
-    assert begins == [0, 8, 10, 42, 74]
-    assert total == 75
+    # smallest power of two S <= 8 with C/S <= 16 waves, 8/S tiles per block:
+    # (32 tiles, S=1) 4, (8, S=1) 1, (128, S=1) 16, (32, S=4) 16, (2, S=1) 1
+    assert begins == [0, 4, 5, 21, 37]
+    assert total == 38
     assert ctypes.sizeof(sh.sherry_gemv_desc) == 72
     descs[3].k = 6
     with pytest.raises(sh.SherryError):
