@@ -187,6 +187,34 @@ def test_mfma_large_tile_config(dev):
     assert np.array_equal(y.astype(np.float64), acc.astype(np.float64) * 0.125)
 
 
+@pytest.mark.parametrize("kernel", ["MFMA", "SKINNY"])
+@pytest.mark.parametrize("m,n,k", [(64, 256, 512), (300, 512, 1032), (2048, 1024, 640)])
+def test_epilogue_unaligned_outputs(dev, kernel, m, n, k):
+    # y and acc 4 bytes past a 16-byte boundary (n a multiple of 4): the MFMA
+    # kernels' 16-byte row stores must fall back to 4-byte stores
+    sh = _sh()
+    _say("unaligned epilogue", kernel, m, n, k)
+    t = synth.ternary_34(n, k, 37, "ua", n, k)
+    q = synth.int8_any(m, k, 37, "uaq", m, k)
+    sx = np.abs(synth.activations(1, m, 37, "uas", m)[0]).astype(np.float32) + 0.01
+    sw = _channel_scales(n, 37)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    yb = torch.full((m * n + 4,), float("nan"), dtype=torch.float32, device=dev)
+    ab = torch.full((m * n + 4,), -7, dtype=torch.int32, device=dev)
+    y, acc = yb[1:1 + m * n], ab[1:1 + m * n]
+    assert y.data_ptr() % 16 == 4 and acc.data_ptr() % 16 == 4
+    sh.sherry_gemm_channel(w, torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev),
+                           torch.from_numpy(sw).to(dev), y, acc, m, n, k,
+                           getattr(sh, "SHERRY_KERNEL_" + kernel))
+    torch.cuda.synchronize()
+    acc_ref = oracle.gemm_i32(q, t, threads=8)
+    assert np.array_equal(acc.cpu().numpy().reshape(m, n), acc_ref)
+    assert _y_ok(y.cpu().numpy().reshape(m, n), oracle.epilogue_rows(acc_ref, sx, sw))
+    # the guard words on both sides are untouched
+    assert np.isnan(yb[0].item()) and np.isnan(yb[-3:].cpu().numpy()).all()
+    assert ab[0].item() == -7 and (ab[-3:].cpu().numpy() == -7).all()
+
+
 # The MFMA tile configuration follows from (m, n): m <= 32 -> 32x256; else
 # the cheapest of 256x256, 128x256, 128x128 by rounds of 256 workgroups x
 # tile area.  These are the M = 2048 prefill shapes of LLaMA-3.2-3B (the
