@@ -237,8 +237,10 @@ int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
                         int64_t total_blocks, void* stream);
 
 /* ---------------------------------------------------------------------- */
-/* Grouped small-M products (1 <= m <= 64 tokens each): many independent  */
-/* products in one launch, on the small-M kernel (SHERRY_KERNEL_SKINNY).   */
+/* Grouped products: many independent products (any m, e.g. the q, k and  */
+/* v projections of one layer) in one launch, on the register-decoded      */
+/* kernel (SHERRY_KERNEL_SKINNY); products run in token blocks of 32 when  */
+/* every m <= 32, else of 64.                                              */
 /* ---------------------------------------------------------------------- */
 
 typedef struct sherry_gemm_desc {
@@ -248,7 +250,7 @@ typedef struct sherry_gemm_desc {
   float* y;              /* device, fp32 [m][n]                            */
   int32_t* acc;          /* device, int32 [m][n] or NULL                   */
   const float* w_scales; /* device, fp32 [n] per-channel scales, or NULL   */
-  int32_t n, k, m;       /* 1 <= m <= 64                                   */
+  int32_t n, k, m;       /* 1 <= m <= SHERRY_MAX_M                         */
   float w_scale;
   int32_t block_begin;   /* written by sherry_gemm_batched_prepare         */
   int32_t reserved;      /* set to 0                                       */

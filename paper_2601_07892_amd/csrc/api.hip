@@ -47,7 +47,6 @@ constexpr int64_t kGemvMaxM = 4;
 constexpr int64_t kSkinnyMaxM = 512;
 constexpr int64_t kSkinnyMinLongK = 3072, kSkinnyMaxLongM = 2048;
 // Largest m of one product in a grouped small-M launch (one token block).
-constexpr int64_t kBatchedMaxM = 64;
 
 int check_product(const uint8_t* w, const int8_t* x, const float* x_scale, float* y,
                   int64_t m, int64_t n, int64_t k, uintptr_t x_align) {
@@ -294,20 +293,24 @@ extern "C" int sherry_gemv_f32_batched(const sherry_gemv_f32_desc* descs_dev, in
 extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
                                            int64_t* total_blocks, int32_t* max_m) {
   if (!descs || !total_blocks || !max_m || count < 1) return SHERRY_E_INVALID;
-  int64_t blocks = 0;
   int32_t mm = 0;
   for (int i = 0; i < count; ++i) {
-    sherry_gemm_desc& d = descs[i];
+    const sherry_gemm_desc& d = descs[i];
     int st = check_product(d.w, d.x, d.x_scale, d.y, d.m, d.n, d.k, 16);
     if (st != SHERRY_OK) return st;
-    if (d.m > kBatchedMaxM) return SHERRY_E_SHAPE;
     if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)))
       return SHERRY_E_ALIGN;
+    if (d.m > mm) mm = d.m;
+  }
+  // every product runs in token blocks of the size the largest m selects
+  const int64_t tok = skinny_batched_tokens(mm);
+  int64_t blocks = 0;
+  for (int i = 0; i < count; ++i) {
+    sherry_gemm_desc& d = descs[i];
     d.block_begin = static_cast<int32_t>(blocks);
     d.reserved = 0;
-    blocks += skinny_blocks(d.n);
+    blocks += int64_t(skinny_blocks(d.n)) * ceil_div(d.m, tok);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
-    if (d.m > mm) mm = d.m;
   }
   *total_blocks = blocks;
   *max_m = mm;
@@ -318,7 +321,7 @@ extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
                                    int64_t total_blocks, int32_t max_m, void* stream) {
   if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
     return SHERRY_E_INVALID;
-  if (max_m < 1 || max_m > kBatchedMaxM) return SHERRY_E_SHAPE;
+  if (max_m < 1 || max_m > SHERRY_MAX_M) return SHERRY_E_SHAPE;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
   return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
 }

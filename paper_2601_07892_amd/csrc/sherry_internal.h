@@ -171,6 +171,7 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
                      int64_t n, int64_t k, hipStream_t s);
 
 int skinny_blocks(int64_t n);
+int skinny_batched_tokens(int max_m);
 int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                   float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);
 int launch_skinny_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,

@@ -571,16 +571,36 @@ __global__ __launch_bounds__(64 * kSkWavesGrouped) void skinny_batched_kernel(
   }
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
-  const SkProblem p{d.w,   d.x,   d.x_scale, d.y, d.acc, d.n, d.k, d.m,
-                    WScale{d.w_scales, d.w_scale}, nullptr};
-  sk_block<MT, 1, NST, W>(p, blk - d.block_begin, lut, lds + kSkLutBytes);
+  // a product's blocks: its tile groups for token block 0, then for token
+  // block 1, ... (blocks in flight together share their activations)
+  constexpr int TOK = SkCfg<MT, NST, W>::TOK;
+  const int gb = static_cast<int>(ceil_div(ceil_div(d.n, kTileRows), W));
+  const int lb = blk - d.block_begin;
+  const int tb = lb / gb;
+  const int t0 = tb * TOK;
+  const SkProblem p{d.w,
+                    d.x + int64_t(t0) * d.k,
+                    d.x_scale + t0,
+                    d.y + int64_t(t0) * d.n,
+                    d.acc ? d.acc + int64_t(t0) * d.n : nullptr,
+                    d.n,
+                    d.k,
+                    (d.m - t0 < TOK) ? d.m - t0 : TOK,
+                    WScale{d.w_scales, d.w_scale},
+                    nullptr};
+  sk_block<MT, 1, NST, W>(p, lb - tb * gb, lut, lds + kSkLutBytes);
 }
 
 }  // namespace
 
-// Workgroups of one product in a grouped launch.
+// Workgroups of one product's token block in a grouped launch, and the
+// token block of a grouped launch whose largest product has max_m tokens.
 int skinny_blocks(int64_t n) {
   return static_cast<int>(ceil_div(ceil_div(n, kTileRows), kSkWavesGrouped));
+}
+int skinny_batched_tokens(int max_m) {
+  return max_m <= 32 ? SkCfg<1, kSkStages<1, true>, kSkWavesGrouped>::TOK
+                     : SkCfg<2, kSkStages<2, true>, kSkWavesGrouped>::TOK;
 }
 
 // K splits per tile of a lone launch: the smallest power of two (up to a

@@ -262,15 +262,28 @@ def test_skinny_validation_without_launch():
     # one workgroup per 8 row tiles: 32 tiles -> 4, 128 -> 16, 2 -> 1
     assert [d.block_begin for d in descs] == [0, 4, 20] and total == 21 and max_m == 64
     assert ctypes.sizeof(sh.sherry_gemm_desc) == 72
-    # a grouped launch stages at most one 64-token block per product
+    # longer products run in 64-token blocks: 65 tokens -> 2 blocks of 16
     descs[1].m = 65
-    with pytest.raises(sh.SherryError):
-        sh.sherry_gemm_batched_prepare(descs)
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    assert [d.block_begin for d in descs] == [0, 4, 36] and total == 37 and max_m == 65
+    # 2048 tokens -> 32 token blocks of each product's tile groups
+    descs[0].m = 2048
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    assert [d.block_begin for d in descs] == [0, 128, 160] and total == 161
+    # every m <= 32: 32-token blocks
+    for d, m in zip(descs, (32, 20, 1)):
+        d.m = m
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    assert [d.block_begin for d in descs] == [0, 4, 20] and total == 21 and max_m == 32
+    descs[0].m = 33
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    assert total == 21 and max_m == 33
     descs[1].m = 64
     descs[2].x = FAKE + 4
     with pytest.raises(sh.SherryError):
         sh.sherry_gemm_batched_prepare(descs)
-    assert L.sherry_gemm_batched(FAKE, 1, 1, 65, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_batched(FAKE, 1, 1, sh.SHERRY_MAX_M + 1, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_batched(FAKE, 1, 1, 0, None) == sh.SHERRY_E_SHAPE
     assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 16, None) == sh.SHERRY_E_ALIGN
     assert L.sherry_gemm_batched(None, 1, 1, 16, None) == sh.SHERRY_E_INVALID
 

@@ -759,7 +759,20 @@ def test_skinny_batched_parity(dev, big):
         assert _y_ok(y.cpu().numpy(), oracle.epilogue(acc_ref, sx, sw))
 
 
-@pytest.mark.parametrize("spec_name,m", [("LLAMA_3B", 16), ("STRESS_8B", 64)])
+def test_skinny_batched_any_m(dev):
+    # products longer than one token block (several 64-token blocks, ragged
+    # last block) grouped with short ones in one launch
+    _say("skinny batched any m")
+    cases = [(65, 64, 128), (300, 520, 2052), (5, 130, 1032), (129, 257, 388), (200, 64, 4)]
+    keep, max_m = _skinny_batched(dev, cases, 57, channel=True)
+    assert max_m == 300
+    for t, q, sx, sw, w, qd, sxd, y, a in keep:
+        acc_ref = oracle.gemm_i32(q, t, threads=8)
+        assert np.array_equal(a.cpu().numpy(), acc_ref)
+        assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw))
+
+
+@pytest.mark.parametrize("spec_name,m", [("LLAMA_3B", 16), ("STRESS_8B", 64), ("LLAMA_3B", 2048)])
 def test_skinny_batched_model_step_sampled(dev, spec_name, m):
     # every linear of one layer of the model at M tokens in one grouped
     # launch (the configurations the benchmark times), sampled outputs
