@@ -334,6 +334,65 @@ def bench_prefill(sh, torch, dev, spec, m, seed, reps=10):
             "shapes": rows}
 
 
+def bench_prefill_grouped(sh, torch, dev, spec, m, seed, reps=10):
+    """One layer at M tokens in the four launches its data dependences allow:
+    q, k and v grouped in one launch (they read the same activations), o
+    alone, gate and up grouped, down alone (lone launches: automatic kernel
+    choice).  Dense-equivalent 2MNK ops over the layer's time."""
+    blk = {lin.name: lin for lin in synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])}
+    bufs = {}
+    for name, lin in blk.items():
+        t = synth.ternary_34(lin.n, lin.k, seed, "pw", lin.name, lin.k)
+        bufs[name] = (torch.from_numpy(sh.sherry_pack(t)).to(dev),
+                      torch.empty((m, lin.n), dtype=torch.float32, device=dev))
+    acts = {}
+    for src in ("qkv", "o", "gateup", "down"):
+        k = blk["down"].k if src == "down" else blk["q"].k
+        x = torch.from_numpy(synth.activations(m, k, seed, "pgx", src, outlier_frac=0.01)).to(dev)
+        q = torch.empty((m, k), dtype=torch.int8, device=dev)
+        sx = torch.empty(m, dtype=torch.float32, device=dev)
+        sh.sherry_quantize_act(x, q, sx)
+        acts[src] = (q, sx)
+
+    def group(names, src):
+        descs = (sh.sherry_gemm_desc * len(names))()
+        q, sx = acts[src]
+        for i, name in enumerate(names):
+            lin, (w, y) = blk[name], bufs[name]
+            d = descs[i]
+            d.w, d.x, d.x_scale, d.y, d.acc = (w.data_ptr(), q.data_ptr(), sx.data_ptr(),
+                                               y.data_ptr(), None)
+            d.n, d.k, d.m, d.w_scale = lin.n, lin.k, m, 0.02
+        total, max_m = sh.sherry_gemm_batched_prepare(descs)
+        return torch.from_numpy(sh.descs_to_bytes(descs)).to(dev), len(names), total, max_m
+
+    g_qkv, g_gu = group(["q", "k", "v"], "qkv"), group(["gate", "up"], "gateup")
+
+    def layer():
+        sh.sherry_gemm_batched(*g_qkv)
+        q, sx = acts["o"]
+        sh.sherry_gemm(bufs["o"][0], q, sx, 0.02, bufs["o"][1], None, m, blk["o"].n, blk["o"].k)
+        sh.sherry_gemm_batched(*g_gu)
+        q, sx = acts["down"]
+        sh.sherry_gemm(bufs["down"][0], q, sx, 0.02, bufs["down"][1], None, m, blk["down"].n,
+                       blk["down"].k)
+
+    for _ in range(2):
+        layer()
+    a, b = _events(torch)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        layer()
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) / reps * 1e3
+    ops = sum(2.0 * m * lin.n * lin.k for lin in blk.values())
+    return {"m": m, "launches": ["qkv grouped", "o", "gate+up grouped", "down"],
+            "per_layer_us": round(us, 2), "tops": round(ops / (us * 1e-6) / 1e12, 1),
+            "mfma_frac": round(ops / (us * 1e-6) / 1e12 / INT8_PEAK_TOPS, 4)}
+
+
 # ---------------------------------------------------------------------------
 # other decode configurations: LLaMA-3.2-3B and the 8B-scale stress model
 # ---------------------------------------------------------------------------
@@ -619,7 +678,11 @@ def main():
         args.no_extra = args.no_cpu = True
     if args.only == "prefill":
         r = bench_prefill(sh, torch, dev, synth.LLAMA_3B, 2048, args.seed)
-        print(json.dumps({"prefill_m2048_llama-3.2-3b": r}), flush=True)
+        g = bench_prefill_grouped(sh, torch, dev, synth.LLAMA_3B, 2048, args.seed)
+        log("prefill llama-3.2-3b M=2048: %.1f TOPS per projection launch, %.1f TOPS "
+            "with grouped launches" % (r["tops"], g["tops"]))
+        print(json.dumps({"prefill_m2048_llama-3.2-3b": r,
+                          "prefill_m2048_grouped_llama-3.2-3b": g}), flush=True)
         return
     if args.only == "grouped":
         rows = [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2)
@@ -704,6 +767,11 @@ def main():
             pre[name] = bench_prefill(sh, torch, dev, spec, 2048, args.seed)
             log("prefill %s M=2048: %.1f TOPS" % (name, pre[name]["tops"]))
         out["prefill_m2048"] = pre
+        grp = {}
+        for name, spec in (("llama-3.2-3b", synth.LLAMA_3B), ("llama-3.2-1b", synth.LLAMA_1B)):
+            grp[name] = bench_prefill_grouped(sh, torch, dev, spec, 2048, args.seed)
+            log("prefill %s M=2048, grouped launches: %.1f TOPS" % (name, grp[name]["tops"]))
+        out["prefill_m2048_grouped"] = grp
         other = {}
         for name, spec, copies in (("llama-3.2-3b", synth.LLAMA_3B, 2),
                                    ("stress-8b", synth.STRESS_8B, 1)):
