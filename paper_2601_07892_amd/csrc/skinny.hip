@@ -118,7 +118,9 @@ __device__ __forceinline__ void sk_lookup8(const uint32_t (&d)[5], const uint32_
 // K 32s..32s+15 of this lane's row, 8s+4..8s+7 the next 16; after the swap
 // the first four hold rows 0-31 and the last four rows 32-63, in the operand
 // layout.  Once the step's MFMAs are issued the 8 words take the next
-// container's lookups.
+// container's lookups; the compiler schedules the lookups among the
+// following steps (no scheduling barrier here: measured 2-5% faster, with
+// the same order of global loads and waits).
 template <int MT, int s>
 __device__ __forceinline__ void sk_mfma_step(uint32_t (&wv)[32], const uint32_t (&dn)[5],
                                              const uint32_t* lut, const v4i (&xv)[MT],
@@ -140,7 +142,6 @@ __device__ __forceinline__ void sk_mfma_step(uint32_t (&wv)[32], const uint32_t 
     c[1][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xv[tb], wh, c[1][tb], 0, 0, 0);
   }
   sk_lookup8<8 * s>(dn, lut, wv, std::make_integer_sequence<int, 8>{});
-  __builtin_amdgcn_sched_barrier(0);
 }
 
 // Accumulates one container's 128 K values (looked-up weights wv) against the
