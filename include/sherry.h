@@ -79,6 +79,12 @@ typedef enum sherry_status {
 #define SHERRY_KERNEL_GEMV 1 /* VALU decode + dot4 per token, M <= 4         */
 #define SHERRY_KERNEL_MFMA 2 /* decode to int8 tiles in LDS + int8 MFMA      */
 #define SHERRY_KERNEL_SKINNY 3 /* decode in registers + int8 MFMA, any M     */
+/* Activation lookup tables, M = 1, k <= SHERRY_ALUT_MAX_K: the table        */
+/* direction of the paper's CPU engine (16 dot products per block of 4       */
+/* activations, 4-bit index + sign bit per code; Sec. 3.1, Appendix A), a    */
+/* comparison point for SHERRY_KERNEL_GEMV.  Never chosen automatically.     */
+#define SHERRY_KERNEL_ALUT 4
+#define SHERRY_ALUT_MAX_K 8192
 
 /* Static string for a status code (never NULL). */
 const char* sherry_status_str(int status);
@@ -163,7 +169,8 @@ int sherry_gemm(const uint8_t* w, const int8_t* x, const float* x_scale,
                 int64_t k, void* stream);
 
 /* sherry_gemm with an explicit kernel (SHERRY_KERNEL_*); SHERRY_KERNEL_GEMV
- * requires m <= 4.  Results are bit-identical across kernels. */
+ * requires m <= 4, SHERRY_KERNEL_ALUT m = 1 and k <= SHERRY_ALUT_MAX_K
+ * (SHERRY_E_SHAPE otherwise).  Results are bit-identical across kernels. */
 int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
                    float w_scale, float* y, int32_t* acc, int64_t m,
                    int64_t n, int64_t k, int kernel, void* stream);

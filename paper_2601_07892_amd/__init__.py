@@ -27,6 +27,8 @@ SHERRY_KERNEL_AUTO = 0
 SHERRY_KERNEL_GEMV = 1
 SHERRY_KERNEL_MFMA = 2
 SHERRY_KERNEL_SKINNY = 3
+SHERRY_KERNEL_ALUT = 4
+SHERRY_ALUT_MAX_K = 8192
 SHERRY_MAX_K = 174720
 SHERRY_MAX_M = 1 << 24
 SHERRY_FUSED_MAX_K = 32768

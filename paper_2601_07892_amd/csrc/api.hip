@@ -126,6 +126,13 @@ int gemm_dispatch(const uint8_t* w, const int8_t* x, const float* x_scale, WScal
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
     return launch_gemm_mfma(w, x, x_scale, ws, y, acc, m, n, k, as_stream(stream));
   }
+  if (kernel == SHERRY_KERNEL_ALUT) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 4);
+    if (st != SHERRY_OK) return st;
+    if (m != 1 || k > SHERRY_ALUT_MAX_K) return SHERRY_E_SHAPE;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_gemv_alut(w, x, x_scale, ws, y, acc, n, k, as_stream(stream));
+  }
   return SHERRY_E_INVALID;
 }
 }  // namespace

@@ -170,6 +170,10 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
                      WScale ws, float* y, int32_t* acc, int64_t m,
                      int64_t n, int64_t k, hipStream_t s);
 
+// Activation-table product for one token (k <= SHERRY_ALUT_MAX_K).
+int launch_gemv_alut(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
+                     float* y, int32_t* acc, int64_t n, int64_t k, hipStream_t s);
+
 int skinny_blocks(int64_t n);
 int skinny_batched_tokens(int max_m);
 int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,

@@ -342,3 +342,20 @@ def test_batched_scale_fields_validation():
         assert prep(descs, 1, ctypes.byref(total)) == sh.SHERRY_E_ALIGN
         d.w_group_scales = FAKE
         assert prep(descs, 1, ctypes.byref(total)) == sh.SHERRY_OK and total.value >= 1
+
+
+def test_activation_table_kernel_validation_without_launch():
+    g = L.sherry_gemm_ex
+    K = sh.SHERRY_KERNEL_ALUT
+    # one token only, k up to SHERRY_ALUT_MAX_K, never the automatic choice
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 2, 64, 128, K, None) == sh.SHERRY_E_SHAPE
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 1, 64, sh.SHERRY_ALUT_MAX_K + 4, K,
+             None) == sh.SHERRY_E_SHAPE
+    assert g(FAKE, FAKE + 2, FAKE, 1.0, FAKE, None, 1, 64, 128, K, None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, FAKE + 2, 1, 64, 128, K, None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 1, 64, 128, 5, None) == sh.SHERRY_E_INVALID
+    for m in (1, 4, 16, 2048):
+        assert sh.sherry_gemm_kernel_for(m, 2048, 2048) != K
+    # per-group scales have no activation-table variant
+    assert L.sherry_gemm_group(FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, 64, 128, K,
+                               None) == sh.SHERRY_E_INVALID

@@ -215,6 +215,52 @@ def test_epilogue_unaligned_outputs(dev, kernel, m, n, k):
     assert ab[0].item() == -7 and (ab[-3:].cpu().numpy() == -7).all()
 
 
+# ------------------------------------------- activation-table kernel (M = 1)
+
+ALUT_CASES = [(1, 4), (64, 128), (65, 132), (300, 1032), (2048, 2048), (512, 8192),
+              (3072, 8188), (100, 260)]
+
+
+@pytest.mark.parametrize("n,k", ALUT_CASES)
+@pytest.mark.parametrize("channel", [False, True])
+def test_activation_table_kernel_parity(dev, n, k, channel):
+    sh = _sh()
+    _say("alut", n, k, channel)
+    t = synth.ternary_34(n, k, 39, "al", n, k)
+    q = synth.int8_any(1, k, 39, "alq", k)
+    q[0, :min(k, 8)] = [-128, -128, -128, -128, 127, 127, 127, 127][:min(k, 8)]  # extreme entries
+    sx = np.array([0.037], np.float32)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    y = torch.full((n,), float("nan"), dtype=torch.float32, device=dev)
+    acc = torch.full((n,), -7, dtype=torch.int32, device=dev)
+    qd, sxd = torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev)
+    if channel:
+        sw = _channel_scales(n, 39)
+        sh.sherry_gemm_channel(w, qd, sxd, torch.from_numpy(sw).to(dev), y, acc, 1, n, k,
+                               sh.SHERRY_KERNEL_ALUT)
+    else:
+        sw = synth.weight_scale(39, "al", n, k)
+        sh.sherry_gemm_ex(w, qd, sxd, sw, y, acc, 1, n, k, sh.SHERRY_KERNEL_ALUT)
+    torch.cuda.synchronize()
+    acc_ref = oracle.gemm_i32(q, t, threads=8)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref[0])
+    assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw)[0])
+
+
+def test_activation_table_matches_weight_table_kernel(dev):
+    # bit-identical y and acc to the weight-table GEMV on a LLaMA-3.2-3B down
+    # projection shape
+    sh = _sh()
+    n, k = 3072, 8192
+    _say("alut vs gemv", n, k)
+    t = synth.ternary_34(n, k, 41, "av")
+    q = synth.int8_any(1, k, 41, "avq")
+    sx = np.array([0.02], np.float32)
+    ya, aa = _run(dev, t, q, sx, 0.03, sh.SHERRY_KERNEL_ALUT, 1)
+    yg, ag = _run(dev, t, q, sx, 0.03, sh.SHERRY_KERNEL_GEMV, 1)
+    assert np.array_equal(aa, ag) and np.array_equal(ya, yg)
+
+
 # The MFMA tile configuration follows from (m, n): m <= 32 -> 32x256; else
 # the cheapest of 256x256, 128x256, 128x128 by rounds of 256 workgroups x
 # tile area.  These are the M = 2048 prefill shapes of LLaMA-3.2-3B (the

@@ -68,6 +68,22 @@ def test_mirror_pairs():
     assert len(pairs) == 16
 
 
+def test_sign_bit_and_four_index_bits():
+    # Sec. 3.1 / Appendix A reading: one sign bit and a 4-bit index.  With the
+    # third sign bit s2 as the sign, every code is +-(a code with s2 clear):
+    # decode(c) = (-1)^s2 * decode((c & 15) ^ (12 if s2 else 0)), and the 16
+    # codes with s2 clear are 16 distinct patterns (the activation-table
+    # kernel's 16 entries per block of 4 activations).
+    canon = {tuple(oracle.decode_code(i)) for i in range(16)}
+    assert len(canon) == 16
+    for c in range(32):
+        s2 = c >> 4
+        idx = (c & 15) ^ (12 if s2 else 0)
+        assert idx < 16
+        want = -oracle.decode_code(idx) if s2 else oracle.decode_code(idx)
+        assert list(oracle.decode_code(c)) == list(want)
+
+
 def test_low_two_bits_are_zero_position():
     for c in range(32):
         w = oracle.decode_code(c)
