@@ -561,6 +561,36 @@ def bench_scale_granularity(sh, torch, dev, spec, seed, ms=(1, 16), shapes=("q",
     return rows
 
 
+def bench_activation_tables(sh, torch, dev, spec, seed, shapes=("q", "gate", "down"), reps=3):
+    """M = 1 products on the weight-table kernel (the library's GEMV) and on
+    the activation-table kernel (the paper's LUT direction), same packed
+    weights rotated over copies, launched from a captured graph."""
+    blk = {lin.name: lin for lin in synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])}
+    rows = []
+    for name in shapes:
+        lin = blk[name]
+        n, k = lin.n, lin.k
+        t = synth.ternary_34(n, k, seed, "atk", name)
+        packed = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        nb = packed.numel()
+        ws = [packed.clone() for _ in range(_rotation(nb))]
+        q = torch.from_numpy(synth.int8_any(1, k, seed, "atkx", name)).to(dev)
+        sx = torch.full((1,), 0.01, dtype=torch.float32, device=dev)
+        y = torch.empty((n,), dtype=torch.float32, device=dev)
+        byts = nb + k + 4 + 4 * n
+        row = {"proj": name, "n": n, "k": k}
+        for key, kern in (("weight_table", sh.SHERRY_KERNEL_GEMV),
+                          ("activation_table", sh.SHERRY_KERNEL_ALUT)):
+            us = time_graph(lambda i: sh.sherry_gemm_ex(ws[i % len(ws)], q, sx, 0.02, y, None,
+                                                        1, n, k, kern), reps * len(ws), torch)
+            row[key + "_us"] = round(us, 3)
+            row[key + "_gbs"] = round(byts / (us * 1e-6) / 1e9, 1)
+        rows.append(row)
+        del ws, packed, q, sx, y
+        torch.cuda.empty_cache()
+    return rows
+
+
 def bench_two_bit(sh, torch, dev, spec, seed, shapes=("q", "gate", "down"), reps=3):
     """The same ternary weights as 1.25-bit codes and as the 2-bit reference
     layout, M = 1, each timed over rotated copies (launched from a captured
@@ -642,7 +672,8 @@ def main():
                     help="rotated weight copies (working set = copies x 152 MB)")
     ap.add_argument("--no-extra", action="store_true", help="skip the M=2048 GEMM and ceiling")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--only", choices=["decode", "product", "prefill", "grouped", "ternarize"],
+    ap.add_argument("--only", choices=["decode", "product", "prefill", "grouped", "ternarize",
+                                       "tables"],
                     default=None,
                     help="run only one part (for profiler runs): the timed decode steps, the "
                          "back-to-back product launches, the M=2048 LLaMA-3.2-3B layer, the "
@@ -689,6 +720,10 @@ def main():
                 for mm in (4, 16)]
         rows.append(bench_model_step_m(sh, torch, dev, synth.STRESS_8B, args.seed, 64, 1))
         print(json.dumps({"decode_small_m_grouped": rows}), flush=True)
+        return
+    if args.only == "tables":
+        print(json.dumps({"activation_vs_weight_tables_3b": bench_activation_tables(
+            sh, torch, dev, synth.LLAMA_3B, args.seed)}), flush=True)
         return
     if args.only == "ternarize":
         print(json.dumps({"ternarize_pack": bench_ternarize(sh, torch, dev, args.seed)}),
@@ -793,6 +828,11 @@ def main():
             "stress-8b": bench_shapes(sh, torch, dev, synth.STRESS_8B, args.seed, (1, 64)),
         }
         out["two_bit_vs_sherry_8b"] = bench_two_bit(sh, torch, dev, synth.STRESS_8B, args.seed)
+        out["activation_vs_weight_tables_3b"] = bench_activation_tables(sh, torch, dev,
+                                                                        synth.LLAMA_3B, args.seed)
+        for r in out["activation_vs_weight_tables_3b"]:
+            log("3b %s M=1: weight tables %.2f us, activation tables %.2f us" %
+                (r["proj"], r["weight_table_us"], r["activation_table_us"]))
         for r in out["two_bit_vs_sherry_8b"]:
             log("8b %s: 1.25-bit %.2f us vs 2-bit %.2f us (bytes %.3f, time %.3f)" %
                 (r["proj"], r["sherry_us"], r["two_bit_us"], r["bytes_ratio"], r["time_ratio"]))
