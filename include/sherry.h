@@ -257,6 +257,9 @@ typedef struct sherry_gemm_desc {
   float* y;              /* device, fp32 [m][n]                            */
   int32_t* acc;          /* device, int32 [m][n] or NULL                   */
   const float* w_scales; /* device, fp32 [n] per-channel scales, or NULL   */
+  const float* w_group_scales; /* device, fp32 [n][ceil(k/128)] per-group  */
+                         /* scales as in sherry_gemm_group, or NULL; not   */
+                         /* with w_scales, and acc must then be NULL       */
   int32_t n, k, m;       /* 1 <= m <= SHERRY_MAX_M                         */
   float w_scale;
   int32_t block_begin;   /* written by sherry_gemm_batched_prepare         */
@@ -264,7 +267,9 @@ typedef struct sherry_gemm_desc {
 } sherry_gemm_desc;
 
 /* Host: validates descs[0..count), fills each block_begin, *total_blocks
- * and *max_m (the largest m, which selects the launch's staging). */
+ * and *max_m, which selects the launch's token blocks: the largest m, or
+ * at most 32 when a descriptor carries per-group scales (their kernel runs
+ * 32-token blocks).  Pass it to sherry_gemm_batched unchanged. */
 int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
                                 int64_t* total_blocks, int32_t* max_m);
 

@@ -76,6 +76,7 @@ class sherry_gemm_desc(ctypes.Structure):
     _fields_ = [
         ("w", ctypes.c_void_p), ("x", ctypes.c_void_p), ("x_scale", ctypes.c_void_p),
         ("y", ctypes.c_void_p), ("acc", ctypes.c_void_p), ("w_scales", ctypes.c_void_p),
+        ("w_group_scales", ctypes.c_void_p),
         ("n", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32),
         ("w_scale", ctypes.c_float), ("block_begin", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]

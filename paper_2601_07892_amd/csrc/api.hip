@@ -97,7 +97,7 @@ extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
 // The descriptor layouts are part of the ABI (Python and C callers build them).
 static_assert(sizeof(sherry_gemv_desc) == 72, "sherry_gemv_desc layout");
 static_assert(sizeof(sherry_gemv_f32_desc) == 72, "sherry_gemv_f32_desc layout");
-static_assert(sizeof(sherry_gemm_desc) == 72, "sherry_gemm_desc layout");
+static_assert(sizeof(sherry_gemm_desc) == 80, "sherry_gemm_desc layout");
 
 namespace {
 // Product on the chosen kernel (kernel already resolved from AUTO).
@@ -301,26 +301,32 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
                                            int64_t* total_blocks, int32_t* max_m) {
   if (!descs || !total_blocks || !max_m || count < 1) return SHERRY_E_INVALID;
   int32_t mm = 0;
+  bool grouped = false;
   for (int i = 0; i < count; ++i) {
     const sherry_gemm_desc& d = descs[i];
     int st = check_product(d.w, d.x, d.x_scale, d.y, d.m, d.n, d.k, 16);
     if (st != SHERRY_OK) return st;
-    if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)))
+    if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)) ||
+        (d.w_group_scales && !aligned(d.w_group_scales, 4)))
       return SHERRY_E_ALIGN;
+    if (d.w_group_scales && (d.w_scales || d.acc)) return SHERRY_E_INVALID;
+    if (d.w_group_scales) grouped = true;
     if (d.m > mm) mm = d.m;
   }
-  // every product runs in token blocks of the size the largest m selects
-  const int64_t tok = skinny_batched_tokens(mm);
+  // every product runs in token blocks of the size the largest m selects;
+  // per-group scales run 32-token blocks
+  const int32_t sel = grouped && mm > 32 ? 32 : mm;
+  const int64_t tok = skinny_batched_tokens(sel);
   int64_t blocks = 0;
   for (int i = 0; i < count; ++i) {
     sherry_gemm_desc& d = descs[i];
     d.block_begin = static_cast<int32_t>(blocks);
     d.reserved = 0;
-    blocks += int64_t(skinny_blocks(d.n)) * ceil_div(d.m, tok);
+    blocks += int64_t(skinny_blocks(d.n, d.w_group_scales != nullptr)) * ceil_div(d.m, tok);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
   }
   *total_blocks = blocks;
-  *max_m = mm;
+  *max_m = sel;
   return SHERRY_OK;
 }
 

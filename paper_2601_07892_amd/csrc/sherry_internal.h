@@ -174,7 +174,7 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
 int launch_gemv_alut(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                      float* y, int32_t* acc, int64_t n, int64_t k, hipStream_t s);
 
-int skinny_blocks(int64_t n);
+int skinny_blocks(int64_t n, bool group_scales = false);
 int skinny_batched_tokens(int max_m);
 int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                   float* y, int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);

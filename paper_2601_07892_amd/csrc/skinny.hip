@@ -575,8 +575,29 @@ __global__ __launch_bounds__(64 * kSkWavesGrouped) void skinny_batched_kernel(
   // a product's blocks: its tile groups for token block 0, then for token
   // block 1, ... (blocks in flight together share their activations)
   constexpr int TOK = SkCfg<MT, NST, W>::TOK;
-  const int gb = static_cast<int>(ceil_div(ceil_div(d.n, kTileRows), W));
   const int lb = blk - d.block_begin;
+  if constexpr (MT == 1) {
+    // per-group scales (prepare reports a 32-token launch for them): K split
+    // in two, fp32 sums per group, no int32 totals
+    if (d.w_group_scales) {
+      const int gg = static_cast<int>(ceil_div(ceil_div(d.n, kTileRows), W / 2));
+      const int tg = lb / gg;
+      const int tg0 = tg * TOK;
+      const SkProblem pg{d.w,
+                         d.x + int64_t(tg0) * d.k,
+                         d.x_scale + tg0,
+                         d.y + int64_t(tg0) * d.n,
+                         nullptr,
+                         d.n,
+                         d.k,
+                         (d.m - tg0 < TOK) ? d.m - tg0 : TOK,
+                         WScale{nullptr, 0.0f},
+                         d.w_group_scales};
+      sk_block<1, 2, NST, W, true>(pg, lb - tg * gg, lut, lds + kSkLutBytes);
+      return;
+    }
+  }
+  const int gb = static_cast<int>(ceil_div(ceil_div(d.n, kTileRows), W));
   const int tb = lb / gb;
   const int t0 = tb * TOK;
   const SkProblem p{d.w,
@@ -594,10 +615,13 @@ __global__ __launch_bounds__(64 * kSkWavesGrouped) void skinny_batched_kernel(
 
 }  // namespace
 
-// Workgroups of one product's token block in a grouped launch, and the
-// token block of a grouped launch whose largest product has max_m tokens.
-int skinny_blocks(int64_t n) {
-  return static_cast<int>(ceil_div(ceil_div(n, kTileRows), kSkWavesGrouped));
+// Workgroups of one product's token block in a grouped launch (products
+// with per-group scales split each tile's K in two, so a workgroup holds
+// half as many tiles), and the token block of a grouped launch whose
+// largest product has max_m tokens.
+int skinny_blocks(int64_t n, bool group_scales) {
+  return static_cast<int>(
+      ceil_div(ceil_div(n, kTileRows), group_scales ? kSkWavesGrouped / 2 : kSkWavesGrouped));
 }
 int skinny_batched_tokens(int max_m) {
   return max_m <= 32 ? SkCfg<1, kSkStages<1, true>, kSkWavesGrouped>::TOK

@@ -261,7 +261,7 @@ def test_skinny_validation_without_launch():
     total, max_m = sh.sherry_gemm_batched_prepare(descs)
     # one workgroup per 8 row tiles: 32 tiles -> 4, 128 -> 16, 2 -> 1
     assert [d.block_begin for d in descs] == [0, 4, 20] and total == 21 and max_m == 64
-    assert ctypes.sizeof(sh.sherry_gemm_desc) == 72
+    assert ctypes.sizeof(sh.sherry_gemm_desc) == 80
     # longer products run in 64-token blocks: 65 tokens -> 2 blocks of 16
     descs[1].m = 65
     total, max_m = sh.sherry_gemm_batched_prepare(descs)
@@ -359,3 +359,30 @@ def test_activation_table_kernel_validation_without_launch():
     # per-group scales have no activation-table variant
     assert L.sherry_gemm_group(FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, 64, 128, K,
                                None) == sh.SHERRY_E_INVALID
+
+
+def test_grouped_per_group_scales_validation():
+    cases = [(16, 2048, 2048), (100, 8192, 2048), (1, 70, 132)]
+    descs = (sh.sherry_gemm_desc * len(cases))()
+    for i, (m, n, k) in enumerate(cases):
+        d = descs[i]
+        d.w, d.x, d.x_scale, d.y, d.acc = FAKE, FAKE, FAKE, FAKE, None
+        d.m, d.n, d.k, d.w_scale = m, n, k, 0.02
+    descs[1].w_group_scales = FAKE
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    # a descriptor with per-group scales makes the launch run 32-token blocks
+    # and splits its tiles' K in two (4 tiles per workgroup):
+    # 32 tiles -> 4 x 1 block; 128 tiles -> 32 x 4 token blocks; 2 tiles -> 1
+    assert max_m == 32
+    assert [d.block_begin for d in descs] == [0, 4, 132] and total == 133
+    descs[1].acc = FAKE  # no int32 totals with per-group scales
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemm_batched_prepare(descs)
+    descs[1].acc = None
+    descs[1].w_scales = FAKE  # per-channel and per-group exclude each other
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemm_batched_prepare(descs)
+    descs[1].w_scales = None
+    descs[1].w_group_scales = FAKE + 2
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemm_batched_prepare(descs)

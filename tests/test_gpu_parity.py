@@ -818,6 +818,54 @@ def test_skinny_batched_any_m(dev):
         assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw))
 
 
+def test_skinny_batched_group_scales(dev):
+    # per-group descriptors (K split in two, 32-token blocks, no int32 totals)
+    # grouped with per-tensor and per-channel ones in one launch
+    sh = _sh()
+    _say("skinny batched group scales")
+    cases = [(5, 64, 128), (100, 257, 3076), (16, 600, 2048), (33, 130, 1028), (1, 70, 132),
+             (64, 512, 8192)]
+    descs = (sh.sherry_gemm_desc * len(cases))()
+    keep = []
+    for i, (m, n, k) in enumerate(cases):
+        t = synth.ternary_34(n, k, 61, "sg", i)
+        q = synth.int8_any(m, k, 61, "sgq", i)
+        sx = np.abs(synth.activations(1, m, 61, "sgs", i)[0]).astype(np.float32) + 0.01
+        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        qd, sxd = torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev)
+        y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+        a = torch.full((m, n), -7, dtype=torch.int32, device=dev)
+        d = descs[i]
+        d.w, d.x, d.x_scale, d.y = w.data_ptr(), qd.data_ptr(), sxd.data_ptr(), y.data_ptr()
+        d.n, d.k, d.m, d.w_scale = n, k, m, 0.03
+        extra = None
+        if i % 3 == 1 or i == 5:
+            gs = torch.from_numpy(_group_scales(n, k, 61 + i)).to(dev)
+            d.w_group_scales, d.acc, extra = gs.data_ptr(), None, ("groups", gs)
+        elif i % 3 == 2:
+            sw = torch.from_numpy(_channel_scales(n, 61 + i)).to(dev)
+            d.w_scales, d.acc, extra = sw.data_ptr(), a.data_ptr(), ("rows", sw)
+        else:
+            d.acc = a.data_ptr()
+        keep.append((t, q, sx, w, qd, sxd, y, a, extra))
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    assert max_m == 32
+    dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+    sh.sherry_gemm_batched(dd, len(cases), total, max_m)
+    torch.cuda.synchronize()
+    for t, q, sx, w, qd, sxd, y, a, extra in keep:
+        k = t.shape[1]
+        if extra and extra[0] == "groups":
+            y_ref, mag, _ = oracle.product_groups(q, t, sx, extra[1].cpu().numpy(), threads=8)
+            assert _group_ok(y.cpu().numpy(), y_ref, mag, k)
+            assert (a.cpu().numpy() == -7).all()  # no totals requested, none written
+        else:
+            acc_ref = oracle.gemm_i32(q, t, threads=8)
+            assert np.array_equal(a.cpu().numpy(), acc_ref)
+            sw = extra[1].cpu().numpy() if extra else 0.03
+            assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw))
+
+
 @pytest.mark.parametrize("spec_name,m", [("LLAMA_3B", 16), ("STRESS_8B", 64), ("LLAMA_3B", 2048)])
 def test_skinny_batched_model_step_sampled(dev, spec_name, m):
     # every linear of one layer of the model at M tokens in one grouped
