@@ -201,8 +201,8 @@ int sherry_gemm_channel(const uint8_t* w, const int8_t* x, const float* x_scale,
  * x_scale * sum_g |acc_g * scale| of the exact value, G = ceil(k/128)).
  * acc, if not NULL, receives sum_g acc_g (the unscaled int32 product).
  * kernel: SHERRY_KERNEL_AUTO (GEMV for m <= 4, else register-decoded),
- * SHERRY_KERNEL_GEMV (m <= 4) or SHERRY_KERNEL_SKINNY; the LDS-tiled kernel
- * has no per-group epilogue (SHERRY_E_INVALID).  SHERRY_E_INVALID if
+ * SHERRY_KERNEL_GEMV (m <= 4), SHERRY_KERNEL_SKINNY or SHERRY_KERNEL_MFMA
+ * (its 128 x 128 tile); SHERRY_E_INVALID for SHERRY_KERNEL_ALUT and if
  * w_group_scales is NULL. */
 int sherry_gemm_group(const uint8_t* w, const int8_t* x, const float* x_scale,
                       const float* w_group_scales, float* y, int32_t* acc, int64_t m,

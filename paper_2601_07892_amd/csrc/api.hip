@@ -163,7 +163,14 @@ extern "C" int sherry_gemm_group(const uint8_t* w, const int8_t* x, const float*
     return launch_skinny_group(w, x, x_scale, w_group_scales, y, acc, m, n, k,
                                as_stream(stream));
   }
-  return SHERRY_E_INVALID;  // the LDS-tiled kernel has no per-group epilogue
+  if (kernel == SHERRY_KERNEL_MFMA) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 16);
+    if (st != SHERRY_OK) return st;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_gemm_mfma_group(w, x, x_scale, w_group_scales, y, acc, m, n, k,
+                                  as_stream(stream));
+  }
+  return SHERRY_E_INVALID;
 }
 
 extern "C" int sherry_gemm_channel(const uint8_t* w, const int8_t* x, const float* x_scale,

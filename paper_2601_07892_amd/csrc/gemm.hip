@@ -73,11 +73,16 @@ __device__ __forceinline__ void decode_codes(const uint32_t (&d)[5], const uint3
 
 // kFullK: K % 128 == 0, every X chunk of a step is in its row, so all loads
 // are branch-free buffer loads (rows past M and units past N read as zero).
-template <class G, bool kFullK>
+// With GR, gs holds per-group scales ([N][C] fp32, one per row and K-step):
+// after each K-step's MFMAs the int32 accumulators are scaled into fp32 sums
+// (ascending K-steps) and cleared; y = x_scale * sum, acc_out the int32
+// totals.
+template <class G, bool kFullK, bool GR = false>
 __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
     const uint8_t* __restrict__ w, const int8_t* __restrict__ x,
     const float* __restrict__ x_scale, WScale ws, float* __restrict__ y,
-    int32_t* __restrict__ acc_out, int64_t M, int64_t N, int64_t K, int MT, int NT) {
+    int32_t* __restrict__ acc_out, int64_t M, int64_t N, int64_t K, int MT, int NT,
+    const float* __restrict__ gs = nullptr) {
   // LDS: the 32-entry code table at address 0 (table reads then need no base
   // in their address), then the two stages
   __shared__ __attribute__((aligned(16))) int8_t lds[kLutBytes + 2 * G::STAGE];
@@ -235,6 +240,47 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
     }
   };
 
+  // per-group: fp32 sums and int32 totals per accumulator element; lane's
+  // column of fragment bb
+  typedef float v16f __attribute__((ext_vector_type(16)));
+  v16f cf[GR ? G::FM : 1][GR ? G::FN : 1];
+  v16i tot[GR ? G::FM : 1][GR ? G::FN : 1];
+  float gcur[G::FN];
+  if constexpr (GR) {
+#pragma unroll
+    for (int a = 0; a < G::FM; ++a)
+#pragma unroll
+      for (int bb = 0; bb < G::FN; ++bb) {
+        cf[a][bb] = v16f{};
+        tot[a][bb] = v16i{};
+      }
+  }
+  // scale of K-step kk for each fragment column (0 past N)
+  auto load_scales = [&](int64_t kk) {
+    if constexpr (GR) {
+#pragma unroll
+      for (int bb = 0; bb < G::FN; ++bb) {
+        const int64_t col = n0 + wc * G::WN + bb * 32 + frow;
+        gcur[bb] = col < N ? gs[col * C + kk] : 0.0f;
+      }
+    }
+  };
+  auto flush = [&]() {
+    if constexpr (GR) {
+#pragma unroll
+      for (int a = 0; a < G::FM; ++a)
+#pragma unroll
+        for (int bb = 0; bb < G::FN; ++bb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            cf[a][bb][e] = __builtin_fmaf(static_cast<float>(acc[a][bb][e]), gcur[bb],
+                                          cf[a][bb][e]);
+            tot[a][bb][e] += acc[a][bb][e];
+            acc[a][bb][e] = 0;
+          }
+    }
+  };
+
   load_step(0);
   __syncthreads();  // lut ready
   store_step(smem);
@@ -256,9 +302,11 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
       __builtin_amdgcn_sched_barrier(0);
       load_step(ks + 2);
     }
+    load_scales(ks);
     __builtin_amdgcn_sched_barrier(0);
     compute(smem + (ks & 1) * G::STAGE);
     __builtin_amdgcn_sched_barrier(0);
+    flush();
     if (mfma_first) {
       store_step(smem + ((ks + 1) & 1) * G::STAGE);
       __builtin_amdgcn_sched_barrier(0);
@@ -268,11 +316,15 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
   }
   if (ks + 1 < C) {
     store_step(smem + ((ks + 1) & 1) * G::STAGE);
+    load_scales(ks);
     compute(smem + (ks & 1) * G::STAGE);
+    flush();
     __syncthreads();
     ++ks;
   }
+  load_scales(ks);
   compute(smem + (ks & 1) * G::STAGE);
+  flush();
 
   // ---- epilogue, staged through LDS so that every lane stores 16 bytes of
   // one row and a wave writes whole rows.  Lane holds C[i][j] of fragment
@@ -289,41 +341,66 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
   const bool vec = (N % 4 == 0) && (reinterpret_cast<uintptr_t>(y) % 16 == 0) &&
                    (!acc_out || reinterpret_cast<uintptr_t>(acc_out) % 16 == 0);
   constexpr int RP = G::WN / 4;  // 16-byte pieces per strip row
+  // pass 0 writes y (and, without per-group scales, the int32 sums); with
+  // per-group scales pass 0 stages the fp32 sums and pass 1 the int32 totals
+  const int passes = (GR && acc_out) ? 2 : 1;
+  for (int pass = 0; pass < passes; ++pass) {
 #pragma unroll
-  for (int a = 0; a < G::FM; ++a) {
+    for (int a = 0; a < G::FM; ++a) {
 #pragma unroll
-    for (int bb = 0; bb < G::FN; ++bb)
+      for (int bb = 0; bb < G::FN; ++bb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        strip[(8 * (r >> 2) + 4 * fhalf + (r & 3)) * SW + bb * 32 + frow] = acc[a][bb][r];
-    __asm__ volatile("" ::: "memory");
+        for (int r = 0; r < 16; ++r) {
+          int32_t v;
+          if constexpr (GR) {
+            const float f = cf[a][bb][r];  // copied out: a vector element is not bit-cast in place
+            v = pass == 0 ? __float_as_int(f) : tot[a][bb][r];
+          } else {
+            v = acc[a][bb][r];
+          }
+          strip[(8 * (r >> 2) + 4 * fhalf + (r & 3)) * SW + bb * 32 + frow] = v;
+        }
+      __asm__ volatile("" ::: "memory");
 #pragma unroll
-    for (int i = 0; i < 32 * RP / 64; ++i) {
-      const int p = lane + 64 * i;
-      const int row = p / RP, c4 = p % RP;
-      const v4i v = *reinterpret_cast<const v4i*>(strip + row * SW + 4 * c4);
-      const int64_t gm = m0 + wr * G::WM + a * 32 + row;
-      const int64_t gn = n0 + wc * G::WN + 4 * c4;
-      if (gm >= M || gn >= N) continue;
-      const float sx = x_scale[gm];
-      if (vec) {
-        const float4 o = make_float4(static_cast<float>(v.x) * (sx * ws.at(gn)),
-                                     static_cast<float>(v.y) * (sx * ws.at(gn + 1)),
-                                     static_cast<float>(v.z) * (sx * ws.at(gn + 2)),
-                                     static_cast<float>(v.w) * (sx * ws.at(gn + 3)));
-        *reinterpret_cast<float4*>(y + gm * N + gn) = o;
-        if (acc_out) *reinterpret_cast<v4i*>(acc_out + gm * N + gn) = v;
-      } else {
+      for (int i = 0; i < 32 * RP / 64; ++i) {
+        const int p = lane + 64 * i;
+        const int row = p / RP, c4 = p % RP;
+        const v4i v = *reinterpret_cast<const v4i*>(strip + row * SW + 4 * c4);
+        const int64_t gm = m0 + wr * G::WM + a * 32 + row;
+        const int64_t gn = n0 + wc * G::WN + 4 * c4;
+        if (gm >= M || gn >= N) continue;
         const int32_t vv[4] = {v.x, v.y, v.z, v.w};
+        if (GR && pass == 1) {  // int32 totals only
+          if (vec) {
+            *reinterpret_cast<v4i*>(acc_out + gm * N + gn) = v;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (gn + e < N) acc_out[gm * N + gn + e] = vv[e];
+          }
+          continue;
+        }
+        const float sx = x_scale[gm];
+        float o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          if (gn + e >= N) break;
-          y[gm * N + gn + e] = static_cast<float>(vv[e]) * (sx * ws.at(gn + e));
-          if (acc_out) acc_out[gm * N + gn + e] = vv[e];
+          if constexpr (GR) o[e] = __int_as_float(vv[e]) * sx;
+          else o[e] = static_cast<float>(vv[e]) * (sx * ws.at(gn + e));
+        }
+        if (vec) {
+          *reinterpret_cast<float4*>(y + gm * N + gn) = make_float4(o[0], o[1], o[2], o[3]);
+          if (!GR && acc_out) *reinterpret_cast<v4i*>(acc_out + gm * N + gn) = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (gn + e >= N) break;
+            y[gm * N + gn + e] = o[e];
+            if (!GR && acc_out) acc_out[gm * N + gn + e] = vv[e];
+          }
         }
       }
+      __asm__ volatile("" ::: "memory");  // the next strip overwrites these reads
     }
-    __asm__ volatile("" ::: "memory");  // the next strip overwrites these reads
   }
 }
 
@@ -335,9 +412,9 @@ int launch_cfg(const uint8_t* w, const int8_t* x, const float* x_scale, WScale w
   const dim3 grid(static_cast<unsigned>(MT) * NT), block(G::THREADS);
   if (k % kBK == 0)
     return launch(gemm_kernel<G, true>, grid, block, 0, s, w, x, x_scale, ws, y, acc, m, n,
-                  k, MT, NT);
+                  k, MT, NT, static_cast<const float*>(nullptr));
   return launch(gemm_kernel<G, false>, grid, block, 0, s, w, x, x_scale, ws, y, acc, m, n, k,
-                MT, NT);
+                MT, NT, static_cast<const float*>(nullptr));
 }
 
 using CfgLarge = GemmCfg<256, 256, 2, 4, 512>;  // wave block 128 x 64
@@ -363,6 +440,23 @@ int gemm_config_for(int64_t m, int64_t n) {
                 cs = gemm_cost<CfgSmall>(m, n);
   if (cl <= cm && cl <= cs) return 3;
   return cm <= cs ? 2 : 1;
+}
+
+// Per-group scales: the 128 x 128 tile (its fp32 sums and int32 totals fit
+// beside the accumulators).
+int launch_gemm_mfma_group(const uint8_t* w, const int8_t* x, const float* x_scale,
+                           const float* gs, float* y, int32_t* acc, int64_t m, int64_t n,
+                           int64_t k, hipStream_t s) {
+  using G = CfgSmall;
+  const int MT = static_cast<int>(ceil_div(m, G::BM));
+  const int NT = static_cast<int>(ceil_div(n, G::BN));
+  const dim3 grid(static_cast<unsigned>(MT) * NT), block(G::THREADS);
+  const WScale none{nullptr, 0.0f};
+  if (k % kBK == 0)
+    return launch(gemm_kernel<G, true, true>, grid, block, 0, s, w, x, x_scale, none, y, acc, m,
+                  n, k, MT, NT, gs);
+  return launch(gemm_kernel<G, false, true>, grid, block, 0, s, w, x, x_scale, none, y, acc, m,
+                n, k, MT, NT, gs);
 }
 
 int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,

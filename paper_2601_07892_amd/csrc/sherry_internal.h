@@ -198,6 +198,9 @@ int launch_skinny_group(const uint8_t* w, const int8_t* x, const float* x_scale,
 // MFMA tile configuration chosen for an m x n product: 0 skinny (32 x 256),
 // 1 small (128 x 128), 2 mid (128 x 256), 3 large (256 x 256).
 int gemm_config_for(int64_t m, int64_t n);
+int launch_gemm_mfma_group(const uint8_t* w, const int8_t* x, const float* x_scale,
+                           const float* gs, float* y, int32_t* acc, int64_t m, int64_t n,
+                           int64_t k, hipStream_t s);
 int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale,
                      WScale ws, float* y, int32_t* acc, int64_t m,
                      int64_t n, int64_t k, hipStream_t s);

@@ -318,7 +318,11 @@ def test_group_validation_without_launch():
              None) == sh.SHERRY_E_INVALID
     assert g(FAKE, FAKE, FAKE, FAKE + 2, FAKE, None, 1, 64, 128, sh.SHERRY_KERNEL_AUTO,
              None) == sh.SHERRY_E_ALIGN
-    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 16, 64, 128, sh.SHERRY_KERNEL_MFMA,
+    assert g(FAKE, FAKE + 4, FAKE, FAKE, FAKE, None, 16, 64, 128, sh.SHERRY_KERNEL_MFMA,
+             None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 2, 16, 64, 128, sh.SHERRY_KERNEL_MFMA,
+             None) == sh.SHERRY_E_ALIGN
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, 64, 128, sh.SHERRY_KERNEL_ALUT,
              None) == sh.SHERRY_E_INVALID
     assert g(FAKE, FAKE, FAKE, FAKE, FAKE, None, 5, 64, 128, sh.SHERRY_KERNEL_GEMV,
              None) == sh.SHERRY_E_SHAPE

@@ -1024,11 +1024,13 @@ def _group_ok(y, y_ref, mag, k):
     return bool(np.all(np.abs(np.asarray(y, np.float64) - y_ref) <= bound))
 
 
-# GEMV (m <= 4) and the register-decoded kernel (32-token blocks, K split in
-# 2, 4 or 8) with ragged n, a partial last group, and the int32 totals
+# GEMV (m <= 4), the register-decoded kernel (32-token blocks, K split in
+# 2, 4 or 8) and the LDS-tiled kernel (128 x 128 tiles), with ragged n, a
+# partial last group, and the int32 totals
 GROUP_CASES = [(1, 70, 132, "GEMV"), (4, 600, 2048, "GEMV"), (3, 300, 8196, "GEMV"),
                (5, 64, 128, "SKINNY"), (33, 130, 1028, "SKINNY"), (100, 257, 3076, "SKINNY"),
-               (17, 3072, 8192, "SKINNY")]
+               (17, 3072, 8192, "SKINNY"), (5, 64, 128, "MFMA"), (33, 130, 1028, "MFMA"),
+               (300, 520, 2052, "MFMA"), (256, 1024, 3072, "MFMA"), (130, 200, 8196, "MFMA")]
 
 
 @pytest.mark.parametrize("m,n,k,kernel", GROUP_CASES)
