@@ -247,7 +247,7 @@ int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
 /* Grouped products: many independent products (any m, e.g. the q, k and  */
 /* v projections of one layer) in one launch, on the register-decoded      */
 /* kernel (SHERRY_KERNEL_SKINNY); products run in token blocks of 32 when  */
-/* every m <= 32, else of 64.                                              */
+/* every m <= 32 or a descriptor has per-group scales, else of 64.        */
 /* ---------------------------------------------------------------------- */
 
 typedef struct sherry_gemm_desc {
