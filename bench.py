@@ -437,9 +437,10 @@ def bench_model_step(sh, torch, dev, spec, seed, copies, steps=100):
     return out
 
 
-def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20):
+def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20, group_scales=False):
     """All linears of the model at M tokens in one grouped launch
-    (sherry_gemm_batched, small-M MFMA kernel), int8 activations ready."""
+    (sherry_gemm_batched, small-M MFMA kernel), int8 activations ready; with
+    group_scales every product carries per-group (128 along K) scales."""
     lins = synth.model_linears(spec)
     host = [sh.sherry_pack(synth.ternary_34(l.n, l.k, seed, "w", layer, l.name))
             for layer, l in lins]
@@ -450,15 +451,19 @@ def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20):
         q = {kk: torch.randint(-127, 128, (m, kk), dtype=torch.int8, device=dev) for kk in ks}
         sx = torch.full((m,), 0.01, dtype=torch.float32, device=dev)
         ys = [torch.empty((m, l.n), dtype=torch.float32, device=dev) for _, l in lins]
+        gsc = ([torch.full((l.n, (l.k + 127) // 128), 0.02, dtype=torch.float32, device=dev)
+                for _, l in lins] if group_scales else None)
         descs = (sh.sherry_gemm_desc * len(lins))()
         for i, (_, l) in enumerate(lins):
             d = descs[i]
             d.w, d.x, d.x_scale, d.y, d.acc = (w[i].data_ptr(), q[l.k].data_ptr(),
                                                sx.data_ptr(), ys[i].data_ptr(), None)
             d.n, d.k, d.m, d.w_scale = l.n, l.k, m, 0.02
+            if group_scales:
+                d.w_group_scales = gsc[i].data_ptr()
         total, max_m = sh.sherry_gemm_batched_prepare(descs)
         dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
-        sets.append((w, q, sx, ys, dd, total, max_m))
+        sets.append((w, q, sx, ys, dd, total, max_m, gsc))
     run = lambda i: sh.sherry_gemm_batched(sets[i % copies][4], len(lins), sets[i % copies][5],
                                            sets[i % copies][6])
     settle(run, torch, 0.02)
@@ -471,9 +476,12 @@ def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20):
     us = a.elapsed_time(b) / reps * 1e3
     wbytes = sum(int(p.size) for p in host)
     byts = wbytes + sum(m * l.k + 4 * m + 4 * m * l.n for _, l in lins)
+    if group_scales:
+        byts += sum(4 * l.n * ((l.k + 127) // 128) for _, l in lins)
     del sets
     torch.cuda.empty_cache()
-    return {"m": m, "products": len(lins), "step_us": round(us, 2), "bytes_per_step": byts,
+    return {"m": m, "products": len(lins), "group_scales": group_scales,
+            "step_us": round(us, 2), "bytes_per_step": byts,
             "gbs": round(byts / (us * 1e-6) / 1e9, 1),
             "tops": round(sum(2.0 * m * l.n * l.k for _, l in lins) / (us * 1e-6) / 1e12, 1)}
 
@@ -719,6 +727,8 @@ def main():
         rows = [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2)
                 for mm in (4, 16)]
         rows.append(bench_model_step_m(sh, torch, dev, synth.STRESS_8B, args.seed, 64, 1))
+        rows += [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2,
+                                    group_scales=True) for mm in (4, 16)]
         print(json.dumps({"decode_small_m_grouped": rows}), flush=True)
         return
     if args.only == "tables":
@@ -817,7 +827,11 @@ def main():
         grouped = {"llama-3.2-3b": [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed,
                                                        mm, 2) for mm in (4, 16)],
                    "stress-8b": [bench_model_step_m(sh, torch, dev, synth.STRESS_8B, args.seed,
-                                                    64, 1)]}
+                                                    64, 1)],
+                   "llama-3.2-3b-group128": [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B,
+                                                                args.seed, mm, 2,
+                                                                group_scales=True)
+                                             for mm in (4, 16)]}
         for name, rows in grouped.items():
             for r in rows:
                 log("grouped step %s M=%d: %.2f us, %.0f GB/s, %.1f TOPS" %
