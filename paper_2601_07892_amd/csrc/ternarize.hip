@@ -3,20 +3,23 @@
 // channel out, with the same bytes as sherry_pack applied to the ternary
 // matrix of Eq. 4.
 //
-// Work mapping.  A workgroup owns RW rows (64, 32 or 16) of one 64-row tile
-// and all of their units; lane l of a wave is row l % RW and unit slot l / RW,
-// so a lane turns one row of one unit (128 weights) into its 16-byte head
-// and 4-byte tail directly.  Each lane reads its 128 values as 32 16-byte
-// loads (one block of 4 per load).  Fewer rows per workgroup give small-N
-// matrices more workgroups.  The kept magnitudes are summed in fp64 per
-// lane and the partial sums of each row are added in a fixed order.
+// Work mapping.  A workgroup owns ROWS rows (16, 8 or 4) of one 64-row tile
+// and every unit of them.  Its 32 * ROWS threads read the rows' weights one
+// unit at a time, 32 consecutive lanes per row, each lane one block of 4
+// (16 bytes): every wave load covers whole 512-byte row segments.  A lane
+// turns its block into a code (Eq. 4) and adds the kept magnitudes to its
+// fp64 partial sum.  The codes of 8 units go through LDS, and each unit row's
+// 32 codes are then packed by one lane into its 16-byte head and 4-byte tail.
+// Rows past n, blocks past k and units past the padded row read as zeros
+// (buffer loads past the row return zero) and so become code 0, the padding
+// code.  The alpha of a row (Eq. 5) adds its 32 lanes' partial sums in a
+// fixed order.
 #include "sherry_internal.h"
 
 namespace sherry {
 namespace {
 
-constexpr int kTpWaves = 8;
-constexpr int kTpThreads = 64 * kTpWaves;
+constexpr int kTpRound = 8;  // units in flight per round
 
 // Code of one block (Eq. 4): the smallest |w| is dropped (ties to the lowest
 // position); the other three keep their sign, +1 for a kept zero.  Adds the
@@ -49,54 +52,65 @@ __device__ __forceinline__ void tp_put(uint32_t (&d)[5], uint32_t code) {
 }
 
 template <int... js>
-__device__ __forceinline__ void tp_unit(const float* row_w, bool in, int64_t b0, int64_t nb,
-                                        uint32_t (&d)[5], double& kept,
+__device__ __forceinline__ void tp_pack(const uint8_t* codes, uint32_t (&d)[5],
                                         std::integer_sequence<int, js...>) {
-  (
-      [&] {
-        const int64_t b = b0 + js;
-        uint32_t code = 0;  // padding rows and blocks hold code 0
-        if (in && b < nb) {
-          const float4 v = *reinterpret_cast<const float4*>(as_global(row_w + 4 * b));
-          code = tp_block(v, kept);
-        }
-        tp_put<js>(d, code);
-      }(),
-      ...);
+  (tp_put<js>(d, codes[js]), ...);
 }
 
-template <int RW>
-__global__ __launch_bounds__(kTpThreads) void ternarize_pack_kernel(
+template <int ROWS>
+__global__ __launch_bounds__(32 * ROWS) void ternarize_pack_kernel(
     const float* __restrict__ w, int64_t n, int64_t k, uint8_t* __restrict__ out,
     float* __restrict__ alpha) {
-  constexpr int SLOTS = 64 / RW;  // units in flight per wave
-  __shared__ double red[kTpWaves * 64];
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t r = blockIdx.x / SLOTS;           // tile
-  const int ri = (blockIdx.x % SLOTS) * RW + lane % RW;  // row within the tile
-  const int64_t row = r * kTileRows + ri;
+  constexpr int THREADS = 32 * ROWS, WAVES = THREADS / 64;
+  constexpr int QUARTERS = kTileRows / ROWS;  // workgroups per tile
+  __shared__ __attribute__((aligned(16))) uint8_t codes[kTpRound][ROWS][32];
+  __shared__ double part[ROWS][32];
+  const int tid = threadIdx.x;
+  const int rl = tid >> 5, j = tid & 31;  // row of the workgroup, block of the unit
+  const int64_t tile = blockIdx.x / QUARTERS;
+  const int r0 = (blockIdx.x % QUARTERS) * ROWS;  // first row within the tile
+  const int64_t row = tile * kTileRows + r0 + rl;
   const int64_t C = (k + kTileK - 1) / kTileK, nb = k / 4;
   const bool in = row < n;
-  const float* row_w = w + (in ? row : 0) * k;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(w) + (in ? row : 0) * k, 0, in ? static_cast<int>(k * 4) : 0,
+      kBufferWord3);
   double kept = 0.0;
-  for (int64_t c = wave * SLOTS + lane / RW; c < C; c += kTpWaves * SLOTS) {
-    uint32_t d[5] = {0, 0, 0, 0, 0};
-    tp_unit(row_w, in, c * 32, nb, d, kept, std::make_integer_sequence<int, 32>{});
-    uint8_t* unit = out + (r * C + c) * kUnitBytes;
-    *reinterpret_cast<uint4*>(as_global_mut(unit + 16 * ri)) = make_uint4(d[0], d[1], d[2], d[3]);
-    *reinterpret_cast<uint32_t*>(as_global_mut(unit + kHeadBytes + 4 * ri)) = d[4];
+  for (int64_t c0 = 0; c0 < C; c0 += kTpRound) {
+    float4 v[kTpRound];
+#pragma unroll
+    for (int u = 0; u < kTpRound; ++u) {
+      const u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(
+          rs, static_cast<int>(((c0 + u) * 32 + j) * 16), 0, kLoadStream);
+      v[u] = make_float4(__uint_as_float(raw.x), __uint_as_float(raw.y), __uint_as_float(raw.z),
+                         __uint_as_float(raw.w));
+    }
+#pragma unroll
+    for (int u = 0; u < kTpRound; ++u) codes[u][rl][j] = static_cast<uint8_t>(tp_block(v[u], kept));
+    __syncthreads();
+    // unit c0 + u, row lane: one lane per unit row packs its 32 codes
+    const int wv = tid >> 6, lane = tid & 63;
+    for (int u = wv; u < kTpRound; u += WAVES) {
+      if (lane < ROWS && c0 + u < C) {
+        uint32_t d[5] = {0, 0, 0, 0, 0};
+        tp_pack(codes[u][lane], d, std::make_integer_sequence<int, 32>{});
+        uint8_t* unit = out + (tile * C + c0 + u) * kUnitBytes;
+        const int ri = r0 + lane;
+        *reinterpret_cast<uint4*>(as_global_mut(unit + 16 * ri)) = make_uint4(d[0], d[1], d[2], d[3]);
+        *reinterpret_cast<uint32_t*>(as_global_mut(unit + kHeadBytes + 4 * ri)) = d[4];
+      }
+    }
+    __syncthreads();  // the next round rewrites codes
   }
-  red[wave * 64 + lane] = kept;
+  part[rl][j] = kept;
   __syncthreads();
-  if (threadIdx.x < RW) {
-    const int64_t arow = r * kTileRows + (blockIdx.x % SLOTS) * RW + threadIdx.x;
+  if (tid < ROWS) {
+    const int64_t arow = tile * kTileRows + r0 + tid;
     if (arow < n && alpha) {
-      double s = 0.0;
-      for (int q = 0; q < kTpWaves * SLOTS; ++q)  // wave-major, then slot
-        s += red[(q / SLOTS) * 64 + (q % SLOTS) * RW + threadIdx.x];
+      double sum = 0.0;
+      for (int q = 0; q < 32; ++q) sum += part[tid][q];  // ascending block position
       // Eq. 5: mean |W| over the row's kept weights (three per block)
-      as_global_mut(alpha)[arow] = static_cast<float>(s / static_cast<double>(3 * nb));
+      as_global_mut(alpha)[arow] = static_cast<float>(sum / static_cast<double>(3 * nb));
     }
   }
 }
@@ -106,16 +120,16 @@ __global__ __launch_bounds__(kTpThreads) void ternarize_pack_kernel(
 int launch_ternarize_pack(const float* w, int64_t n, int64_t k, uint8_t* out, float* alpha,
                           hipStream_t s) {
   const int64_t R = ceil_div(n, kTileRows);
-  const dim3 block(kTpThreads);
-  // rows per workgroup: whole tiles when there are enough of them
-  if (R >= 256)
-    return launch(ternarize_pack_kernel<64>, dim3(static_cast<unsigned>(R)), block, 0, s, w, n,
-                  k, out, alpha);
-  if (R >= 128)
-    return launch(ternarize_pack_kernel<32>, dim3(static_cast<unsigned>(2 * R)), block, 0, s, w,
-                  n, k, out, alpha);
-  return launch(ternarize_pack_kernel<16>, dim3(static_cast<unsigned>(4 * R)), block, 0, s, w, n,
-                k, out, alpha);
+  // rows per workgroup: fewer for matrices with few tiles, so that there are
+  // enough workgroups to spread over the GPU
+  if (R >= 64)
+    return launch(ternarize_pack_kernel<16>, dim3(static_cast<unsigned>(4 * R)), dim3(512), 0, s,
+                  w, n, k, out, alpha);
+  if (R >= 16)
+    return launch(ternarize_pack_kernel<8>, dim3(static_cast<unsigned>(8 * R)), dim3(256), 0, s,
+                  w, n, k, out, alpha);
+  return launch(ternarize_pack_kernel<4>, dim3(static_cast<unsigned>(16 * R)), dim3(128), 0, s, w,
+                n, k, out, alpha);
 }
 
 }  // namespace sherry
