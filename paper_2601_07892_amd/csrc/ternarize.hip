@@ -9,7 +9,8 @@
 // (16 bytes): every wave load covers whole 512-byte row segments.  A lane
 // turns its block into a code (Eq. 4) and adds the kept magnitudes to its
 // fp64 partial sum.  The codes of 8 units go through LDS, and each unit row's
-// 32 codes are then packed by one lane into its 16-byte head and 4-byte tail.
+// 32 codes are then packed by one lane into its 16-byte head and 4-byte tail,
+// while the next 8 units' loads are in flight.
 // Rows past n, blocks past k and units past the padded row read as zeros
 // (buffer loads past the row return zero) and so become code 0, the padding
 // code.  The alpha of a row (Eq. 5) adds its 32 lanes' partial sums in a
@@ -76,8 +77,8 @@ __global__ __launch_bounds__(32 * ROWS) void ternarize_pack_kernel(
       const_cast<float*>(w) + (in ? row : 0) * k, 0, in ? static_cast<int>(k * 4) : 0,
       kBufferWord3);
   double kept = 0.0;
-  for (int64_t c0 = 0; c0 < C; c0 += kTpRound) {
-    float4 v[kTpRound];
+  float4 v[kTpRound];
+  auto load_round = [&](int64_t c0) {
 #pragma unroll
     for (int u = 0; u < kTpRound; ++u) {
       const u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(
@@ -85,8 +86,13 @@ __global__ __launch_bounds__(32 * ROWS) void ternarize_pack_kernel(
       v[u] = make_float4(__uint_as_float(raw.x), __uint_as_float(raw.y), __uint_as_float(raw.z),
                          __uint_as_float(raw.w));
     }
+  };
+  load_round(0);
+  for (int64_t c0 = 0; c0 < C; c0 += kTpRound) {
 #pragma unroll
     for (int u = 0; u < kTpRound; ++u) codes[u][rl][j] = static_cast<uint8_t>(tp_block(v[u], kept));
+    // the next round's loads fly while this round is packed
+    if (c0 + kTpRound < C) load_round(c0 + kTpRound);
     __syncthreads();
     // unit c0 + u, row lane: one lane per unit row packs its 32 codes
     const int wv = tid >> 6, lane = tid & 63;
