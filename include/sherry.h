@@ -177,8 +177,9 @@ int sherry_gemm_ex(const uint8_t* w, const int8_t* x, const float* x_scale,
 
 /* The kernel sherry_gemm picks for this shape, or -SHERRY_E_SHAPE for an
  * invalid shape: SHERRY_KERNEL_GEMV for m <= 4, SHERRY_KERNEL_SKINNY for
- * 5 <= m <= 512, for k > n, and for k >= 3072 with m <= 2048, else
- * SHERRY_KERNEL_MFMA (thresholds measured on the MI355X). */
+ * 5 <= m <= 8192, for k > n and for k >= 3072, else SHERRY_KERNEL_MFMA
+ * (longer products with k <= 2048 and k <= n; thresholds measured on the
+ * MI355X). */
 int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k);
 
 /* sherry_gemm_ex with one weight scale per output channel: the footnote to

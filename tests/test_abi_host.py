@@ -170,18 +170,16 @@ def test_kernel_choice_by_m():
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_GEMV
     for m in (5, 16, 32, 64, 65, 512):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_SKINNY
-    for m in (513, 2048):
+    # up to 8192 tokens every product is register-decoded
+    for m in (513, 2048, 8192):
+        for n, k in ((2048, 2048), (8192, 2048), (2048, 8192), (3072, 3072), (14336, 4096)):
+            assert sh.sherry_gemm_kernel_for(m, n, k) == sh.SHERRY_KERNEL_SKINNY
+    # longer products: the LDS-tiled kernel for k <= 2048 and k <= n
+    for m in (8193, 16384):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) == sh.SHERRY_KERNEL_MFMA
         assert sh.sherry_gemm_kernel_for(m, 8192, 2048) == sh.SHERRY_KERNEL_MFMA
-        # a longer K than N (down projections) stays register-decoded
         assert sh.sherry_gemm_kernel_for(m, 2048, 8192) == sh.SHERRY_KERNEL_SKINNY
-        # so do k >= 3072 shapes up to 2048 tokens
         assert sh.sherry_gemm_kernel_for(m, 3072, 3072) == sh.SHERRY_KERNEL_SKINNY
-        assert sh.sherry_gemm_kernel_for(m, 14336, 4096) == sh.SHERRY_KERNEL_SKINNY
-        assert sh.sherry_gemm_kernel_for(m, 8192, 3072) == sh.SHERRY_KERNEL_SKINNY
-    assert sh.sherry_gemm_kernel_for(2049, 3072, 3072) == sh.SHERRY_KERNEL_MFMA
-    assert sh.sherry_gemm_kernel_for(4096, 3072, 3072) == sh.SHERRY_KERNEL_MFMA
-    assert sh.sherry_gemm_kernel_for(2048, 3071 + 1, 2048) == sh.SHERRY_KERNEL_MFMA
     assert sh.sherry_gemm_kernel_for(0, 2048, 2048) == -sh.SHERRY_E_SHAPE
 
 
