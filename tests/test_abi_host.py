@@ -388,3 +388,18 @@ def test_grouped_per_group_scales_validation():
     descs[1].w_group_scales = FAKE + 2
     with pytest.raises(sh.SherryError):
         sh.sherry_gemm_batched_prepare(descs)
+
+
+def test_import_fails_loudly_without_the_library(tmp_path):
+    # no CPU fallback: a copy of the package without libsherry.so refuses to
+    # import
+    import shutil
+    import subprocess
+    import sys
+    pkg = os.path.dirname(sh.__file__)
+    dst = tmp_path / "paper_2601_07892_amd"
+    shutil.copytree(pkg, dst, ignore=shutil.ignore_patterns("*.so", "__pycache__", "csrc"))
+    r = subprocess.run([sys.executable, "-c", "import paper_2601_07892_amd"], cwd=tmp_path,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "not built" in r.stderr
