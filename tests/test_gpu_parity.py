@@ -261,6 +261,29 @@ def test_activation_table_matches_weight_table_kernel(dev):
     assert np.array_equal(aa, ag) and np.array_equal(ya, yg)
 
 
+@pytest.mark.parametrize("m,kernel", [(1, "GEMV"), (4, "GEMV"), (5, "SKINNY"), (40, "SKINNY"),
+                                      (64, "MFMA")])
+def test_longest_k(dev, m, kernel):
+    # k = SHERRY_MAX_K with the largest sums the bound allows: x = -128 against
+    # rows of +1 (code 0) reach 128 * 3K/4 = 16,773,120 < 2^24, still exact in
+    # fp32; other rows are random
+    sh = _sh()
+    n, k = 70, sh.SHERRY_MAX_K
+    _say("longest k", m, kernel)
+    t = synth.ternary_34(n, k, 45, "lk")
+    t[0] = np.tile(np.array([0, 1, 1, 1], np.int8), k // 4)
+    t[1] = -t[0]
+    q = synth.int8_any(m, k, 45, "lkq")
+    q[0] = -128
+    sx = np.full(m, 0.5, np.float32)
+    y, acc = _run(dev, t, q, sx, 0.25, getattr(sh, "SHERRY_KERNEL_" + kernel), m)
+    acc_ref = oracle.gemm_i32(q, t, threads=8)
+    assert acc_ref[0, 0] == -128 * 3 * (k // 4) and acc_ref[0, 1] == 128 * 3 * (k // 4)
+    assert np.array_equal(acc, acc_ref)
+    # exact scales: y = acc / 8 exactly
+    assert np.array_equal(y.astype(np.float64), acc.astype(np.float64) * 0.125)
+
+
 # The MFMA tile configuration follows from (m, n): m <= 32 -> 32x256; else
 # the cheapest of 256x256, 128x256, 128x128 by rounds of 256 workgroups x
 # tile area.  These are the M = 2048 prefill shapes of LLaMA-3.2-3B (the
