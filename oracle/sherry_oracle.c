@@ -38,6 +38,11 @@
  *                         weight per 2 bits), used only as a bytes-moved
  *                         comparison; layout is this project's own.
  *
+ *  Parity unpinned: the bit assignment inside a code (i) and the placement of
+ *  the codes in the stream (ii).  The paper prints no packed example, so the
+ *  tests pin them only to the written reading (a hand-written code table and
+ *  hand-derived byte fixtures under tests/golden), not to the paper.
+ *
  * Build: gcc -O2 -std=c11 -fPIC -shared -ffp-contract=off -pthread.
  */
 #include <math.h>
