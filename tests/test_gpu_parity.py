@@ -1112,3 +1112,60 @@ def test_gemv_f32_group_parity(dev, n, k):
     y_ref, mag, acc_ref = oracle.product_groups(q, t, sx, gs, threads=8)
     assert np.array_equal(acc.cpu().numpy(), acc_ref)
     assert _group_ok(y.cpu().numpy(), y_ref, mag, k)
+
+
+def test_graph_replay_matches_eager(dev):
+    # the kernels launched from a captured HIP graph, replayed several times
+    # with eager work and synchronisation in between: every replay must give
+    # the eager results (fused grouped decode, register-decoded and LDS-tiled
+    # products, quantization)
+    sh = _sh()
+    _say("graph replay")
+    shapes = [(512, 2048), (2048, 2048), (300, 8192)]
+    fd = _fused_batched(dev, shapes, 71)  # eager run, outputs checked elsewhere
+    descs = (sh.sherry_gemv_f32_desc * len(shapes))()
+    for i, (t, x, sw, w, xd, sxd, y, a) in enumerate(fd):
+        d = descs[i]
+        d.w, d.x, d.x_scale, d.y, d.acc = (w.data_ptr(), xd.data_ptr(), sxd.data_ptr(),
+                                           y.data_ptr(), a.data_ptr())
+        d.n, d.k, d.w_scale = t.shape[0], t.shape[1], sw
+    total = sh.sherry_gemv_f32_batched_prepare(descs)
+    ddev = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+    m, n, k = 96, 520, 2052
+    tt = synth.ternary_34(n, k, 72, "gr")
+    wq = torch.from_numpy(sh.sherry_pack(tt)).to(dev)
+    xf = torch.from_numpy(synth.activations(m, k, 72, "grx")).to(dev)
+    qd = torch.empty((m, k), dtype=torch.int8, device=dev)
+    sxd2 = torch.empty(m, dtype=torch.float32, device=dev)
+    y1 = torch.empty((m, n), dtype=torch.float32, device=dev)
+    y2 = torch.empty((m, n), dtype=torch.float32, device=dev)
+
+    def work():
+        sh.sherry_gemv_f32_batched(ddev, len(shapes), total)
+        sh.sherry_quantize_act(xf, qd, sxd2)
+        sh.sherry_gemm_ex(wq, qd, sxd2, 0.02, y1, None, m, n, k, sh.SHERRY_KERNEL_SKINNY)
+        sh.sherry_gemm_ex(wq, qd, sxd2, 0.02, y2, None, m, n, k, sh.SHERRY_KERNEL_MFMA)
+
+    work()
+    torch.cuda.synchronize()
+    ref = [v.clone() for v in [e[6] for e in fd] + [e[7] for e in fd] + [e[5] for e in fd]
+           + [qd, sxd2, y1, y2]]
+    outs = [e[6] for e in fd] + [e[7] for e in fd] + [e[5] for e in fd] + [qd, sxd2, y1, y2]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            work()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for o in outs:  # eager work between replays: poison every output
+            if o.dtype.is_floating_point:
+                o.fill_(float("nan"))
+            else:
+                o.fill_(-3)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for o, r in zip(outs, ref):
+            assert torch.equal(o, r), rep
