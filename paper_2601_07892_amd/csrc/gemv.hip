@@ -28,6 +28,8 @@ namespace {
 constexpr int kGemvThreads = 64 * kGemvWaves;
 constexpr int kRing = 3;  // containers per wave held in the register ring
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+
 template <int j0, int... js>
 __device__ __forceinline__ void group_offsets(const uint32_t (&d)[5], uint32_t* a4,
                                               std::integer_sequence<int, js...>) {
@@ -108,6 +110,43 @@ __device__ __forceinline__ void dot_container_lds(const uint32_t (&d)[5], const 
   }
 }
 
+// One token on the matrix cores: decodes codes [g, g + 16) of a container and
+// accumulates them with v_mfma_i32_16x16x64_i8.  Lane 16b + t holds row
+// 16b + t of the tile, so the looked-up words of a 4-code chunk (16 weights)
+// are the B operand as they stand: column t, k block b.  The A operand is the
+// chunk's 16 activations in lane 16b + b (A row b, k block b) and zeros in
+// every other lane, so D[i][t] sums row 16i + t of the tile and nothing else
+// (rows i >= 4 of D stay zero).  Only the lanes with own set read the
+// activations at xv into xw; the other lanes' xw hold zeros throughout.  Two
+// accumulators take alternate chunks.
+template <int g>
+__device__ __forceinline__ void dot_container_mfma(const uint32_t (&d)[5], const u32x4* xv,
+                                                   bool own, u32x4 (&xw)[4], const uint32_t* lut,
+                                                   v4i (&acc)[2]) {
+  if constexpr (g < 32) {
+    __builtin_amdgcn_sched_barrier(0);
+    if (own) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xw[i] = xv[g / 4 + i];
+    }
+    uint32_t a4[16];
+    group_offsets<g>(d, a4, std::make_integer_sequence<int, 16>{});
+    uint32_t wv[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      wv[j] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + a4[j]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const v4i a = {static_cast<int>(xw[q].x), static_cast<int>(xw[q].y),
+                     static_cast<int>(xw[q].z), static_cast<int>(xw[q].w)};
+      const v4i b = {static_cast<int>(wv[4 * q]), static_cast<int>(wv[4 * q + 1]),
+                     static_cast<int>(wv[4 * q + 2]), static_cast<int>(wv[4 * q + 3])};
+      acc[q & 1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc[q & 1], 0, 0, 0);
+    }
+    dot_container_mfma<g + 16>(d, xv, own, xw, lut, acc);
+  }
+}
+
 // Activation source: the activation words of container c, read with scalar
 // loads (wave-uniform) into SGPRs; dot masks the words past K of a partial
 // last container.
@@ -137,6 +176,25 @@ struct XFromLds {
     dot_container_lds<0>(d, reinterpret_cast<const u32x4*>(xq + c * kTileK), lut, acc);
   }
 };
+
+// The same activations as the A operand of dot_container_mfma: lanes 16b + b
+// read container c's words from xq (exec-masked LDS reads of 4 lanes); the
+// other lanes' registers keep the zeros they start with.
+struct XFromLdsMfma {
+  const int8_t* xq;  // LDS, ceil(k/128)*128 bytes
+  mutable u32x4 xw[4] = {};
+  __device__ __forceinline__ void dot(const uint32_t (&d)[5], int c, const uint32_t* lut,
+                                      v4i (&acc)[2]) const {
+    const int lane = threadIdx.x & 63;
+    dot_container_mfma<0>(d, reinterpret_cast<const u32x4*>(xq + c * kTileK),
+                          (lane & 15) == (lane >> 4), xw, lut, acc);
+  }
+};
+
+template <class X>
+constexpr bool kMfmaSource = false;
+template <>
+constexpr bool kMfmaSource<XFromLdsMfma> = true;
 
 // Container c through a buffer resource spanning a wave's containers (reads
 // outside it return zero and never fault): 16-byte head at lane*16, 4-byte
@@ -173,10 +231,10 @@ __device__ __forceinline__ void ring_fill(uint32_t (&ring)[kRing][5], __amdgpu_b
   }
 }
 
-template <int M, class X>
+template <class X, class Acc>
 __device__ __forceinline__ void ring_run(uint32_t (&ring)[kRing][5], __amdgpu_buffer_rsrc_t r,
                                          int c0, int c1, const X& xsrc, const uint32_t* lut,
-                                         int32_t (&acc)[M]) {
+                                         Acc& acc) {
   const int lane = threadIdx.x & 63;
   const int n = c1 - c0;
   for (int i = 0; i < n; i += kRing) {
@@ -291,12 +349,23 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
 #pragma unroll
     for (int m = 0; m < M; ++m) accf[m] = 0.0f;
     ring_run_groups<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
+  } else if constexpr (kMfmaSource<X>) {
+    static_assert(M == 1 && !kGrp, "the matrix-core source serves one token");
+    v4i macc[2] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
+    ring_run(ring, range, c0, c1, xsrc, lut, macc);
+    // lane l < 16 holds rows l, 16 + l, 32 + l, 48 + l of the tile
+    if (lane < 16) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) red[wave * 64 + 16 * e + lane] = macc[0][e] + macc[1][e];
+    }
   } else {
-    ring_run<M>(ring, range, c0, c1, xsrc, lut, acc);
+    ring_run(ring, range, c0, c1, xsrc, lut, acc);
   }
 
+  if constexpr (!kMfmaSource<X>) {
 #pragma unroll
-  for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + lane] = acc[m];
+    for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + lane] = acc[m];
+  }
   if constexpr (kGrp) {
 #pragma unroll
     for (int m = 0; m < M; ++m) redf[(wave * M + m) * 64 + lane] = accf[m];
@@ -500,20 +569,26 @@ __device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, fl
                                             int8_t* xq, const float* gs = nullptr,
                                             float* redf = nullptr) {
   const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
+  // per-tensor and per-channel scales sum a tile row's containers in int32 on
+  // the matrix cores; per-group scales need each container's sum per lane
+  const auto xsrc = [&] {
+    if constexpr (kGrp) return XFromLds{xq};
+    else return XFromLdsMfma{xq};
+  }();
   if (kp <= 4 * kGemvThreads) {
-    gemv_block<1, kGrp>(w, XFromLds{xq},
+    gemv_block<1, kGrp>(w, xsrc,
                         QuantizeRow<1>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
                         n, k, g, S, lut, red, gs, redf);
   } else if (kp <= 16 * kGemvThreads) {
-    gemv_block<1, kGrp>(w, XFromLds{xq},
+    gemv_block<1, kGrp>(w, xsrc,
                         QuantizeRow<4>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
                         n, k, g, S, lut, red, gs, redf);
   } else if (kp <= 32 * kGemvThreads) {
-    gemv_block<1, kGrp>(w, XFromLds{xq},
+    gemv_block<1, kGrp>(w, xsrc,
                         QuantizeRow<8>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
                         n, k, g, S, lut, red, gs, redf);
   } else {
-    gemv_block<1, kGrp>(w, XFromLds{xq},
+    gemv_block<1, kGrp>(w, xsrc,
                         QuantizeRow<0>{x, k, kp, xq, part, x_scale, write_scale}, ws, y, acc,
                         n, k, g, S, lut, red, gs, redf);
   }
