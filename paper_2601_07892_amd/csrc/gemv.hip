@@ -17,7 +17,9 @@
 // Decode.  Per code: a funnel shift and mask (or one SDWA mask) give code*4,
 // one LDS read of the 32-entry table gives the int8x4 weights, one v_dot4 per
 // token accumulates x . w in int32.  The table holds one dword per code, so
-// any 64 lookups are free of bank conflicts.
+// any 64 lookups are free of bank conflicts.  The fused quantize + product
+// kernels (one token) accumulate on the matrix cores instead of with v_dot4
+// (dot_container_mfma).
 #include <utility>
 
 #include "sherry_internal.h"
