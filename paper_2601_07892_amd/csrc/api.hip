@@ -289,7 +289,8 @@ extern "C" int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int 
         (d.w_group_scales && !aligned(d.w_group_scales, 4)))
       return SHERRY_E_ALIGN;
     d.block_begin = static_cast<int32_t>(blocks);
-    blocks += gemv_blocks(d.n, d.k, kFusedTarget);
+    blocks += ceil_div(ceil_div(d.n, kTileRows) * fused_split(static_cast<int>(ceil_div(d.k, kTileK))),
+                       kGemvWaves);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
   }
   *total_blocks = blocks;

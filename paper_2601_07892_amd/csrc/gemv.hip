@@ -646,7 +646,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
   const sherry_gemv_f32_desc& d = descs[lo];
   const int k = static_cast<int>(d.k);
   const int C = (k + kTileK - 1) / kTileK;
-  const int S = gemv_split(C, kFusedTarget);
+  const int S = fused_split(C);
   if (d.w_group_scales) {
     fused_block<true>(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{nullptr, 0.0f}, d.y,
                       d.acc, d.n, k, blk - d.block_begin, S, lut, red, part, xq,

@@ -228,16 +228,17 @@ def test_fused_validation_without_launch():
     assert f(FAKE, FAKE + 4, FAKE, 1.0, FAKE, None, 64, 128, None) == sh.SHERRY_E_ALIGN
     assert f(FAKE, FAKE, FAKE + 2, 1.0, FAKE, None, 64, 128, None) == sh.SHERRY_E_ALIGN
     assert f(FAKE, FAKE, FAKE, 1.0, FAKE, FAKE + 2, 64, 128, None) == sh.SHERRY_E_ALIGN
-    shapes = [(2048, 2048), (8192, 2048), (2048, 8192)]
+    shapes = [(2048, 2048), (8192, 2048), (2048, 8192), (3072, 3072)]
     descs = (sh.sherry_gemv_f32_desc * len(shapes))()
     for i, (n, k) in enumerate(shapes):
         descs[i].w, descs[i].x, descs[i].x_scale, descs[i].y = FAKE, FAKE, None, FAKE
         descs[i].n, descs[i].k, descs[i].w_scale = n, k, 0.02
     total = sh.sherry_gemv_f32_batched_prepare(descs)
-    # fused workgroups are longer: C/S <= 16 containers per wave
-    assert [d.block_begin for d in descs] == [0, 4, 20] and total == 36
+    # fused workgroups are longer: C/S <= 16 containers per wave, and a row
+    # of up to 32 containers is not split (k = 3072: 24 containers, S = 1)
+    assert [d.block_begin for d in descs] == [0, 4, 20, 36] and total == 42
     assert ctypes.sizeof(sh.sherry_gemv_f32_desc) == 72
-    descs[2].k = 40000
+    descs[3].k = 40000
     with pytest.raises(sh.SherryError):
         sh.sherry_gemv_f32_batched_prepare(descs)
     assert L.sherry_gemv_f32_batched(None, 1, 1, None) == sh.SHERRY_E_INVALID
