@@ -689,8 +689,11 @@ def _fused_batched(dev, shapes, seed, with_scale=True, channel=False):
 
 def test_fused_batched_parity(dev):
     _say("fused batched")
+    # rows of 17-32 units run unsplit in one wave (3072: 24 units; 4000: a
+    # ragged 32nd unit), 2176 (17 units) is the shortest such row
     shapes = [(64, 128), (65, 132), (2048, 2048), (512, 2048), (300, 8192), (1, 4), (70, 1032),
-              (100, 8196), (65, 14336), (3, 32768)]
+              (100, 8196), (65, 14336), (3, 32768), (96, 3072), (33, 4000), (130, 2176),
+              (64, 4224)]
     for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 49):
         sx_ref, acc_ref, y_ref = _fused_ref(x, t, sw)
         assert sxd.cpu().numpy()[0] == sx_ref[0]
