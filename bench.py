@@ -119,8 +119,18 @@ class DecodeStep:
             for i in range(self.count):
                 fdescs[i].w_scales = self.channel_scales[i].data_ptr()
             fdev_ch = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
-            self.copies.append(dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total,
-                                    fdescs=fdev, ftotal=ftotal, fdescs_ch=fdev_ch))
+            cp = dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total,
+                      fdescs=fdev, ftotal=ftotal, fdescs_ch=fdev_ch)
+            if c == 0:
+                # the same fused step with int32 outputs as well (parity check)
+                accs = [torch.empty(lin.n, dtype=torch.int32, device=dev)
+                        for _, lin in self.lins]
+                for i in range(self.count):
+                    fdescs[i].w_scales = None
+                    fdescs[i].acc = accs[i].data_ptr()
+                cp["accs"] = accs
+                cp["fdescs_acc"] = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
+            self.copies.append(cp)
         torch.cuda.synchronize()
         self.total_blocks = self.copies[0]["total"]
         self.weight_bytes = sum(sh.sherry_packed_bytes(l.n, l.k) for _, l in self.lins)
@@ -276,7 +286,8 @@ def bench_product_only(step: DecodeStep, torch, launches):
 
 
 def bench_stream_ceiling(sh, torch, dev, nbytes=2 << 30, reps=20):
-    """Practical HBM read ceiling: 128-bit streaming read of 2 GiB."""
+    """Practical HBM read ceiling: a streaming read of 2 GiB with the loads the
+    products use for their weights (128-bit buffer loads, non-temporal)."""
     src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     sink = torch.empty(sh.sherry_stream_read_groups(nbytes), dtype=torch.int32, device=dev)
     for _ in range(3):
@@ -633,29 +644,130 @@ def bench_two_bit(sh, torch, dev, spec, seed, shapes=("q", "gate", "down"), reps
 # CPU baseline: the oracle on the host cores
 # ---------------------------------------------------------------------------
 
-def cpu_baseline(step: DecodeStep, min_seconds=10.0):
+def oracle_step(step: DecodeStep, threads: int):
+    """One full decode step on the CPU oracle: per product, the activation
+    quantization, the int32 product on the unpacked ternary matrix and the
+    fp64 epilogue.  Returns [(x_scale, acc, y)] in product order."""
     import oracle
-    threads = min(16, os.cpu_count() or 1)
-    xk = {kk: oracle.quantize_act(step.x_host[kk]) for kk in step.ks}
-    reps, t_total = 0, 0.0
-    while t_total < min_seconds and reps < 2000:
+    out = []
+    row = {kk: 0 for kk in step.ks}
+    for i, (_, lin) in enumerate(step.lins):
+        q, sx = oracle.quantize_act(step.x_host[lin.k][row[lin.k]:row[lin.k] + 1])
+        row[lin.k] += 1
+        acc = oracle.gemm_i32(q, step.t[i], threads=threads)
+        out.append((sx, acc, oracle.epilogue(acc, sx, step.scales[i])))
+    return out
+
+
+def host_cpu():
+    """Core counts and model of the host CPU the oracle runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    avail = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"nproc": os.cpu_count(), "available": avail, "model": model}
+
+
+def _time_oracle(step, threads, min_seconds, max_reps=2000):
+    reps, t_total, last = 0, 0.0, None
+    while (t_total < min_seconds or reps == 0) and reps < max_reps:
         t0 = time.perf_counter()
-        row = {kk: 0 for kk in step.ks}
-        for i, (_, lin) in enumerate(step.lins):
-            q, sx = oracle.quantize_act(step.x_host[lin.k][row[lin.k]:row[lin.k] + 1])
-            row[lin.k] += 1
-            acc = oracle.gemm_i32(q, step.t[i], threads=threads)
-            oracle.epilogue(acc, sx, step.scales[i])
+        last = oracle_step(step, threads)
         t_total += time.perf_counter() - t0
         reps += 1
-    del xk
-    per_step = t_total / reps
-    return {"value": round(step.fused_bytes / per_step / 1e9, 3),
-            "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": "%d full decode step(s) of the same workload (112 products of the "
-                      "16-layer LLaMA-3.2-1B linears, quantize + int32 product + fp64 "
-                      "epilogue); algorithmic bytes as the GPU line, the oracle reads "
-                      "T unpacked at 1 byte/weight; %.2f s per step" % (reps, per_step)}
+    return reps, t_total / reps, last
+
+
+def cpu_baseline(step: DecodeStep, min_seconds=10.0, single_seconds=5.0):
+    """The oracle as it stands, timed on the host over full decode steps of
+    the benchmark's workload: with one thread per core of this process's
+    share (at most 16, the host share of one GPU) and with one thread.
+    Returns the JSON record and the last step's results."""
+    cpu = host_cpu()
+    threads = max(1, min(16, cpu["available"] or 1))
+    reps, per_step, last = _time_oracle(step, threads, min_seconds)
+    reps1, per_step1, _ = _time_oracle(step, 1, single_seconds)
+    rec = {"value": round(step.fused_bytes / per_step / 1e9, 3),
+           "unit": "GB/s", "cores": threads, "kind": "oracle",
+           "sample": "%d full decode step(s) of the same workload (112 products of the "
+                     "16-layer LLaMA-3.2-1B linears, quantize + int32 product + fp64 "
+                     "epilogue), %d threads over output rows; algorithmic bytes as the GPU "
+                     "line, the oracle reads T unpacked at 1 byte/weight; %.3f s per step"
+                     % (reps, threads, per_step),
+           "single_thread": {"value": round(step.fused_bytes / per_step1 / 1e9, 4),
+                             "unit": "GB/s", "cores": 1, "steps": reps1,
+                             "s_per_step": round(per_step1, 3)},
+           "host": cpu}
+    return rec, last
+
+
+def step_parity(sh, step: DecodeStep, torch, ref):
+    """Checks the decode step against the oracle's results for the same
+    inputs: every fp32 output of the last timed launch of copy 0, then an
+    untimed launch of the same descriptors with int32 outputs (bit-exact)
+    and the activation scales it writes (bit-exact)."""
+    cp = step.copies[0]
+    torch.cuda.synchronize()
+    ys = [y.cpu().numpy() for y in cp["ys"]]
+    sh.sherry_gemv_f32_batched(cp["fdescs_acc"], step.count, cp["ftotal"])
+    torch.cuda.synchronize()
+    accs = [a.cpu().numpy() for a in cp["accs"]]
+    sxs = {kk: cp["sxs"][kk].cpu().numpy() for kk in step.ks}
+    row = {kk: 0 for kk in step.ks}
+    acc_ok = sx_ok = True
+    worst, outputs = 0.0, 0
+    for i, (_, lin) in enumerate(step.lins):
+        sx_ref, acc_ref, y_ref = ref[i]
+        acc_ok &= bool(np.array_equal(accs[i], acc_ref[0]))
+        sx_ok &= bool(sxs[lin.k][row[lin.k]] == sx_ref[0])
+        row[lin.k] += 1
+        yr = y_ref[0]
+        err = np.abs(ys[i].astype(np.float64) - yr)
+        nz = yr != 0
+        if (~nz & (err != 0)).any():
+            worst = float("inf")
+        elif nz.any():
+            worst = max(worst, float(np.max(err[nz] / np.abs(yr[nz]))))
+        outputs += lin.n
+    ok = acc_ok and sx_ok and worst <= 1e-5
+    return {"products": step.count, "outputs": outputs, "acc_bit_exact": acc_ok,
+            "x_scale_bit_exact": sx_ok, "y_max_rel_err": worst, "tolerance": 1e-5, "ok": ok,
+            "checked": "every y of the timed step (copy 0), every int32 accumulator and "
+                       "activation scale of one more launch of the same descriptors, "
+                       "against the CPU oracle on the same inputs"}
+
+
+def bench_config0(sh, torch, dev, seed, reps=3):
+    """The single-GEMV case: LLaMA-3.2-1B q_proj shape, M = 1, K = N = 2048,
+    per-tensor scale 0.02, fp32 N(0,1) activations quantized in the same
+    launch (sherry_gemv_f32); weights rotated over copies totalling more than
+    600 MB, launched from a captured graph."""
+    n = k = 2048
+    t = synth.ternary_34(n, k, seed, "c0", "q")
+    packed = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    nb = packed.numel()
+    ncp = -(-600_000_000 // nb) + 24
+    ws = [packed.clone() for _ in range(ncp)]
+    x = torch.from_numpy(synth.activations(1, k, seed, "c0x")[0]).to(dev)
+    sx = torch.empty(1, dtype=torch.float32, device=dev)
+    y = torch.empty(n, dtype=torch.float32, device=dev)
+    us = time_graph(lambda i: sh.sherry_gemv_f32(ws[i % ncp], x, sx, 0.02, y, None, n, k),
+                    reps * ncp, torch)
+    byts = nb + 4 * k + 4 + 4 * n
+    del ws, packed
+    torch.cuda.empty_cache()
+    return {"workload": "single GEMV, M=1, K=N=2048 (LLaMA-3.2-1B q_proj), sw=0.02, "
+                        "fused int8 quantization", "copies": ncp,
+            "working_set_mb": round(nb * ncp / 1e6, 1), "us": round(us, 3),
+            "bytes": byts, "gbs": round(byts / (us * 1e-6) / 1e9, 1),
+            "frac": round(byts / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "note": "one launch per GEMV; 665 KB per call, so launch latency dominates"}
 
 
 def load_traffic(src_hash: str):
@@ -803,10 +915,10 @@ def main():
         out["ternarize_pack"] = bench_ternarize(sh, torch, dev, args.seed)
         for r in out["ternarize_pack"]:
             log("ternarize+pack %s: %.1f us, %.0f GB/s" % (r["shape"], r["us"], r["gbs"]))
-        try:
-            out["hbm_read_ceiling_gbs"] = round(bench_stream_ceiling(sh, torch, dev), 1)
-        except Exception as e:  # pragma: no cover
-            log("ceiling probe failed:", e)
+        out["hbm_read_ceiling_gbs"] = round(bench_stream_ceiling(sh, torch, dev), 1)
+        out["config0_single_gemv"] = bench_config0(sh, torch, dev, args.seed)
+        log("config 0 single GEMV: %.2f us, %.0f GB/s" % (out["config0_single_gemv"]["us"],
+                                                       out["config0_single_gemv"]["gbs"]))
         pre = {}
         for name, spec in (("llama-3.2-3b", synth.LLAMA_3B), ("llama-3.2-1b", synth.LLAMA_1B)):
             pre[name] = bench_prefill(sh, torch, dev, spec, 2048, args.seed)
@@ -850,10 +962,15 @@ def main():
         for r in out["two_bit_vs_sherry_8b"]:
             log("8b %s: 1.25-bit %.2f us vs 2-bit %.2f us (bytes %.3f, time %.3f)" %
                 (r["proj"], r["sherry_us"], r["two_bit_us"], r["bytes_ratio"], r["time_ratio"]))
+    t0 = time.time()
     if not args.no_cpu:
-        t0 = time.time()
-        out["cpu_baseline"] = cpu_baseline(step)
+        out["cpu_baseline"], ref = cpu_baseline(step)
         log("cpu baseline %.1f s" % (time.time() - t0))
+    else:
+        ref = oracle_step(step, max(1, min(16, host_cpu()["available"] or 1)))
+    out["parity"] = step_parity(sh, step, torch, ref)
+    log("parity of the timed step against the oracle: %s (max rel err %.3g)" %
+        ("ok" if out["parity"]["ok"] else "FAILED", out["parity"]["y_max_rel_err"]))
     print(json.dumps(out), flush=True)
 
 

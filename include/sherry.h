@@ -355,8 +355,9 @@ int sherry_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,
 /* ---------------------------------------------------------------------- */
 
 /* Streaming-read ceiling probe: reads `bytes` (multiple of 16, src 16-byte
- * aligned) with 128-bit loads and writes one XOR checksum word per workgroup
- * to sink (device, uint32 [sherry_stream_read_groups(bytes)]). */
+ * aligned) with the loads the products use for their packed weights (128-bit
+ * buffer loads, non-temporal hint) and writes one XOR checksum word per
+ * workgroup to sink (device, uint32 [sherry_stream_read_groups(bytes)]). */
 int sherry_stream_read(const void* src, size_t bytes, uint32_t* sink,
                        void* stream);
 int64_t sherry_stream_read_groups(size_t bytes);

@@ -36,17 +36,15 @@ int check_fused(const uint8_t* w, const float* x, const float* x_scale, float* y
   return SHERRY_OK;
 }
 
-// Largest M the VALU decode kernel serves and the largest the small-M MFMA
-// kernel serves (measured on LLaMA-3.2-3B / 8B-scale projections, single
-// launches: the VALU kernel is faster up to 4 tokens, the small-M kernel up
-// to its limit of 64); above it the LDS-tiled MFMA kernel runs.
+// Largest M the VALU decode kernel serves: up to 4 tokens it is faster than
+// the register-decoded MFMA kernel (LLaMA-3.2-3B and 8B-scale projections,
+// single launches).
 constexpr int64_t kGemvMaxM = 4;
-// Above this many tokens the LDS-tiled kernel takes products with k <= n
-// (the register-decoded kernel keeps those with k > n): the faster of the two
-// on the LLaMA projection shapes at M = 1024 and 2048.
-constexpr int64_t kSkinnyMaxM = 512;
+// The register-decoded MFMA kernel takes every product of up to
+// kSkinnyMaxLongM tokens and every product with k > n or k >= kSkinnyMinLongK;
+// the LDS-tiled kernel keeps the longer products with k <= 2048 <= n (about
+// 5% faster on those shapes at 16384 tokens).
 constexpr int64_t kSkinnyMinLongK = 3072, kSkinnyMaxLongM = 8192;
-// Largest m of one product in a grouped small-M launch (one token block).
 
 int check_product(const uint8_t* w, const int8_t* x, const float* x_scale, float* y,
                   int64_t m, int64_t n, int64_t k, uintptr_t x_align) {
@@ -90,7 +88,7 @@ extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
   // measured: the register-decoded kernel is as fast or faster on every
   // LLaMA shape up to 8192 tokens and on every k >= 3072 shape; the LDS-tiled
   // kernel keeps the longer, k <= 2048 products (5% faster at 16384 tokens)
-  const bool skinny = m <= kSkinnyMaxM || k > n || k >= kSkinnyMinLongK || m <= kSkinnyMaxLongM;
+  const bool skinny = m <= kSkinnyMaxLongM || k > n || k >= kSkinnyMinLongK;
   return skinny ? SHERRY_KERNEL_SKINNY : SHERRY_KERNEL_MFMA;
 }
 

@@ -1,7 +1,8 @@
 // Register-decoded int8-MFMA product (Eq. 2), for any number of tokens:
 // the weight stream of the decode kernel, with the multiply-accumulate on
-// int8 MFMA.  Its first use is small M (a few to 128 tokens), where the
-// weights dominate the traffic; larger M runs as a grid of 128-token blocks.
+// int8 MFMA.  Its first use is small M (5 to a few dozen tokens), where the
+// weights dominate the traffic; larger M runs as a grid of token blocks (32
+// tokens for products of up to 32, else 64).
 //
 // Work mapping.  A workgroup is W = 8 waves; wave w owns 64-row tile
 // (W/S)g + w/S and part w%S of its containers along K (S = 1 unless a lone

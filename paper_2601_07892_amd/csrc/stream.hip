@@ -1,6 +1,8 @@
 // Streaming-read probe: the practical HBM read ceiling next to the 8 TB/s
-// specification.  Each workgroup reads a contiguous slice with 128-bit loads
-// and writes one XOR checksum word (so the loads cannot be elided).
+// specification, read the way the products read their packed weights: raw
+// 128-bit buffer loads with the non-temporal hint.  Each workgroup reads a
+// contiguous slice and writes one XOR checksum word (so the loads cannot be
+// elided).
 #include "sherry_internal.h"
 
 namespace sherry {
@@ -9,24 +11,24 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int64_t kSliceBytes = 256 * 1024;  // per workgroup
 
-__global__ __launch_bounds__(kThreads) void stream_read_kernel(const uint4* __restrict__ src,
-                                                               int64_t n16,
+__global__ __launch_bounds__(kThreads) void stream_read_kernel(const uint8_t* __restrict__ src,
+                                                               int64_t bytes,
                                                                uint32_t* __restrict__ sink) {
   __shared__ uint32_t part[kThreads / 64];
-  const int64_t per = kSliceBytes / 16;
-  const int64_t b = int64_t(blockIdx.x) * per;
-  const int64_t e = (b + per < n16) ? b + per : n16;
+  const int64_t b = int64_t(blockIdx.x) * kSliceBytes;
+  const int64_t len = (b + kSliceBytes < bytes) ? kSliceBytes : bytes - b;
+  // the resource spans exactly this slice: loads past it return zero
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(src) + b, 0, static_cast<int>(len), kBufferWord3);
   uint32_t h = 0;
-  int64_t i = b + threadIdx.x;
-  for (; i + 3 * kThreads < e; i += 4 * kThreads) {
-    const uint4 a = src[i], c = src[i + kThreads], d = src[i + 2 * kThreads],
-                f = src[i + 3 * kThreads];
+  const int v = 16 * static_cast<int>(threadIdx.x);
+  for (int off = 0; off < len; off += 4 * 16 * kThreads) {
+    const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(r, v, off, kLoadStream);
+    const u32x4 c = __builtin_amdgcn_raw_buffer_load_b128(r, v, off + 16 * kThreads, kLoadStream);
+    const u32x4 d = __builtin_amdgcn_raw_buffer_load_b128(r, v, off + 32 * kThreads, kLoadStream);
+    const u32x4 f = __builtin_amdgcn_raw_buffer_load_b128(r, v, off + 48 * kThreads, kLoadStream);
     h ^= a.x ^ a.y ^ a.z ^ a.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w ^ f.x ^ f.y ^
          f.z ^ f.w;
-  }
-  for (; i < e; i += kThreads) {
-    const uint4 a = src[i];
-    h ^= a.x ^ a.y ^ a.z ^ a.w;
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) h ^= __shfl_xor(h, off, 64);
@@ -44,8 +46,7 @@ int64_t stream_read_groups(size_t bytes) {
 int launch_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s) {
   const int64_t groups = stream_read_groups(bytes);
   return launch(stream_read_kernel, dim3(static_cast<unsigned>(groups)), dim3(kThreads),
-                     0, s, static_cast<const uint4*>(src), static_cast<int64_t>(bytes / 16),
-                     sink);
+                     0, s, static_cast<const uint8_t*>(src), static_cast<int64_t>(bytes), sink);
 }
 
 }  // namespace sherry

@@ -246,6 +246,76 @@ def test_quantize_hand_derived():
     assert sx[2] == 0.0 and not q[2].any()
 
 
+def _rne_f32(fr):
+    """The float32 nearest to the rational fr, ties to the even significand,
+    found exactly by comparing the three float32 neighbours as fractions."""
+    from fractions import Fraction
+    f = np.float32(float(fr))
+    best = None
+    for c in (np.nextafter(f, np.float32(-np.inf)), f, np.nextafter(f, np.float32(np.inf))):
+        odd = int(np.float32(c).view(np.uint32)) & 1
+        key = (abs(Fraction(float(c)) - fr), odd)
+        if best is None or key < best[0]:
+            best = (key, np.float32(c))
+    return best[1]
+
+
+def _rne_int(fr):
+    """Round a rational to the nearest integer, ties to even (exact)."""
+    from fractions import Fraction
+    fl = fr.numerator // fr.denominator
+    rest = fr - fl
+    return fl + 1 if rest > Fraction(1, 2) or (rest == Fraction(1, 2) and fl % 2) else fl
+
+
+def _q_division(x, s):
+    # the reading: the IEEE fp32 quotient x / s, then to the nearest integer
+    from fractions import Fraction
+    return _rne_int(Fraction(float(_rne_f32(Fraction(float(x)) / Fraction(float(s))))))
+
+
+def _q_reciprocal(x, s):
+    # a plausible wrong oracle: fp32 reciprocal of s, then an fp32 product
+    from fractions import Fraction
+    r = _rne_f32(1 / Fraction(float(s)))
+    return _rne_int(Fraction(float(_rne_f32(Fraction(float(x)) * Fraction(float(r))))))
+
+
+def test_quantize_ieee_division_at_inexact_scales():
+    # The reading of the quantizer takes the IEEE fp32 quotient x / s.  At a
+    # scale that is not a power of two, x * (1/s) rounds differently for some
+    # x; every expected code here is derived with exact rational arithmetic
+    # (the fp32 scale absmax/127 and the fp32 quotient both rounded exactly),
+    # independently of the oracle.  absmax 3, x = -2.7992127: s = 3/127
+    # rounded, x/s rounds to -118.5000... -> -119, x*(1/s) to -118.
+    from fractions import Fraction
+    x = np.array([[3.0, -2.7992127]], np.float32)
+    q, sx = oracle.quantize_act(x)
+    assert sx[0] == _rne_f32(Fraction(3) / 127)
+    assert list(q[0]) == [127, -119]
+    assert _q_reciprocal(np.float32(-2.7992127), sx[0]) == -118  # the pin discriminates
+    # rows at four inexact scales: absmax first, then values one or two ulps
+    # around half-integer multiples of the scale, where the two readings split
+    rng = np.random.default_rng(20260107)
+    found = 0
+    for amax in (3.0, 0.7, 11.3, 1e-3):
+        s = _rne_f32(Fraction(float(np.float32(amax))) / 127)
+        cands = []
+        for _ in range(400):
+            h = int(rng.integers(-126, 126)) + 0.5
+            v = np.float32(float(s) * h)
+            for _ in range(int(rng.integers(0, 3))):
+                v = np.nextafter(v, np.float32(np.inf) if rng.random() < 0.5 else np.float32(-np.inf))
+            cands.append(v)
+        row = np.array([np.float32(amax)] + cands, np.float32)[None, :]
+        q, sx = oracle.quantize_act(row)
+        assert sx[0] == s
+        want = [127] + [max(-127, min(127, _q_division(v, s))) for v in cands]
+        assert list(q[0].astype(int)) == want
+        found += sum(_q_division(v, s) != _q_reciprocal(v, s) for v in cands)
+    assert found >= 10  # the rows do separate the division from the reciprocal
+
+
 def test_quantize_properties():
     x = synth.activations(9, 1000, 8, "qp", outlier_frac=0.01)
     q, sx = oracle.quantize_act(x)
