@@ -709,12 +709,13 @@ def cpu_baseline(step: DecodeStep, min_seconds=10.0, single_seconds=5.0):
 
 def step_parity(sh, step: DecodeStep, torch, ref):
     """Checks the decode step against the oracle's results for the same
-    inputs: every fp32 output of the last timed launch of copy 0, then an
-    untimed launch of the same descriptors with int32 outputs (bit-exact)
-    and the activation scales it writes (bit-exact)."""
+    inputs: every fp32 output of the last timed launch of copy 0 (saved right
+    after the timed loop), then an untimed launch of the same descriptors
+    with int32 outputs (bit-exact) and the activation scales it writes
+    (bit-exact)."""
     cp = step.copies[0]
+    ys = step.timed_y
     torch.cuda.synchronize()
-    ys = [y.cpu().numpy() for y in cp["ys"]]
     sh.sherry_gemv_f32_batched(cp["fdescs_acc"], step.count, cp["ftotal"])
     torch.cuda.synchronize()
     accs = [a.cpu().numpy() for a in cp["accs"]]
@@ -863,6 +864,9 @@ def main():
                           "bytes_per_launch": step.gemv_bytes}), flush=True)
         return
     ms_step = bench_fused(step, torch, args.steps, args.warmup)
+    # the outputs of the timed steps (copy 0's last launch), before any other
+    # run writes the same buffers
+    step.timed_y = [y.cpu().numpy() for y in step.copies[0]["ys"]]
     value = step.fused_bytes / (ms_step * 1e-3) / 1e9
     log("decode step (fused quantize + product, one launch) %.2f us, %.0f GB/s" %
         (ms_step * 1e3, value))
