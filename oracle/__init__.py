@@ -23,6 +23,10 @@ Parity status of each piece (what pins it, in ``tests/test_oracle.py``):
 * ternarizer         -- pinned: brute force over all 32 patterns per block
                          (Appendix D) and least-squares alpha (Eq. 5);
 * 2-bit codec        -- pinned: hand-derived bytes and round trips.
+* 1.67-bit codec     -- pinned: hand-derived code table and bytes, 27 of the
+                         32 codes used (3^3 triples, Sec. 2.3), mirror
+                         code(-t) = 26 - code(t), rejection of the unused
+                         codes, round trips.
 """
 from __future__ import annotations
 
@@ -100,6 +104,16 @@ def lib():
         L.oracle_pack2.restype = i64
         L.oracle_unpack2.argtypes = [u8p, i64, i64, i8p]
         L.oracle_unpack2.restype = ctypes.c_int
+        L.oracle_code3_table.argtypes = [i8p]
+        L.oracle_code3_table.restype = ctypes.c_int
+        L.oracle_encode3.argtypes = [i8p]
+        L.oracle_encode3.restype = ctypes.c_int
+        L.oracle_packed3_bytes.argtypes = [i64, i64]
+        L.oracle_packed3_bytes.restype = i64
+        L.oracle_pack3.argtypes = [i8p, i64, i64, u8p]
+        L.oracle_pack3.restype = i64
+        L.oracle_unpack3.argtypes = [u8p, i64, i64, i8p]
+        L.oracle_unpack3.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -317,6 +331,43 @@ def unpack2(p: np.ndarray, n: int, k: int) -> np.ndarray:
     t = np.zeros((n, k), dtype=np.int8)
     if lib().oracle_unpack2(_p(p, ctypes.c_uint8), n, k, _p(t, ctypes.c_int8)) != 0:
         raise OracleError("bad 2-bit stream")
+    return t
+
+
+# ---- (viii) 1.67-bit layout (three weights per 5-bit code, Sec. 2.3) --------
+
+def code3_table():
+    """(27 x 3) int8 table: row c = the weights (t0, t1, t2) of code c, and
+    the count of codes the enumeration used."""
+    t = np.zeros((27, 3), dtype=np.int8)
+    used = lib().oracle_code3_table(_p(t, ctypes.c_int8))
+    return t, int(used)
+
+
+def encode3(w) -> int:
+    a = np.ascontiguousarray(np.asarray(w, dtype=np.int8))
+    return int(lib().oracle_encode3(_p(a, ctypes.c_int8)))
+
+
+def packed3_bytes(n: int, k: int) -> int:
+    return int(lib().oracle_packed3_bytes(n, k))
+
+
+def pack3(t: np.ndarray) -> np.ndarray:
+    t = np.ascontiguousarray(t, dtype=np.int8)
+    n, k = t.shape
+    out = np.zeros(packed3_bytes(n, k), dtype=np.uint8)
+    rc = lib().oracle_pack3(_p(t, ctypes.c_int8), n, k, _p(out, ctypes.c_uint8))
+    if rc != 0:
+        raise OracleError("bad weight at %d" % (-rc - 1))
+    return out
+
+
+def unpack3(p: np.ndarray, n: int, k: int) -> np.ndarray:
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    t = np.zeros((n, k), dtype=np.int8)
+    if lib().oracle_unpack3(_p(p, ctypes.c_uint8), n, k, _p(t, ctypes.c_int8)) != 0:
+        raise OracleError("bad 1.67-bit stream")
     return t
 
 

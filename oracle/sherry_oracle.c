@@ -37,6 +37,13 @@
  *  (vii) 2-bit codec   -- the "2-bit strategy" of Sec. 2.3 (one ternary
  *                         weight per 2 bits), used only as a bytes-moved
  *                         comparison; layout is this project's own.
+ *  (viii) 1.67-bit codec -- the "1.67-bit strategy" of Sec. 2.3: three
+ *                         ternary weights per 5-bit code, 3^3 = 27 of the 32
+ *                         codes used.  The digit order is this project's
+ *                         reading: code = (t0+1) + 3(t1+1) + 9(t2+1) for the
+ *                         weights t0, t1, t2 of a block in ascending K.
+ *                         Built by enumerating the 27 triples.  Comparison
+ *                         layout only.
  *
  *  Parity unpinned: the bit assignment inside a code (i) and the placement of
  *  the codes in the stream (ii).  The paper prints no packed example, so the
@@ -364,8 +371,10 @@ void oracle_ternarize_rows(const float* w, int64_t n, int64_t k, int8_t* t,
 /* Rows padded to ceil(N/64)*64, reduction dim to ceil(K/64)*64 (padding     */
 /* value 1, i.e. weight 0).  Unit (r, c) of 64 rows x 64 weights is 1024     */
 /* bytes at (r*C + c)*1024 with C = Kp/64; row i holds the 16 bytes at       */
-/* 16*i, a 128-bit little-endian word whose bits [2u, 2u+2) carry weight     */
-/* 64*c + u.                                                                 */
+/* 16*i.  Weight 64*c + u, u = 16*w + 4*j + p (w, j, p in 0..3), sits in     */
+/* byte 4*w + p of those 16, at bits [2j, 2j+2): byte p of 32-bit word w     */
+/* gathers the 2-bit fields of weights 16w + p, 16w + 4 + p, 16w + 8 + p and */
+/* 16w + 12 + p.                                                             */
 /* ------------------------------------------------------------------------ */
 
 int64_t oracle_packed2_bytes(int64_t n, int64_t k) {
@@ -376,9 +385,10 @@ int64_t oracle_packed2_bytes(int64_t n, int64_t k) {
 static int64_t two_bit_byte(int64_t row, int64_t kk, int q, int64_t C, int* bit) {
   int64_t r = row / 64, c = kk / 64;
   int i = (int)(row % 64);
-  int sb = 2 * (int)(kk % 64) + q;
-  *bit = sb % 8;
-  return (r * C + c) * 1024 + 16 * i + sb / 8;
+  int u = (int)(kk % 64);
+  int w = u / 16, j = (u % 16) / 4, p = u % 4;
+  *bit = 2 * j + q;
+  return (r * C + c) * 1024 + 16 * i + 4 * w + p;
 }
 
 int64_t oracle_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
@@ -418,6 +428,127 @@ int oracle_unpack2(const uint8_t* pk, int64_t n, int64_t k, int8_t* t) {
       }
       if (v > 2) return -2;
       t[row * k + kk] = (int8_t)(v - 1);
+    }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* (viii) 1.67-bit layout: three weights per 5-bit code, bit by bit         */
+/*                                                                          */
+/* The matrix is extended with zero weights to Np = ceil(N/64)*64 rows and   */
+/* Kp = ceil(K/96)*96 columns.  Block b of a row is weights 3b, 3b+1, 3b+2;  */
+/* its code is (t0+1) + 3*(t1+1) + 9*(t2+1) (0..26; an all-zero block is     */
+/* 13).  Unit (r, c) of 64 rows x 96 weights (32 codes per row) is 1280      */
+/* bytes at (r*C + c)*1280 with C = Kp/96; inside it the codes sit exactly   */
+/* as in the 5-bit layout (ii): row i's 160-bit stream holds code j of the   */
+/* unit (weights 96c + 3j .. 96c + 3j + 2) at stream bits [5j, 5j+5), stream */
+/* bits 0..127 in bytes 16*i + (0..15), bits 128..159 in 1024 + 4*i + (0..3).*/
+/* ------------------------------------------------------------------------ */
+
+static int8_t g_table3[27][3];
+static int g_table3_ready = 0;
+
+/* Fills table[code] = (t0, t1, t2) by enumerating every ternary triple;
+ * returns the number of codes used (27). */
+int oracle_code3_table(int8_t table[27][3]) {
+  int used = 0;
+  for (int t2 = -1; t2 <= 1; ++t2)
+    for (int t1 = -1; t1 <= 1; ++t1)
+      for (int t0 = -1; t0 <= 1; ++t0) {
+        int code = (t0 + 1) + 3 * (t1 + 1) + 9 * (t2 + 1);
+        table[code][0] = (int8_t)t0;
+        table[code][1] = (int8_t)t1;
+        table[code][2] = (int8_t)t2;
+        ++used;
+      }
+  return used;
+}
+
+static void ensure_table3(void) {
+  if (!g_table3_ready) {
+    oracle_code3_table(g_table3);
+    g_table3_ready = 1;
+  }
+}
+
+/* Code of a block of three weights, or -1 if a weight is not in {-1,0,1}. */
+int oracle_encode3(const int8_t w[3]) {
+  ensure_table3();
+  for (int c = 0; c < 27; ++c)
+    if (g_table3[c][0] == w[0] && g_table3[c][1] == w[1] && g_table3[c][2] == w[2]) return c;
+  return -1;
+}
+
+int64_t oracle_packed3_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1) return 0;
+  return ceil_to(n, 64) * (ceil_to(k, 96) / 96) * 20;
+}
+
+static void stream3_bit_addr(int64_t row, int64_t c, int sp, int64_t C, int64_t* byte,
+                             int* bit) {
+  int64_t r = row / 64;
+  int i = (int)(row % 64);
+  int64_t unit = (r * C + c) * 1280;
+  if (sp < 128) {
+    *byte = unit + 16 * i + sp / 8;
+    *bit = sp % 8;
+  } else {
+    *byte = unit + 1024 + 4 * i + (sp - 128) / 8;
+    *bit = (sp - 128) % 8;
+  }
+}
+
+/* Packs T (N x K, values in {-1,0,1}); returns 0, or -(e+1) for the flat
+ * index e (n*K + k) of the first weight outside {-1,0,1}. */
+int64_t oracle_pack3(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
+  int64_t bytes = oracle_packed3_bytes(n, k);
+  if (bytes == 0) return -((int64_t)1 << 62);
+  for (int64_t e = 0; e < n * k; ++e)
+    if (t[e] < -1 || t[e] > 1) return -(e + 1);
+  memset(out, 0, (size_t)bytes);
+  int64_t np = ceil_to(n, 64), kp = ceil_to(k, 96), C = kp / 96;
+  for (int64_t row = 0; row < np; ++row) {
+    for (int64_t b = 0; b < kp / 3; ++b) {
+      int8_t w[3];
+      for (int q = 0; q < 3; ++q) {
+        int64_t kk = 3 * b + q;
+        w[q] = (row < n && kk < k) ? t[row * k + kk] : 0;
+      }
+      int code = oracle_encode3(w);
+      int64_t c = (3 * b) / 96;
+      int j = (int)(b % 32);
+      for (int q = 0; q < 5; ++q) {
+        int64_t byte;
+        int bit;
+        stream3_bit_addr(row, c, 5 * j + q, C, &byte, &bit);
+        if ((code >> q) & 1) out[byte] |= (uint8_t)(1u << bit);
+      }
+    }
+  }
+  return 0;
+}
+
+/* Inverse of oracle_pack3 for the first n rows and k weights; returns -2 if
+ * a code read there is one of the five unused ones (27..31). */
+int oracle_unpack3(const uint8_t* p, int64_t n, int64_t k, int8_t* t) {
+  if (oracle_packed3_bytes(n, k) == 0) return -1;
+  ensure_table3();
+  int64_t C = ceil_to(k, 96) / 96;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t b = 0; b < (k + 2) / 3; ++b) {
+      int64_t c = (3 * b) / 96;
+      int j = (int)(b % 32);
+      int code = 0;
+      for (int q = 0; q < 5; ++q) {
+        int64_t byte;
+        int bit;
+        stream3_bit_addr(row, c, 5 * j + q, C, &byte, &bit);
+        code |= ((p[byte] >> bit) & 1) << q;
+      }
+      if (code > 26) return -2;
+      for (int q = 0; q < 3; ++q)
+        if (3 * b + q < k) t[row * k + 3 * b + q] = g_table3[code][q];
     }
   }
   return 0;

@@ -457,3 +457,107 @@ def test_ternarizer_ties_and_zeros():
     t, _ = oracle.ternarize(w)
     # ties for the smallest |W| go to the lowest position; a kept zero is +1
     assert list(t[0]) == [0, -1, 1, -1, 0, 1, 1, -1]
+
+
+# ------------------------------------------------ 1.67-bit comparison layout
+
+def _golden_table3():
+    rows = {}
+    with open(os.path.join(GOLDEN, "code3_table.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if not line:
+                continue
+            c, w = line.split()
+            rows[int(c)] = [SYM[ch] for ch in w]
+    return rows
+
+
+def test_code3_table_matches_hand_written_table():
+    g = _golden_table3()
+    assert sorted(g) == list(range(27))
+    t, used = oracle.code3_table()
+    # three weights in five bits: 3^3 = 27 of the 32 codes (Sec. 2.3)
+    assert used == 27 == 3 ** 3 and 2 ** 5 - used == 5
+    for c in range(27):
+        assert list(t[c]) == g[c], c
+    # every ternary triple has exactly one code, and it decodes back
+    seen = set()
+    for w in itertools.product((-1, 0, 1), repeat=3):
+        c = oracle.encode3(w)
+        assert 0 <= c < 27 and c not in seen
+        seen.add(c)
+        assert tuple(int(v) for v in t[c]) == w
+    assert oracle.encode3((2, 0, 0)) == -1 and oracle.encode3((0, 0, -2)) == -1
+
+
+def test_code3_mirror():
+    # negating a block maps code c to 26 - c (the digits t+1 become 2 - (t+1))
+    t, _ = oracle.code3_table()
+    for c in range(27):
+        assert np.array_equal(t[26 - c], -t[c])
+
+
+def _zero_row3():
+    fx = json.load(open(os.path.join(GOLDEN, "packed_fixtures.json")))["about_code3"]
+    head = bytes.fromhex(fx.split("head ")[1].split(",")[0].replace(" ", ""))
+    tail = bytes.fromhex(fx.split("tail ")[1].split(" (")[0].replace(" ", ""))
+    assert len(head) == 16 and len(tail) == 4
+    return head, tail
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2, 3])
+def test_pack3_hand_derived_bytes(idx):
+    with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
+        fx = json.load(f)["code3"][idx]
+    t = np.zeros((fx["n"], fx["k"]), np.int8)
+    for row, kk, w in fx["weights"]:
+        t[row, kk] = w
+    p = oracle.pack3(t)
+    assert p.size == fx["total_bytes"] == oracle.packed3_bytes(fx["n"], fx["k"])
+    head, tail = _zero_row3()
+    exp = np.zeros(fx["total_bytes"], np.uint8)
+    for unit in range(0, fx["total_bytes"], 1280):
+        for i in range(64):
+            exp[unit + 16 * i:unit + 16 * i + 16] = np.frombuffer(head, np.uint8)
+            exp[unit + 1024 + 4 * i:unit + 1024 + 4 * i + 4] = np.frombuffer(tail, np.uint8)
+    for a, b in fx["bytes"].items():
+        exp[int(a)] = b
+    assert np.array_equal(p, exp)
+    assert np.array_equal(oracle.unpack3(p, fx["n"], fx["k"]), t)
+
+
+def test_packed3_sizes_are_5_bits_per_3_weights():
+    # 5/3 bits per weight once rows and K fill whole units (64 x 96)
+    for n, k in [(64, 96), (3072, 3072), (1024, 3072), (4096, 14400), (128, 192)]:
+        assert oracle.packed3_bytes(n, k) * 24 == 5 * n * k
+    # padding: K = 2048 rounds up to 2112 (22 units of 96)
+    assert oracle.packed3_bytes(2048, 2048) == 2048 * 22 * 20
+    assert oracle.packed3_bytes(0, 3) == 0 and oracle.packed3_bytes(3, 0) == 0
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 95, 96, 97, 100, 191, 2048])
+@pytest.mark.parametrize("n", [1, 63, 65])
+def test_pack3_round_trip(n, k):
+    t = synth.ternary_any(n, k, 3, "rt3")
+    assert np.array_equal(oracle.unpack3(oracle.pack3(t), n, k), t)
+
+
+def test_pack3_rejects_values_and_unpack3_rejects_unused_codes():
+    t = synth.ternary_any(2, 10, 4, "bad3")
+    t[1, 7] = 2
+    with pytest.raises(oracle.OracleError, match="at 17"):
+        oracle.pack3(t)
+    t[1, 7] = 0
+    p = oracle.pack3(t)
+    # code 0 of row 1 sits in stream bits 0..4 of bytes 16..; write each
+    # unused code (27..31) there
+    for bad in range(27, 32):
+        q = p.copy()
+        q[16] = (q[16] & 0xE0) | bad
+        with pytest.raises(oracle.OracleError):
+            oracle.unpack3(q, 2, 10)
+    # a valid code in the same place decodes
+    q = p.copy()
+    q[16] = (q[16] & 0xE0) | 26
+    assert list(oracle.unpack3(q, 2, 10)[1, :3]) == [1, 1, 1]
