@@ -331,11 +331,24 @@ int sherry_gemv_f32_batched(const sherry_gemv_f32_desc* descs_dev, int count,
                             int64_t total_blocks, void* stream);
 
 /* ---------------------------------------------------------------------- */
-/* 2-bit reference layout (the "2-bit strategy" of Sec. 2.3): one ternary  */
-/* weight per 2 bits, value w+1; unit (r, c) = 64 rows x 64 weights = 1024 */
-/* bytes at (r*Kp/64 + c)*1024, Kp = ceil(K/64)*64; row i's 16 bytes at    */
-/* 16*i hold weight 64c+u at bits [2u, 2u+2); padding is weight 0.         */
-/* Used only to compare bytes moved against the 5-bit layout.             */
+/* Comparison layouts (Sec. 2.3): the "2-bit strategy" and the "1.67-bit   */
+/* strategy" the paper sets against its 1.25-bit codes.  They hold any     */
+/* ternary T and exist to measure bytes moved and time on the same GPU;    */
+/* their products take int8 activations and one weight scale per tensor.  */
+/*                                                                        */
+/* 2-bit layout: one weight per 2 bits, value w+1; unit (r, c) = 64 rows x */
+/* 64 weights = 1024 bytes at (r*Kp/64 + c)*1024, Kp = ceil(K/64)*64; row  */
+/* i's 16 bytes at 16*i hold weight 64c + 16w + 4j + p (w, j, p in 0..3)   */
+/* in byte 4w + p at bits [2j, 2j+2); padding is weight 0.                */
+/*                                                                        */
+/* 1.67-bit layout: three weights per 5-bit code, code = (t0+1) + 3(t1+1)  */
+/* + 9(t2+1) for the block t0, t1, t2 of weights 3b, 3b+1, 3b+2 (codes     */
+/* 27..31 unused); T is extended with zero weights to Np = ceil(N/64)*64   */
+/* rows and Kp = ceil(K/96)*96 columns; unit (r, c) = 64 rows x 96 weights */
+/* = 1280 bytes at (r*Kp/96 + c)*1280, laid out as a 5-bit unit: row i's   */
+/* 160-bit stream holds code j (weights 96c + 3j .. + 2) at stream bits    */
+/* [5j, 5j+5), stream bits 0..127 in bytes 16*i.., 128..159 in            */
+/* 1024 + 4*i...                                                          */
 /* ---------------------------------------------------------------------- */
 
 size_t sherry_packed2_bytes(int64_t n, int64_t k);
@@ -349,6 +362,41 @@ int sherry_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
 int sherry_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,
                  float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
                  void* stream);
+
+/* Bytes of the 1.67-bit layout of an n x k matrix (any k >= 1), or 0 if
+ * n < 1, k < 1, n > SHERRY_MAX_N or k > SHERRY_MAX_K. */
+size_t sherry_packed3_bytes(int64_t n, int64_t k);
+
+/* Packs any ternary T (host, int8 [n][k] in {-1,0,1}) into the 1.67-bit
+ * layout (host buffer of at least sherry_packed3_bytes(n, k) bytes, every
+ * byte written); SHERRY_E_INVALID for another value, its flat index in
+ * *bad_index when not NULL. */
+int sherry_pack3(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                 size_t out_bytes, int64_t* bad_index);
+
+/* Inverse of sherry_pack3 (host); SHERRY_E_INVALID if a code of the first n
+ * rows and k weights is one of the unused codes 27..31. */
+int sherry_unpack3(const uint8_t* packed, size_t packed_bytes, int64_t n,
+                   int64_t k, int8_t* t_out);
+
+/* M = 1 product on the 1.67-bit layout; arguments as sherry_gemv (k % 4 ==
+ * 0 for the int8 activation words). */
+int sherry_gemv3(const uint8_t* w3, const int8_t* x, const float* x_scale,
+                 float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                 void* stream);
+
+/* Grouped M = 1 products on the 2-bit (gemv2) or 1.67-bit (gemv3) layout:
+ * as sherry_gemv_batched_prepare / sherry_gemv_batched, with descriptors
+ * whose w points to that layout; w_scales and w_group_scales must be NULL
+ * (SHERRY_E_INVALID otherwise). */
+int sherry_gemv2_batched_prepare(sherry_gemv_desc* descs, int count,
+                                 int64_t* total_blocks);
+int sherry_gemv2_batched(const sherry_gemv_desc* descs_dev, int count,
+                         int64_t total_blocks, void* stream);
+int sherry_gemv3_batched_prepare(sherry_gemv_desc* descs, int count,
+                                 int64_t* total_blocks);
+int sherry_gemv3_batched(const sherry_gemv_desc* descs_dev, int count,
+                         int64_t total_blocks, void* stream);
 
 /* ---------------------------------------------------------------------- */
 /* Diagnostics.                                                            */

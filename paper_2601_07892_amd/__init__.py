@@ -41,7 +41,9 @@ EXPORTS = [
     "sherry_stream_read_groups", "sherry_gemv_f32", "sherry_gemv_f32_batched_prepare",
     "sherry_gemv_f32_batched", "sherry_gemm_batched_prepare", "sherry_gemm_batched",
     "sherry_gemm_channel", "sherry_gemv_f32_channel", "sherry_ternarize_pack",
-    "sherry_gemm_group", "sherry_gemv_f32_group",
+    "sherry_gemm_group", "sherry_gemv_f32_group", "sherry_packed3_bytes", "sherry_pack3",
+    "sherry_unpack3", "sherry_gemv3", "sherry_gemv2_batched_prepare", "sherry_gemv2_batched",
+    "sherry_gemv3_batched_prepare", "sherry_gemv3_batched",
 ]
 
 
@@ -129,6 +131,16 @@ def _load():
         "sherry_gemm_group": ([vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp],
                               ctypes.c_int),
         "sherry_gemv_f32_group": ([vp, vp, vp, vp, vp, vp, i64, i64, vp], ctypes.c_int),
+        "sherry_packed3_bytes": ([i64, i64], ctypes.c_size_t),
+        "sherry_pack3": ([vp, i64, i64, vp, ctypes.c_size_t, i64p], ctypes.c_int),
+        "sherry_unpack3": ([vp, ctypes.c_size_t, i64, i64, vp], ctypes.c_int),
+        "sherry_gemv3": ([vp, vp, vp, f32, vp, vp, i64, i64, vp], ctypes.c_int),
+        "sherry_gemv2_batched_prepare": ([ctypes.POINTER(sherry_gemv_desc), ctypes.c_int, i64p],
+                                         ctypes.c_int),
+        "sherry_gemv2_batched": ([vp, ctypes.c_int, i64, vp], ctypes.c_int),
+        "sherry_gemv3_batched_prepare": ([ctypes.POINTER(sherry_gemv_desc), ctypes.c_int, i64p],
+                                         ctypes.c_int),
+        "sherry_gemv3_batched": ([vp, ctypes.c_int, i64, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -220,6 +232,27 @@ def sherry_pack2(t: np.ndarray) -> np.ndarray:
     _check(lib.sherry_pack2(t.ctypes.data, n, k, out.ctypes.data, out.nbytes, ctypes.byref(bad)),
            "sherry_pack2")
     return out
+
+
+def sherry_packed3_bytes(n: int, k: int) -> int:
+    return int(lib.sherry_packed3_bytes(n, k))
+
+
+def sherry_pack3(t: np.ndarray) -> np.ndarray:
+    t = _host(t, np.int8)
+    n, k = t.shape
+    out = np.empty(max(sherry_packed3_bytes(n, k), 1), np.uint8)
+    bad = ctypes.c_int64(-1)
+    _check(lib.sherry_pack3(t.ctypes.data, n, k, out.ctypes.data, out.nbytes, ctypes.byref(bad)),
+           "sherry_pack3")
+    return out
+
+
+def sherry_unpack3(p: np.ndarray, n: int, k: int) -> np.ndarray:
+    p = _host(p, np.uint8)
+    t = np.empty((n, k), np.int8)
+    _check(lib.sherry_unpack3(p.ctypes.data, p.nbytes, n, k, t.ctypes.data), "sherry_unpack3")
+    return t
 
 
 # ---- device calls -------------------------------------------------------------
@@ -343,6 +376,37 @@ def sherry_gemm_batched(descs_dev, count: int, total_blocks: int, max_m: int, st
 def sherry_gemv2(w2, x, x_scale, w_scale: float, y, acc, n: int, k: int, stream=None):
     _check(lib.sherry_gemv2(_ptr(w2), _ptr(x), _ptr(x_scale), float(w_scale), _ptr(y), _ptr(acc),
                             n, k, _stream(stream)), "sherry_gemv2")
+
+
+def sherry_gemv3(w3, x, x_scale, w_scale: float, y, acc, n: int, k: int, stream=None):
+    _check(lib.sherry_gemv3(_ptr(w3), _ptr(x), _ptr(x_scale), float(w_scale), _ptr(y), _ptr(acc),
+                            n, k, _stream(stream)), "sherry_gemv3")
+
+
+def sherry_gemv2_batched_prepare(descs) -> int:
+    """As sherry_gemv_batched_prepare, for descriptors on the 2-bit layout."""
+    total = ctypes.c_int64(0)
+    _check(lib.sherry_gemv2_batched_prepare(descs, len(descs), ctypes.byref(total)),
+           "sherry_gemv2_batched_prepare")
+    return int(total.value)
+
+
+def sherry_gemv2_batched(descs_dev, count: int, total_blocks: int, stream=None):
+    _check(lib.sherry_gemv2_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
+           "sherry_gemv2_batched")
+
+
+def sherry_gemv3_batched_prepare(descs) -> int:
+    """As sherry_gemv_batched_prepare, for descriptors on the 1.67-bit layout."""
+    total = ctypes.c_int64(0)
+    _check(lib.sherry_gemv3_batched_prepare(descs, len(descs), ctypes.byref(total)),
+           "sherry_gemv3_batched_prepare")
+    return int(total.value)
+
+
+def sherry_gemv3_batched(descs_dev, count: int, total_blocks: int, stream=None):
+    _check(lib.sherry_gemv3_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
+           "sherry_gemv3_batched")
 
 
 def sherry_stream_read(src, nbytes: int, sink, stream=None):

@@ -236,6 +236,60 @@ extern "C" int sherry_gemv2(const uint8_t* w2, const int8_t* x, const float* x_s
   return launch_gemv2(w2, x, x_scale, w_scale, y, acc, n, k, as_stream(stream));
 }
 
+extern "C" int sherry_gemv3(const uint8_t* w3, const int8_t* x, const float* x_scale,
+                            float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                            void* stream) {
+  int st = check_product(w3, x, x_scale, y, 1, n, k, 4);
+  if (st != SHERRY_OK) return st;
+  if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+  return launch_gemv3(w3, x, x_scale, w_scale, y, acc, n, k, as_stream(stream));
+}
+
+namespace {
+// Grouped launch of M = 1 products on a comparison layout (2 or 3): one
+// weight scale per tensor only.
+int cmp_batched_prepare(int layout, sherry_gemv_desc* descs, int count, int64_t* total_blocks) {
+  if (!descs || !total_blocks || count < 1) return SHERRY_E_INVALID;
+  int64_t blocks = 0;
+  for (int i = 0; i < count; ++i) {
+    sherry_gemv_desc& d = descs[i];
+    int st = check_product(d.w, d.x, d.x_scale, d.y, 1, d.n, d.k, 4);
+    if (st != SHERRY_OK) return st;
+    if (d.w_scales || d.w_group_scales) return SHERRY_E_INVALID;
+    if (d.acc && !aligned(d.acc, 4)) return SHERRY_E_ALIGN;
+    d.block_begin = static_cast<int32_t>(blocks);
+    blocks += cmp_blocks(layout, d.n, d.k);
+    if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
+  }
+  *total_blocks = blocks;
+  return SHERRY_OK;
+}
+int cmp_batched(int layout, const sherry_gemv_desc* descs_dev, int count, int64_t total_blocks,
+                void* stream) {
+  if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
+    return SHERRY_E_INVALID;
+  if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  return launch_cmp_batched(layout, descs_dev, count, total_blocks, as_stream(stream));
+}
+}  // namespace
+
+extern "C" int sherry_gemv2_batched_prepare(sherry_gemv_desc* descs, int count,
+                                            int64_t* total_blocks) {
+  return cmp_batched_prepare(2, descs, count, total_blocks);
+}
+extern "C" int sherry_gemv2_batched(const sherry_gemv_desc* descs_dev, int count,
+                                    int64_t total_blocks, void* stream) {
+  return cmp_batched(2, descs_dev, count, total_blocks, stream);
+}
+extern "C" int sherry_gemv3_batched_prepare(sherry_gemv_desc* descs, int count,
+                                            int64_t* total_blocks) {
+  return cmp_batched_prepare(3, descs, count, total_blocks);
+}
+extern "C" int sherry_gemv3_batched(const sherry_gemv_desc* descs_dev, int count,
+                                    int64_t total_blocks, void* stream) {
+  return cmp_batched(3, descs_dev, count, total_blocks, stream);
+}
+
 extern "C" int64_t sherry_stream_read_groups(size_t bytes) { return stream_read_groups(bytes); }
 
 extern "C" int sherry_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream) {

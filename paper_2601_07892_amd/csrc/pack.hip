@@ -2,7 +2,8 @@
 //
 // sherry_pack turns a ternary 3:4 matrix into the 5-bit tiled layout that the
 // device products stream; sherry_unpack is its exact inverse.  sherry_pack2
-// writes the 2-bit reference layout.  Layouts are defined in sherry.h.
+// and sherry_pack3 write the two comparison layouts (2 bits per weight, and
+// three weights per 5-bit code).  Layouts are defined in sherry.h.
 #include <algorithm>
 #include <atomic>
 #include <cstring>
@@ -210,7 +211,8 @@ extern "C" int sherry_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
         uint8_t* unit = out + static_cast<size_t>(r * C + c) * kUnit2Bytes;
         for (int i = 0; i < kTileRows; ++i) {
           const int64_t row = r * kTileRows + i;
-          uint64_t word[2] = {0x5555555555555555ull, 0x5555555555555555ull};
+          // every field starts as weight 0 (value 1)
+          uint32_t word[4] = {0x55555555u, 0x55555555u, 0x55555555u, 0x55555555u};
           if (row < n) {
             for (int u = 0; u < kTileK2; ++u) {
               const int64_t kk = c * kTileK2 + u;
@@ -223,9 +225,9 @@ extern "C" int sherry_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
                 }
                 continue;
               }
-              const int sh = (2 * u) & 63;
-              word[u >> 5] &= ~(3ull << sh);
-              word[u >> 5] |= static_cast<uint64_t>(v + 1) << sh;
+              // u = 16 wd + 4 j + p: word wd, byte p, bits [2j, 2j + 2)
+              const int wd = u >> 4, sh = 8 * (u & 3) + 2 * ((u >> 2) & 3);
+              word[wd] = (word[wd] & ~(3u << sh)) | (static_cast<uint32_t>(v + 1) << sh);
             }
           }
           std::memcpy(unit + 16 * i, word, 16);
@@ -238,4 +240,92 @@ extern "C" int sherry_pack2(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
     return SHERRY_E_INVALID;
   }
   return SHERRY_OK;
+}
+
+// ---- 1.67-bit comparison layout: three weights per 5-bit code ------------
+
+extern "C" size_t sherry_packed3_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1 || n > SHERRY_MAX_N || k > SHERRY_MAX_K) return 0;
+  return static_cast<size_t>(ceil_div(n, kTileRows) * kTileRows) *
+         static_cast<size_t>(ceil_div(k, kTileK3)) * kUnitBytes / kTileRows;
+}
+
+extern "C" int sherry_pack3(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                            size_t out_bytes, int64_t* bad_index) {
+  if (!t || !out) return SHERRY_E_INVALID;
+  const size_t need = sherry_packed3_bytes(n, k);
+  if (need == 0) return SHERRY_E_SHAPE;
+  if (out_bytes < need) return SHERRY_E_BUFSIZE;
+  const int64_t R = ceil_div(n, kTileRows), C = ceil_div(k, kTileK3);
+  std::atomic<int64_t> first_bad{INT64_MAX};
+  parallel_ranges(R, [&](int64_t r0, int64_t r1) {
+    uint32_t codes[32];
+    for (int64_t r = r0; r < r1; ++r) {
+      for (int64_t c = 0; c < C; ++c) {
+        uint8_t* unit = out + static_cast<size_t>(r * C + c) * kUnitBytes;
+        for (int i = 0; i < kTileRows; ++i) {
+          const int64_t row = r * kTileRows + i;
+          for (int j = 0; j < 32; ++j) {
+            // base-3 digits w + 1, least significant first; weights past k
+            // and rows past n are 0 (digit 1)
+            uint32_t code = 0, scale = 1;
+            for (int q = 0; q < 3; ++q, scale *= 3) {
+              const int64_t kk = c * kTileK3 + 3 * j + q;
+              int v = 0;
+              if (row < n && kk < k) {
+                v = t[row * k + kk];
+                if (v < -1 || v > 1) {
+                  const int64_t flat = row * k + kk;
+                  int64_t cur = first_bad.load();
+                  while (flat < cur && !first_bad.compare_exchange_weak(cur, flat)) {
+                  }
+                  v = 0;
+                }
+              }
+              code += static_cast<uint32_t>(v + 1) * scale;
+            }
+            codes[j] = code;
+          }
+          put_container(codes, unit + 16 * i, unit + kHeadBytes + 4 * i);
+        }
+      }
+    }
+  });
+  if (first_bad.load() != INT64_MAX) {
+    if (bad_index) *bad_index = first_bad.load();
+    return SHERRY_E_INVALID;
+  }
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_unpack3(const uint8_t* packed, size_t packed_bytes, int64_t n,
+                              int64_t k, int8_t* t_out) {
+  if (!packed || !t_out) return SHERRY_E_INVALID;
+  const size_t need = sherry_packed3_bytes(n, k);
+  if (need == 0) return SHERRY_E_SHAPE;
+  if (packed_bytes < need) return SHERRY_E_BUFSIZE;
+  const int64_t R = ceil_div(n, kTileRows), C = ceil_div(k, kTileK3);
+  std::atomic<bool> bad{false};
+  parallel_ranges(R, [&](int64_t r0, int64_t r1) {
+    uint32_t codes[32];
+    for (int64_t r = r0; r < r1; ++r) {
+      for (int64_t c = 0; c < C; ++c) {
+        const uint8_t* unit = packed + static_cast<size_t>(r * C + c) * kUnitBytes;
+        for (int i = 0; i < kTileRows; ++i) {
+          const int64_t row = r * kTileRows + i;
+          if (row >= n) break;
+          get_container(unit + 16 * i, unit + kHeadBytes + 4 * i, codes);
+          for (int j = 0; j < 32; ++j) {
+            uint32_t code = codes[j];
+            const int64_t kk0 = c * kTileK3 + 3 * j;
+            if (kk0 >= k) break;
+            if (code > 26) bad.store(true);
+            for (int q = 0; q < 3; ++q, code /= 3)
+              if (kk0 + q < k) t_out[row * k + kk0 + q] = static_cast<int8_t>(int(code % 3) - 1);
+          }
+        }
+      }
+    }
+  });
+  return bad.load() ? SHERRY_E_INVALID : SHERRY_OK;
 }

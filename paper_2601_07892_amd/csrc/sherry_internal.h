@@ -20,6 +20,9 @@ constexpr int kHeadBytes = 1024;   // 64 rows * 16 bytes
 // Unit of the 2-bit layout: 64 rows x 64 weights, 16 bytes per row.
 constexpr int kTileK2 = 64;
 constexpr int kUnit2Bytes = 1024;
+// Unit of the 1.67-bit layout: 64 rows x 96 weights (32 codes of three
+// weights per row), stored like a 5-bit unit (1280 bytes).
+constexpr int kTileK3 = 96;
 
 constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -213,9 +216,18 @@ int launch_gemm_mfma(const uint8_t* w, const int8_t* x, const float* x_scale,
                      WScale ws, float* y, int32_t* acc, int64_t m,
                      int64_t n, int64_t k, hipStream_t s);
 
+// Comparison layouts (M = 1, one weight scale per tensor): 2-bit and
+// 1.67-bit.  cmp_blocks(layout, n, k) is the workgroup count of one product
+// (layout 2 or 3); launch_cmp_batched runs a prepared descriptor array.
 int launch_gemv2(const uint8_t* w2, const int8_t* x, const float* x_scale,
                  float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
                  hipStream_t s);
+int launch_gemv3(const uint8_t* w3, const int8_t* x, const float* x_scale,
+                 float w_scale, float* y, int32_t* acc, int64_t n, int64_t k,
+                 hipStream_t s);
+int64_t cmp_blocks(int layout, int64_t n, int64_t k);
+int launch_cmp_batched(int layout, const sherry_gemv_desc* descs, int count,
+                       int64_t total_blocks, hipStream_t s);
 
 int launch_stream_read(const void* src, size_t bytes, uint32_t* sink,
                        hipStream_t s);

@@ -75,6 +75,41 @@ def test_pack_matches_oracle(n, k):
     assert np.array_equal(oracle.unpack2(p2, n, k), t2)
 
 
+@pytest.mark.parametrize("n,k", [(1, 1), (1, 3), (2, 4), (63, 95), (64, 96), (65, 97),
+                                 (130, 1028), (257, 2048), (64, 3072), (3, 14336)])
+def test_pack3_matches_oracle(n, k):
+    t = synth.ternary_any(n, k, 25, "pk3")
+    assert sh.sherry_packed3_bytes(n, k) == oracle.packed3_bytes(n, k)
+    p3 = sh.sherry_pack3(t)
+    assert np.array_equal(p3, oracle.pack3(t))
+    assert np.array_equal(sh.sherry_unpack3(p3, n, k), t)
+    # 3:4 matrices are ternary too (the 8B-scale comparison packs the same T)
+    t34 = synth.ternary_34(n, (k + 3) // 4 * 4, 25, "pk3s")
+    assert np.array_equal(sh.sherry_pack3(t34), oracle.pack3(t34))
+
+
+def test_pack3_rejects_values_codes_and_buffers():
+    t = synth.ternary_any(3, 10, 26, "bad3")
+    t[2, 4] = -2
+    bad = ctypes.c_int64(-1)
+    out = np.zeros(sh.sherry_packed3_bytes(3, 10), np.uint8)
+    assert L.sherry_pack3(t.ctypes.data, 3, 10, out.ctypes.data, out.nbytes,
+                          ctypes.byref(bad)) == sh.SHERRY_E_INVALID
+    assert bad.value == 24
+    t[2, 4] = 1
+    assert L.sherry_pack3(t.ctypes.data, 3, 10, out.ctypes.data, out.nbytes - 1,
+                          None) == sh.SHERRY_E_BUFSIZE
+    assert L.sherry_pack3(t.ctypes.data, 0, 10, out.ctypes.data, out.nbytes,
+                          None) == sh.SHERRY_E_SHAPE
+    p = sh.sherry_pack3(t)
+    for code in range(27, 32):  # unused codes, written into row 1's code 0
+        q = p.copy()
+        q[16] = (q[16] & 0xE0) | code
+        with pytest.raises(sh.SherryError):
+            sh.sherry_unpack3(q, 3, 10)
+    assert sh.sherry_packed3_bytes(1, sh.SHERRY_MAX_K + 1) == 0
+
+
 @pytest.mark.parametrize("idx", [0, 1, 2])
 def test_pack_hand_derived_fixtures(idx):
     with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
@@ -161,6 +196,10 @@ def test_gemm_validation_without_launch():
     assert L.sherry_quantize_act(FAKE, 1, 126, FAKE, FAKE, None) == sh.SHERRY_E_SHAPE
     assert L.sherry_quantize_act(None, 1, 128, FAKE, FAKE, None) == sh.SHERRY_E_INVALID
     assert L.sherry_gemv2(FAKE, FAKE, FAKE, 1.0, FAKE, None, 64, 126, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemv3(FAKE, FAKE, FAKE, 1.0, FAKE, None, 64, 126, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemv3(FAKE_MIS, FAKE, FAKE, 1.0, FAKE, None, 64, 128, None) == \
+        sh.SHERRY_E_ALIGN
+    assert L.sherry_gemv3(None, FAKE, FAKE, 1.0, FAKE, None, 64, 128, None) == sh.SHERRY_E_INVALID
     assert L.sherry_stream_read(FAKE, 100, FAKE, None) == sh.SHERRY_E_SHAPE
     assert L.sherry_stream_read(FAKE + 8, 128, FAKE, None) == sh.SHERRY_E_ALIGN
 
@@ -212,6 +251,34 @@ def test_batched_prepare():
         sh.sherry_gemv_batched_prepare(descs)
     assert L.sherry_gemv_batched(None, 1, 1, None) == sh.SHERRY_E_INVALID
     assert L.sherry_gemv_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
+
+
+def test_comparison_batched_prepare():
+    # (n, k) -> workgroups: units of 64 (2-bit) or 96 (1.67-bit) weights per
+    # row, at most 20 / 16 units per wave, 8 waves per workgroup
+    shapes = [(4096, 4096), (1024, 4096), (14336, 4096), (4096, 14336), (70, 100)]
+    for prep, run, exp in (
+            (sh.sherry_gemv2_batched_prepare, L.sherry_gemv2_batched,
+             # C = 64, 64, 64, 224, 2 -> S = 4, 4, 4, 8, 1
+             ([0, 32, 40, 152, 216], 217)),
+            (sh.sherry_gemv3_batched_prepare, L.sherry_gemv3_batched,
+             # C = 43, 43, 43, 150, 2 -> S = 4, 4, 4, 8, 1
+             ([0, 32, 40, 152, 216], 217))):
+        descs = (sh.sherry_gemv_desc * len(shapes))()
+        for i, (n, k) in enumerate(shapes):
+            descs[i].w, descs[i].x, descs[i].x_scale, descs[i].y = FAKE, FAKE, FAKE, FAKE
+            descs[i].n, descs[i].k, descs[i].w_scale = n, k, 0.02
+        total = prep(descs)
+        assert [d.block_begin for d in descs] == exp[0] and total == exp[1]
+        descs[2].w_scales = FAKE  # one scale per tensor only
+        with pytest.raises(sh.SherryError):
+            prep(descs)
+        descs[2].w_scales = None
+        descs[4].k = 102
+        with pytest.raises(sh.SherryError):
+            prep(descs)
+        assert run(None, 1, 1, None) == sh.SHERRY_E_INVALID
+        assert run(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
 
 
 def test_fused_validation_without_launch():
