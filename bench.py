@@ -610,34 +610,67 @@ def bench_activation_tables(sh, torch, dev, spec, seed, shapes=("q", "gate", "do
     return rows
 
 
-def bench_two_bit(sh, torch, dev, spec, seed, shapes=("q", "gate", "down"), reps=3):
-    """The same ternary weights as 1.25-bit codes and as the 2-bit reference
-    layout, M = 1, each timed over rotated copies (launched from a captured
-    graph): time and bytes moved."""
-    blk = {lin.name: lin for lin in synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])}
-    rows = []
-    for name in shapes:
-        lin = blk[name]
-        t = synth.ternary_34(lin.n, lin.k, seed, "tb", name)
-        q = torch.from_numpy(synth.int8_any(1, lin.k, seed, "tbx", name)).to(dev)
-        sx = torch.full((1,), 0.01, dtype=torch.float32, device=dev)
-        y = torch.empty(lin.n, dtype=torch.float32, device=dev)
-        row = {"proj": name, "n": lin.n, "k": lin.k}
-        for fmt, pack, call in (("sherry", sh.sherry_pack, sh.sherry_gemv),
-                                ("two_bit", sh.sherry_pack2, sh.sherry_gemv2)):
-            packed = torch.from_numpy(pack(t)).to(dev)
-            ws = [packed.clone() for _ in range(_rotation(packed.numel()))]
-            run = lambda i: call(ws[i % len(ws)], q, sx, 0.02, y, None, lin.n, lin.k)
-            us = time_graph(run, reps * len(ws), torch)
-            row[fmt + "_bytes"] = packed.numel()
-            row[fmt + "_us"] = round(us, 3)
-            row[fmt + "_gbs"] = round(packed.numel() / (us * 1e-6) / 1e9, 1)
-            del ws, packed
-        row["time_ratio"] = round(row["sherry_us"] / row["two_bit_us"], 3)
-        row["bytes_ratio"] = round(row["sherry_bytes"] / row["two_bit_bytes"], 3)
-        rows.append(row)
+def bench_layouts_8b(sh, torch, dev, seed, reps=30):
+    """One M = 1 decode step of the 8B-scale stress model (32 layers x 7
+    linears, int8 activations and scales ready) in each of the three layouts
+    of Sec. 2.3, each as one grouped launch: the 1.25-bit 3:4 codes
+    (sherry_gemv_batched), three weights per 5-bit code (1.67 bits,
+    sherry_gemv3_batched) and 2 bits per weight (sherry_gemv2_batched).  The
+    same ternary 3:4 weights feed all three.  One layer's seven matrices are
+    generated and packed on the host; each of the 32 layers streams its own
+    device copy of them, so every step reads its whole weight set from HBM
+    (1.09 to 1.74 GB, beyond the Infinity Cache)."""
+    spec = synth.STRESS_8B
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    ts = [synth.ternary_34(lin.n, lin.k, seed, "lay", lin.name) for lin in blk]
+    ks = sorted({lin.k for lin in blk})
+    q = {kk: torch.from_numpy(synth.int8_any(1, kk, seed, "layx", kk)).to(dev) for kk in ks}
+    sx = torch.full((1,), 0.01, dtype=torch.float32, device=dev)
+    layouts = (("sherry_1.25bit", sh.sherry_pack, sh.sherry_gemv_batched_prepare,
+                sh.sherry_gemv_batched),
+               ("three_in_5bit_1.67bit", sh.sherry_pack3, sh.sherry_gemv3_batched_prepare,
+                sh.sherry_gemv3_batched),
+               ("two_bit", sh.sherry_pack2, sh.sherry_gemv2_batched_prepare,
+                sh.sherry_gemv2_batched))
+    rows = {}
+    for name, pack, prep, run in layouts:
+        host = [pack(t) for t in ts]
+        w = [[torch.from_numpy(h).to(dev) for h in host] for _ in range(spec["layers"])]
+        ys = [[torch.empty(lin.n, dtype=torch.float32, device=dev) for lin in blk]
+              for _ in range(spec["layers"])]
+        count = spec["layers"] * len(blk)
+        descs = (sh.sherry_gemv_desc * count)()
+        for layer in range(spec["layers"]):
+            for j, lin in enumerate(blk):
+                d = descs[layer * len(blk) + j]
+                d.w, d.x, d.x_scale, d.y, d.acc = (w[layer][j].data_ptr(), q[lin.k].data_ptr(),
+                                                   sx.data_ptr(), ys[layer][j].data_ptr(), None)
+                d.n, d.k, d.w_scale = lin.n, lin.k, 0.02
+        total = prep(descs)
+        dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+        go = lambda i: run(dd, count, total)
+        settle(go, torch, 0.03)
+        a, b = _events(torch)
+        a.record()
+        for i in range(reps):
+            go(i)
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) / reps * 1e3
+        wbytes = spec["layers"] * sum(int(h.size) for h in host)
+        byts = wbytes + spec["layers"] * sum(lin.k + 4 + 4 * lin.n for lin in blk)
+        rows[name] = {"weight_bytes": wbytes, "bytes_per_step": byts, "step_us": round(us, 2),
+                      "gbs": round(byts / (us * 1e-6) / 1e9, 1),
+                      "frac": round(byts / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+        del w, ys, dd, host
         torch.cuda.empty_cache()
-    return rows
+    ref = rows["sherry_1.25bit"]
+    for name in ("three_in_5bit_1.67bit", "two_bit"):
+        rows[name]["sherry_bytes_ratio"] = round(ref["weight_bytes"] / rows[name]["weight_bytes"], 4)
+        rows[name]["sherry_time_ratio"] = round(ref["step_us"] / rows[name]["step_us"], 4)
+    return {"workload": "8B-scale stress decode step, M=1, 32 layers x 7 linears (224 products), "
+                        "int8 activations, one grouped launch per layout",
+            "products": spec["layers"] * len(blk), "layouts": rows}
 
 
 # ---------------------------------------------------------------------------
@@ -794,7 +827,7 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="skip the M=2048 GEMM and ceiling")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", choices=["decode", "product", "prefill", "grouped", "ternarize",
-                                       "tables"],
+                                       "tables", "layouts"],
                     default=None,
                     help="run only one part (for profiler runs): the timed decode steps, the "
                          "back-to-back product launches, the M=2048 LLaMA-3.2-3B layer, the "
@@ -847,6 +880,10 @@ def main():
     if args.only == "tables":
         print(json.dumps({"activation_vs_weight_tables_3b": bench_activation_tables(
             sh, torch, dev, synth.LLAMA_3B, args.seed)}), flush=True)
+        return
+    if args.only == "layouts":
+        print(json.dumps({"layouts_8b_step": bench_layouts_8b(sh, torch, dev, args.seed)}),
+              flush=True)
         return
     if args.only == "ternarize":
         print(json.dumps({"ternarize_pack": bench_ternarize(sh, torch, dev, args.seed)}),
@@ -957,15 +994,15 @@ def main():
             "llama-3.2-3b": bench_shapes(sh, torch, dev, synth.LLAMA_3B, args.seed, (1, 4, 16)),
             "stress-8b": bench_shapes(sh, torch, dev, synth.STRESS_8B, args.seed, (1, 64)),
         }
-        out["two_bit_vs_sherry_8b"] = bench_two_bit(sh, torch, dev, synth.STRESS_8B, args.seed)
+        out["layouts_8b_step"] = bench_layouts_8b(sh, torch, dev, args.seed)
         out["activation_vs_weight_tables_3b"] = bench_activation_tables(sh, torch, dev,
                                                                         synth.LLAMA_3B, args.seed)
         for r in out["activation_vs_weight_tables_3b"]:
             log("3b %s M=1: weight tables %.2f us, activation tables %.2f us" %
                 (r["proj"], r["weight_table_us"], r["activation_table_us"]))
-        for r in out["two_bit_vs_sherry_8b"]:
-            log("8b %s: 1.25-bit %.2f us vs 2-bit %.2f us (bytes %.3f, time %.3f)" %
-                (r["proj"], r["sherry_us"], r["two_bit_us"], r["bytes_ratio"], r["time_ratio"]))
+        for name, r in out["layouts_8b_step"]["layouts"].items():
+            log("8b step, %s: %.2f us, %.0f GB/s (%d weight bytes)" %
+                (name, r["step_us"], r["gbs"], r["weight_bytes"]))
     t0 = time.time()
     if not args.no_cpu:
         out["cpu_baseline"], ref = cpu_baseline(step)
