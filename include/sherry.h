@@ -84,6 +84,9 @@ typedef enum sherry_status {
 /* activations, 4-bit index + sign bit per code; Sec. 3.1, Appendix A), a    */
 /* comparison point for SHERRY_KERNEL_GEMV.  Never chosen automatically.     */
 #define SHERRY_KERNEL_ALUT 4
+/* Decode in registers + one int8 MFMA per 4-code chunk for up to 4 tokens  */
+/* (the activations staged in LDS): m <= 4 and m*ceil(k/128)*128 <= 32768.  */
+#define SHERRY_KERNEL_GEMV_TOK 5
 #define SHERRY_ALUT_MAX_K 8192
 
 /* Static string for a status code (never NULL). */
@@ -246,9 +249,10 @@ int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
 
 /* ---------------------------------------------------------------------- */
 /* Grouped products: many independent products (any m, e.g. the q, k and  */
-/* v projections of one layer) in one launch, on the register-decoded      */
-/* kernel (SHERRY_KERNEL_SKINNY); products run in token blocks of 32 when  */
-/* every m <= 32 or a descriptor has per-group scales, else of 64.        */
+/* v projections of one layer) in one launch: up to 4 tokens each on the   */
+/* matrix-core GEMV (SHERRY_KERNEL_GEMV_TOK), else on the register-decoded */
+/* kernel (SHERRY_KERNEL_SKINNY); it runs token blocks of 32 when every    */
+/* m <= 32 or a descriptor has per-group scales, else of 64.              */
 /* ---------------------------------------------------------------------- */
 
 typedef struct sherry_gemm_desc {
@@ -268,9 +272,13 @@ typedef struct sherry_gemm_desc {
 } sherry_gemm_desc;
 
 /* Host: validates descs[0..count), fills each block_begin, *total_blocks
- * and *max_m, which selects the launch's token blocks: the largest m, or
- * at most 32 when a descriptor carries per-group scales (their kernel runs
- * 32-token blocks).  Pass it to sherry_gemm_batched unchanged. */
+ * and *max_m, the launch value that selects the kernel and its token
+ * blocks.  When every m <= 4, no descriptor has per-group scales and every
+ * m * ceil(k/128) * 128 <= 32768, the products run on the matrix-core GEMV
+ * (SHERRY_KERNEL_GEMV_TOK) and *max_m is the largest m (1..4); otherwise
+ * they run on the register-decoded kernel and *max_m is the largest m, at
+ * least 5, and at most 32 when a descriptor carries per-group scales (their
+ * kernel runs 32-token blocks).  Pass it to sherry_gemm_batched unchanged. */
 int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
                                 int64_t* total_blocks, int32_t* max_m);
 

@@ -124,6 +124,13 @@ int gemm_dispatch(const uint8_t* w, const int8_t* x, const float* x_scale, WScal
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
     return launch_gemm_mfma(w, x, x_scale, ws, y, acc, m, n, k, as_stream(stream));
   }
+  if (kernel == SHERRY_KERNEL_GEMV_TOK) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 4);
+    if (st != SHERRY_OK) return st;
+    if (!gemv_tok_fits(m, k)) return SHERRY_E_SHAPE;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_gemv_tok(w, x, x_scale, ws, y, acc, m, n, k, as_stream(stream));
+  }
   if (kernel == SHERRY_KERNEL_ALUT) {
     int st = check_product(w, x, x_scale, y, m, n, k, 4);
     if (st != SHERRY_OK) return st;
@@ -373,16 +380,33 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
     if (d.w_group_scales) grouped = true;
     if (d.m > mm) mm = d.m;
   }
-  // every product runs in token blocks of the size the largest m selects;
-  // per-group scales run 32-token blocks
-  const int32_t sel = grouped && mm > 32 ? 32 : mm;
-  const int64_t tok = skinny_batched_tokens(sel);
+  // up to four tokens per product (and no per-group scales): the matrix-core
+  // GEMV, if every product's activations fit its LDS staging
+  bool tok = !grouped && mm <= 4;
+  for (int i = 0; tok && i < count; ++i) tok = gemv_tok_fits(descs[i].m, descs[i].k);
   int64_t blocks = 0;
+  if (tok) {
+    for (int i = 0; i < count; ++i) {
+      sherry_gemm_desc& d = descs[i];
+      d.block_begin = static_cast<int32_t>(blocks);
+      d.reserved = 0;
+      blocks += gemv_tok_blocks(d.n, d.k);
+      if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
+    }
+    *total_blocks = blocks;
+    *max_m = mm;
+    return SHERRY_OK;
+  }
+  // otherwise every product runs on the register-decoded kernel in token
+  // blocks of the size the largest m selects (per-group scales: 32-token
+  // blocks); the launch value is at least 5, which keeps small m here
+  const int32_t sel = grouped && mm > 32 ? 32 : (mm < 5 ? 5 : mm);
+  const int64_t tokens = skinny_batched_tokens(sel);
   for (int i = 0; i < count; ++i) {
     sherry_gemm_desc& d = descs[i];
     d.block_begin = static_cast<int32_t>(blocks);
     d.reserved = 0;
-    blocks += int64_t(skinny_blocks(d.n, d.w_group_scales != nullptr)) * ceil_div(d.m, tok);
+    blocks += int64_t(skinny_blocks(d.n, d.w_group_scales != nullptr)) * ceil_div(d.m, tokens);
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
   }
   *total_blocks = blocks;
@@ -396,6 +420,7 @@ extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
     return SHERRY_E_INVALID;
   if (max_m < 1 || max_m > SHERRY_MAX_M) return SHERRY_E_SHAPE;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  if (max_m <= 4) return launch_gemv_tok_batched(descs_dev, count, total_blocks, as_stream(stream));
   return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
 }
 

@@ -20,6 +20,7 @@
 // any 64 lookups are free of bank conflicts.  The fused quantize + product
 // kernels (one token) accumulate on the matrix cores instead of with v_dot4
 // (dot_container_mfma).
+#include <type_traits>
 #include <utility>
 
 #include "sherry_internal.h"
@@ -193,10 +194,33 @@ struct XFromLdsMfma {
   }
 };
 
+// Up to four tokens on the matrix cores, with the same B operand (lane
+// 16b + t holds row 16b + t of the tile): A row 4b + m carries token m's
+// chunk in k block b, so D[4b + m][t] = x_m . w(row 16b + t), and lane
+// 16b + t ends with its own row's token sums in its accumulator elements
+// 0..M-1.  The A operand of lane 20b + m (m < M) is read from token m's row
+// of xq; every other lane's stays zero.  The matrix-core work per container
+// is the same for one to four tokens.
+struct XFromLdsMfmaTok {
+  const int8_t* xq;  // LDS, M rows of kp bytes (zero past k)
+  int kp, m_count;
+  mutable u32x4 xw[4] = {};
+  __device__ __forceinline__ void dot(const uint32_t (&d)[5], int c, const uint32_t* lut,
+                                      v4i (&acc)[2]) const {
+    const int lane = threadIdx.x & 63;
+    const int m = (lane & 15) - 4 * (lane >> 4);
+    const bool own = m >= 0 && m < m_count;
+    dot_container_mfma<0>(d, reinterpret_cast<const u32x4*>(xq + (own ? m : 0) * kp + c * kTileK),
+                          own, xw, lut, acc);
+  }
+};
+
 template <class X>
 constexpr bool kMfmaSource = false;
 template <>
 constexpr bool kMfmaSource<XFromLdsMfma> = true;
+template <>
+constexpr bool kMfmaSource<XFromLdsMfmaTok> = true;
 
 // Container c through a buffer resource spanning a wave's containers (reads
 // outside it return zero and never fault): 16-byte head at lane*16, 4-byte
@@ -352,13 +376,20 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
     for (int m = 0; m < M; ++m) accf[m] = 0.0f;
     ring_run_groups<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
   } else if constexpr (kMfmaSource<X>) {
-    static_assert(M == 1 && !kGrp, "the matrix-core source serves one token");
+    static_assert(M <= 4 && !kGrp, "the matrix-core sources serve up to four tokens");
     v4i macc[2] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
     ring_run(ring, range, c0, c1, xsrc, lut, macc);
-    // lane l < 16 holds rows l, 16 + l, 32 + l, 48 + l of the tile
-    if (lane < 16) {
+    if constexpr (std::is_same_v<X, XFromLdsMfma>) {
+      // lane l < 16 holds rows l, 16 + l, 32 + l, 48 + l of the tile
+      if (lane < 16) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) red[wave * 64 + 16 * e + lane] = macc[0][e] + macc[1][e];
+        for (int e = 0; e < 4; ++e) red[wave * 64 + 16 * e + lane] = macc[0][e] + macc[1][e];
+      }
+    } else {
+      // the LDS of the activations is reused: every wave has finished reading it
+      __syncthreads();
+#pragma unroll
+      for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + lane] = macc[0][m] + macc[1][m];
     }
   } else {
     ring_run(ring, range, c0, c1, xsrc, lut, acc);
@@ -408,6 +439,126 @@ struct ReadScales {
 
 __device__ __forceinline__ void fill_lut(uint32_t* lut) {
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
+}
+
+// Barrier for LDS traffic only: outstanding global loads (the weight ring)
+// stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Prelude of the matrix-core int8 products: copies the M activation rows
+// (int8 [M][k], k % 4 == 0) into xq (LDS, rows of kp bytes, zero past k) and
+// reads the tokens' scales.
+// Largest M * kp (bytes of staged activations) of the matrix-core int8
+// products: their LDS holds the rows and, after the stream, the partial sums.
+constexpr int kTokMaxBytes = 32768;
+
+template <int M>
+struct StageRows {
+  static constexpr int kPieces = kTokMaxBytes / 16 / kGemvThreads;  // per thread
+  const int8_t* x;
+  const float* x_scale;
+  int k, kp;
+  int8_t* xq;
+  u32x4 v[kPieces];
+  // Rows whose 16-byte pieces are aligned (k % 16 == 0, x 16-byte aligned)
+  // are loaded as such, all of a thread's pieces in flight at once, and
+  // stored by finish(); other rows are copied in 4-byte words by finish().
+  __device__ __forceinline__ bool wide() const {
+    return (k & 15) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+  }
+  __device__ __forceinline__ void issue() {
+    if (!wide()) return;
+    const SHERRY_GLOBAL u32x4* x16 = as_global(reinterpret_cast<const u32x4*>(x));
+    const int k16 = k >> 4, kp16 = kp >> 4;
+#pragma unroll
+    for (int e = 0; e < kPieces; ++e) {
+      const int i = threadIdx.x + e * kGemvThreads;
+      const int m = i / kp16, j = i - m * kp16;
+      // every thread loads (an in-bounds piece when past the rows), so the
+      // loads go out back to back
+      const bool in = m < M && j < k16;
+      const u32x4 t = x16[in ? m * k16 + j : 0];
+      v[e] = in ? t : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ void finish(float (&sx)[M]) {
+    if (wide()) {
+      u32x4* q16 = reinterpret_cast<u32x4*>(xq);
+#pragma unroll
+      for (int e = 0; e < kPieces; ++e) {
+        const int i = threadIdx.x + e * kGemvThreads;
+        if (i < M * (kp >> 4)) q16[i] = v[e];
+      }
+    } else {
+      const SHERRY_GLOBAL uint32_t* x4 = as_global(reinterpret_cast<const uint32_t*>(x));
+      uint32_t* q4 = reinterpret_cast<uint32_t*>(xq);
+      const int k4 = k >> 2, kp4 = kp >> 2;
+      for (int i = threadIdx.x; i < M * kp4; i += kGemvThreads) {
+        const int m = i / kp4, j = i - m * kp4;
+        q4[i] = j < k4 ? x4[m * k4 + j] : 0u;
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < M; ++m) sx[m] = as_const(x_scale)[m];
+    lds_barrier();
+  }
+};
+
+template <int M>
+__global__ __launch_bounds__(kGemvThreads) void gemv_tok_kernel(
+    const uint8_t* __restrict__ w, const int8_t* __restrict__ x,
+    const float* __restrict__ x_scale, WScale ws, float* __restrict__ y,
+    int32_t* __restrict__ acc, int64_t n, int64_t k, int split) {
+  __shared__ uint32_t lut[32];
+  __shared__ __attribute__((aligned(16))) int8_t xq[kTokMaxBytes];
+  fill_lut(lut);
+  const int kp = static_cast<int>((k + kTileK - 1) / kTileK) * kTileK;
+  gemv_block<M>(w, XFromLdsMfmaTok{xq, kp, M},
+                StageRows<M>{x, x_scale, static_cast<int>(k), kp, xq}, ws, y, acc, n,
+                static_cast<int>(k), blockIdx.x, split, lut, reinterpret_cast<int32_t*>(xq));
+}
+
+template <int M>
+__device__ __forceinline__ void tok_batched_block(const sherry_gemm_desc& d, int g,
+                                                  const uint32_t* lut, int8_t* xq) {
+  const int k = static_cast<int>(d.k);
+  const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
+  const int S = gemv_split((k + kTileK - 1) / kTileK);
+  gemv_block<M>(d.w, XFromLdsMfmaTok{xq, kp, M}, StageRows<M>{d.x, d.x_scale, k, kp, xq},
+                WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k, g, S, lut,
+                reinterpret_cast<int32_t*>(xq));
+}
+
+// Grouped products of up to four tokens each (sherry_gemm_desc, no
+// per-group scales, m * ceil(k/128) * 128 <= kTokMaxBytes).
+__global__ __launch_bounds__(kGemvThreads) void gemv_tok_batched_kernel(
+    const sherry_gemm_desc* __restrict__ descs, int count) {
+  __shared__ uint32_t lut[32];
+  __shared__ __attribute__((aligned(16))) int8_t xq[kTokMaxBytes];
+  fill_lut(lut);
+  const int32_t blk = static_cast<int32_t>(blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  int lo = 0;
+  for (int base = 0; base < count; base += 64) {
+    const int i = base + lane;
+    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
+    const int len = __popcll(__ballot(ok));
+    lo = base + len - 1;
+    if (len < 64) break;
+  }
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  const sherry_gemm_desc& d = descs[lo];
+  const int g = blk - d.block_begin;
+  switch (d.m) {
+    case 1: tok_batched_block<1>(d, g, lut, xq); break;
+    case 2: tok_batched_block<2>(d, g, lut, xq); break;
+    case 3: tok_batched_block<3>(d, g, lut, xq); break;
+    default: tok_batched_block<4>(d, g, lut, xq); break;
+  }
 }
 
 template <int M>
@@ -475,14 +626,6 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
 }
 
 // ---- fused per-token quantization + product (M = 1) ----
-
-// Barrier for LDS traffic only: outstanding global loads (the weight ring)
-// stay in flight across it.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 // Block-wide max of one value per thread (part: kGemvWaves floats of LDS).
 __device__ __forceinline__ float block_max_f32(float v, float* part) {
@@ -675,6 +818,37 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale, WS
     case 4: return launch(gemv_kernel<4>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
     default: return SHERRY_E_SHAPE;
   }
+}
+
+bool gemv_tok_fits(int64_t m, int64_t k) {
+  return m >= 1 && m <= 4 && m * ceil_div(k, kTileK) * kTileK <= kTokMaxBytes;
+}
+
+int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws, float* y,
+                    int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
+  if (!gemv_tok_fits(m, k)) return SHERRY_E_SHAPE;
+  const int64_t R = ceil_div(n, kTileRows);
+  const int C = static_cast<int>(ceil_div(k, kTileK));
+  const int S = (R * gemv_split(C) >= 4096) ? gemv_split(C) : kGemvWaves;
+  const dim3 grid(static_cast<unsigned>(ceil_div(R * S, kGemvWaves)));
+  const dim3 block(kGemvThreads);
+  switch (m) {
+    case 1: return launch(gemv_tok_kernel<1>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+    case 2: return launch(gemv_tok_kernel<2>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+    case 3: return launch(gemv_tok_kernel<3>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+    default: return launch(gemv_tok_kernel<4>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+  }
+}
+
+int64_t gemv_tok_blocks(int64_t n, int64_t k) {
+  return ceil_div(ceil_div(n, kTileRows) * gemv_split(static_cast<int>(ceil_div(k, kTileK))),
+                  kGemvWaves);
+}
+
+int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                            hipStream_t s) {
+  return launch(gemv_tok_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
+                dim3(kGemvThreads), 0, s, descs, count);
 }
 
 int launch_gemv_group(const uint8_t* w, const int8_t* x, const float* x_scale, const float* gs,

@@ -185,6 +185,17 @@ int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
 int launch_gemv_alut(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
                      float* y, int32_t* acc, int64_t n, int64_t k, hipStream_t s);
 
+// Up to four tokens on the matrix cores, activations staged in LDS
+// (m * ceil(k/128) * 128 <= 32768 bytes, gemv_tok_fits): single and grouped
+// launches; gemv_tok_blocks is one product's workgroup count in a grouped
+// launch.
+bool gemv_tok_fits(int64_t m, int64_t k);
+int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws, float* y,
+                    int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);
+int64_t gemv_tok_blocks(int64_t n, int64_t k);
+int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                            hipStream_t s);
+
 int skinny_blocks(int64_t n, bool group_scales = false);
 int skinny_batched_tokens(int max_m);
 int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,

@@ -253,6 +253,29 @@ def test_batched_prepare():
     assert L.sherry_gemv_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
 
 
+def test_gemm_batched_prepare_picks_the_token_gemv():
+    def prep(cases, group=False):
+        descs = (sh.sherry_gemm_desc * len(cases))()
+        for i, (m, n, k) in enumerate(cases):
+            d = descs[i]
+            d.w, d.x, d.x_scale, d.y = FAKE, FAKE, FAKE, FAKE
+            d.n, d.k, d.m, d.w_scale = n, k, m, 0.02
+            if group and i == 0:
+                d.w_group_scales = FAKE
+        total, max_m = sh.sherry_gemm_batched_prepare(descs)
+        return [d.block_begin for d in descs], total, max_m
+    # up to 4 tokens, activations fit 32 KB of LDS: the matrix-core GEMV
+    # (the int8 GEMV's work split, 8-wave blocks, at most 16 units per wave:
+    # 48 tiles x S=2 / 8, 16 x 2 / 8, 48 x 4 / 8)
+    assert prep([(4, 3072, 3072), (2, 1024, 3072), (1, 3072, 8192)]) == ([0, 12, 16], 40, 4)
+    assert prep([(1, 64, 128)]) == ([0], 1, 1)
+    # too long for the staging, or per-group scales: the register-decoded
+    # kernel, whose launch value is then at least 5
+    assert prep([(4, 3072, 8320), (1, 64, 128)])[2] == 5
+    assert prep([(2, 64, 128), (1, 64, 128)], group=True)[2] == 5
+    assert prep([(5, 64, 128)])[2] == 5
+
+
 def test_comparison_batched_prepare():
     # (n, k) -> workgroups: units of 64 (2-bit) or 96 (1.67-bit) weights per
     # row, at most 20 / 16 units per wave, 8 waves per workgroup
@@ -423,7 +446,12 @@ def test_activation_table_kernel_validation_without_launch():
              None) == sh.SHERRY_E_SHAPE
     assert g(FAKE, FAKE + 2, FAKE, 1.0, FAKE, None, 1, 64, 128, K, None) == sh.SHERRY_E_ALIGN
     assert g(FAKE, FAKE, FAKE, 1.0, FAKE, FAKE + 2, 1, 64, 128, K, None) == sh.SHERRY_E_ALIGN
-    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 1, 64, 128, 5, None) == sh.SHERRY_E_INVALID
+    assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, 1, 64, 128, 6, None) == sh.SHERRY_E_INVALID
+    # the matrix-core GEMV stages at most 32 KB of activations, 4 tokens
+    T = sh.SHERRY_KERNEL_GEMV_TOK
+    for m, k in ((5, 128), (4, 8320), (3, 10996), (1, 32900)):
+        assert g(FAKE, FAKE, FAKE, 1.0, FAKE, None, m, 64, k, T, None) == sh.SHERRY_E_SHAPE
+    assert g(FAKE, FAKE + 2, FAKE, 1.0, FAKE, None, 1, 64, 128, T, None) == sh.SHERRY_E_ALIGN
     for m in (1, 4, 16, 2048):
         assert sh.sherry_gemm_kernel_for(m, 2048, 2048) != K
     # per-group scales have no activation-table variant

@@ -1,0 +1,173 @@
+"""GPU parity of the matrix-core GEMV for up to four tokens
+(SHERRY_KERNEL_GEMV_TOK: activations staged in LDS, one int8 MFMA per 4-code
+chunk) against the CPU oracle, single and grouped launches: int32 accumulators
+bit-exact, fp32 outputs within 1e-5 relative."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+ORACLE_THREADS = 16
+RTOL = 1e-5
+
+
+def _sh():
+    import paper_2601_07892_amd as sh
+    return sh
+
+
+def _say(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    d = torch.device("cuda:0")
+    torch.cuda.set_device(d)
+    return d
+
+
+def _y_ok(y, y_ref):
+    y = np.asarray(y, np.float64)
+    return not (np.abs(y - y_ref) > RTOL * np.abs(y_ref)).any()
+
+
+def _epi(acc, sx, sw):
+    return oracle.epilogue_rows(acc, sx, sw) if np.ndim(sw) else oracle.epilogue(acc, sx, sw)
+
+
+def _scales(m, seed, tag):
+    return (np.abs(synth.activations(1, m, seed, tag)[0]) + 0.01).astype(np.float32)
+
+
+# ragged n and k, several row tiles and K splits, and the longest k each m
+# can stage (m * ceil(k/128) * 128 <= 32768)
+CASES = [(1, 64, 128), (2, 65, 132), (3, 130, 1028), (4, 300, 2048), (4, 257, 3076),
+         (1, 70, 32768), (2, 129, 16380), (3, 64, 10880), (4, 600, 8192), (4, 3072, 8192)]
+
+
+@pytest.mark.parametrize("m,n,k", CASES)
+@pytest.mark.parametrize("channel", [False, True])
+def test_tok_kernel_parity(dev, m, n, k, channel):
+    sh = _sh()
+    _say("tok", m, n, k, channel)
+    t = synth.ternary_34(n, k, 71, "tok", m, n, k)
+    q = synth.int8_any(m, k, 71, "tokq", m, n, k)
+    sx = _scales(m, 71, "toks%d" % m)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    qd, sxd = torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+    a = torch.full((m, n), -7, dtype=torch.int32, device=dev)
+    if channel:
+        sw = (np.random.default_rng(n + k).random(n) * 0.05 + 0.001).astype(np.float32)
+        swd = torch.from_numpy(sw).to(dev)
+        sh.sherry_gemm_channel(w, qd, sxd, swd, y, a, m, n, k, sh.SHERRY_KERNEL_GEMV_TOK)
+    else:
+        sw = 0.0173
+        sh.sherry_gemm_ex(w, qd, sxd, sw, y, a, m, n, k, sh.SHERRY_KERNEL_GEMV_TOK)
+    torch.cuda.synchronize()
+    acc_ref = oracle.gemm_i32(q, t, threads=ORACLE_THREADS)
+    assert np.array_equal(a.cpu().numpy(), acc_ref)
+    assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw))
+
+
+def test_tok_kernel_extremes_and_agreement(dev):
+    # activations at -128 / 127, all-(+1) and all-(-1) rows next to 3:4 rows;
+    # the same product on the v_dot4 GEMV gives the same bits
+    sh = _sh()
+    m, n, k = 4, 192, 4096
+    q = np.where(synth.int8_any(m, k, 72, "ext") >= 0, 127, -128).astype(np.int8)
+    t = synth.ternary_34(n, k, 72, "ext")
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    qd = torch.from_numpy(q).to(dev)
+    sxd = torch.ones(m, dtype=torch.float32, device=dev)
+    outs = []
+    for kern in (sh.SHERRY_KERNEL_GEMV_TOK, sh.SHERRY_KERNEL_GEMV):
+        y = torch.empty((m, n), dtype=torch.float32, device=dev)
+        a = torch.empty((m, n), dtype=torch.int32, device=dev)
+        sh.sherry_gemm_ex(w, qd, sxd, 1.0, y, a, m, n, k, kern)
+        torch.cuda.synchronize()
+        outs.append((y.cpu().numpy(), a.cpu().numpy()))
+    assert np.array_equal(outs[0][1], oracle.gemm_i32(q, t, threads=ORACLE_THREADS))
+    assert np.array_equal(outs[0][0].view(np.uint32), outs[1][0].view(np.uint32))
+    assert np.array_equal(outs[0][1], outs[1][1])
+
+
+def test_tok_kernel_rejects_what_it_cannot_stage(dev):
+    sh = _sh()
+    L = sh.lib
+    w = torch.zeros(sh.sherry_packed_bytes(64, 8320), dtype=torch.uint8, device=dev)
+    x = torch.zeros((5, 8320), dtype=torch.int8, device=dev)
+    sx = torch.ones(5, dtype=torch.float32, device=dev)
+    y = torch.empty((5, 64), dtype=torch.float32, device=dev)
+    for m, k in ((4, 8320), (5, 128), (3, 11008), (1, 32896)):
+        assert L.sherry_gemm_ex(w.data_ptr(), x.data_ptr(), sx.data_ptr(), 1.0, y.data_ptr(),
+                                None, m, 64, k, sh.SHERRY_KERNEL_GEMV_TOK, None) == \
+            sh.SHERRY_E_SHAPE
+
+
+def _grouped(dev, cases, seed, channel=False):
+    sh = _sh()
+    descs = (sh.sherry_gemm_desc * len(cases))()
+    keep = []
+    for i, (m, n, k) in enumerate(cases):
+        t = synth.ternary_34(n, k, seed, "tg", i)
+        q = synth.int8_any(m, k, seed, "tgq", i)
+        sx = _scales(m, seed, "tgs%d" % i)
+        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        qd, sxd = torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev)
+        y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+        a = torch.full((m, n), -7, dtype=torch.int32, device=dev)
+        d = descs[i]
+        d.w, d.x, d.x_scale, d.y = w.data_ptr(), qd.data_ptr(), sxd.data_ptr(), y.data_ptr()
+        d.acc = a.data_ptr() if i % 4 != 3 else None
+        d.n, d.k, d.m, d.w_scale = n, k, m, synth.weight_scale(seed, "tgw", i)
+        sw, hold = d.w_scale, None
+        if channel and i % 2 == 0:
+            sw = (np.random.default_rng(seed + i).random(n) * 0.05 + 0.001).astype(np.float32)
+            hold = torch.from_numpy(sw).to(dev)
+            d.w_scales = hold.data_ptr()
+        keep.append((t, q, sx, sw, d.acc is not None, w, qd, sxd, y, a, hold))
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+    sh.sherry_gemm_batched(dd, len(cases), total, max_m)
+    torch.cuda.synchronize()
+    for t, q, sx, sw, has_acc, w, qd, sxd, y, a, hold in keep:
+        acc_ref = oracle.gemm_i32(q, t, threads=ORACLE_THREADS)
+        if has_acc:
+            assert np.array_equal(a.cpu().numpy(), acc_ref)
+        else:
+            assert (a.cpu().numpy() == -7).all()
+        assert _y_ok(y.cpu().numpy(), _epi(acc_ref, sx, sw))
+    return max_m
+
+
+@pytest.mark.parametrize("channel", [False, True])
+def test_tok_batched_parity(dev, channel):
+    # 70 products of 1-4 tokens (two ballot rounds of the descriptor search)
+    _say("tok batched", channel)
+    cases = [(1 + i % 4, 64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700)) for i in range(70)]
+    assert _grouped(dev, cases, 73, channel) == 4
+
+
+@pytest.mark.parametrize("m", [2, 4])
+def test_tok_batched_model_step_full(dev, m):
+    # one LLaMA-3.2-3B layer at M tokens in one grouped launch, every output
+    _say("tok batched 3b layer", m)
+    spec = synth.LLAMA_3B
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 74) == m
+
+
+def test_small_m_too_long_goes_to_register_decoded_kernel(dev):
+    # m <= 4 but one product cannot stage its activations: every product
+    # runs on the register-decoded kernel (launch value 5)
+    _say("small m, long k")
+    cases = [(4, 64, 8320), (2, 130, 1028), (1, 65, 132)]
+    assert _grouped(dev, cases, 75) == 5
