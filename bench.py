@@ -119,8 +119,18 @@ class DecodeStep:
             for i in range(self.count):
                 fdescs[i].w_scales = self.channel_scales[i].data_ptr()
             fdev_ch = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
+            # every activation matrix of the step in one quantize launch
+            qdescs = (sh.sherry_quant_desc * len(self.ks))()
+            for j, kk in enumerate(self.ks):
+                qd = qdescs[j]
+                qd.x, qd.q, qd.x_scale = (xs[kk].data_ptr(), qs[kk].data_ptr(),
+                                          sxs[kk].data_ptr())
+                qd.m, qd.k = xs[kk].shape[0], kk
+            qrows, qmaxk = sh.sherry_quantize_act_batched_prepare(qdescs)
+            qdev = torch.from_numpy(sh.descs_to_bytes(qdescs)).to(dev)
             cp = dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total,
-                      fdescs=fdev, ftotal=ftotal, fdescs_ch=fdev_ch)
+                      fdescs=fdev, ftotal=ftotal, fdescs_ch=fdev_ch, qdescs=qdev,
+                      qrows=qrows, qmaxk=qmaxk)
             if c == 0:
                 # the same fused step with int32 outputs as well (parity check)
                 accs = [torch.empty(lin.n, dtype=torch.int32, device=dev)
@@ -151,6 +161,10 @@ class DecodeStep:
         cp = self.copies[c]
         for kk in self.ks:
             self.sh.sherry_quantize_act(cp["xs"][kk], cp["qs"][kk], cp["sxs"][kk])
+
+    def quantize_grouped(self, c):
+        cp = self.copies[c]
+        self.sh.sherry_quantize_act_batched(cp["qdescs"], len(self.ks), cp["qrows"], cp["qmaxk"])
 
     def gemv(self, c):
         cp = self.copies[c]
@@ -253,6 +267,27 @@ def bench_unfused(step: DecodeStep, torch, steps, warmup):
     return start.elapsed_time(stop) / steps
 
 
+def bench_two_launch(step: DecodeStep, torch, steps, warmup):
+    """ms per step as two launches: every activation row quantized in one
+    launch (sherry_quantize_act_batched), then the grouped int8 product."""
+    ncp = len(step.copies)
+
+    def run(i):
+        step.quantize_grouped(i % ncp)
+        step.gemv(i % ncp)
+    settle(run, torch)
+    for i in range(warmup):
+        run(i)
+    start, stop = _events(torch)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        run(i)
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps
+
+
 def heat(sh, torch, dev, seconds=0.03):
     """Brings the GPU to its steady loaded state before a timed loop (the
     first few milliseconds of sustained HBM load run slower): repeated
@@ -311,7 +346,7 @@ def bench_stream_ceiling(sh, torch, dev, nbytes=2 << 30, reps=20):
 def bench_prefill(sh, torch, dev, spec, m, seed, reps=10):
     blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
     rows = []
-    tot_ops, tot_ms = 0.0, 0.0
+    tot_ops, tot_ms, tot_ref = 0.0, 0.0, 0.0
     for lin in blk:
         t = synth.ternary_34(lin.n, lin.k, seed, "pw", lin.name, lin.k)
         w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
@@ -335,13 +370,31 @@ def bench_prefill(sh, torch, dev, spec, m, seed, reps=10):
         ops = 2.0 * m * lin.n * lin.k
         tot_ops += ops
         tot_ms += ms
+        # context: the vendor's dense int8 GEMM (torch._int_mm, hipBLASLt) on
+        # the same shape with unpacked int8 weights (no decode, 1 byte per
+        # weight), the practical ceiling of a plain int8 MFMA GEMM here
+        wd = torch.from_numpy(t).to(dev).t()  # [k][n] view of the [n][k] matrix
+        for _ in range(2):
+            torch._int_mm(q, wd)
+        a.record()
+        for _ in range(reps):
+            torch._int_mm(q, wd)
+        b.record()
+        torch.cuda.synchronize()
+        ms_ref = a.elapsed_time(b) / reps
+        tot_ref += ms_ref
         rows.append({"proj": lin.name, "n": lin.n, "k": lin.k, "us": round(ms * 1e3, 2),
                      "tops": round(ops / (ms * 1e-3) / 1e12, 1),
-                     "kernel": KERNEL_NAMES[sh.sherry_gemm_kernel_for(m, lin.n, lin.k)]})
-        del w, x, q, y
+                     "kernel": KERNEL_NAMES[sh.sherry_gemm_kernel_for(m, lin.n, lin.k)],
+                     "dense_int8_ref_us": round(ms_ref * 1e3, 2)})
+        del w, x, q, y, wd
     return {"m": m, "per_layer_us": round(tot_ms * 1e3, 2),
             "tops": round(tot_ops / (tot_ms * 1e-3) / 1e12, 1),
             "mfma_frac": round(tot_ops / (tot_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+            "dense_int8_ref": {"per_layer_us": round(tot_ref * 1e3, 2),
+                               "tops": round(tot_ops / (tot_ref * 1e-3) / 1e12, 1),
+                               "what": "torch._int_mm (hipBLASLt) on unpacked int8 weights, "
+                                       "same shapes: the plain int8 MFMA GEMM, no decode"},
             "shapes": rows}
 
 
@@ -913,9 +966,11 @@ def main():
                           "bytes_per_launch": step.fused_bytes}), flush=True)
         return
     ms_unfused = bench_unfused(step, torch, args.steps, args.warmup)
+    ms_two = bench_two_launch(step, torch, args.steps, args.warmup)
     kern_ms = bench_product_only(step, torch, args.product_launches)
-    log("unfused step %.2f us; int8 grouped product alone %.2f us (%.0f GB/s)" %
-        (ms_unfused * 1e3, kern_ms * 1e3, step.gemv_bytes / (kern_ms * 1e-3) / 1e9))
+    log("unfused step %.2f us; grouped quantize + product %.2f us; int8 grouped product alone "
+        "%.2f us (%.0f GB/s)" % (ms_unfused * 1e3, ms_two * 1e3, kern_ms * 1e3,
+                                 step.gemv_bytes / (kern_ms * 1e-3) / 1e9))
     src_hash = kernel_source_hash(["gemv.hip", "sherry_internal.h"])
     out = {
         "metric": "ternary GEMV GB/s & % HBM peak at M=1; GEMM TOPS at M=2048 (LLaMA-1B shapes)",
@@ -935,6 +990,10 @@ def main():
                      "kernel": "gemv_f32_batched_kernel", "bytes_per_launch": step.fused_bytes,
                      "avg_launch_us": round(ms_step * 1e3, 3),
                      "kernel_source_hash": src_hash},
+        "two_launch": {"step_us": round(ms_two * 1e3, 2),
+                       "gbs": round(step.fused_bytes / (ms_two * 1e-3) / 1e9, 1),
+                       "launches": "sherry_quantize_act_batched (112 rows) + "
+                                   "sherry_gemv_batched (112 products)"},
         "unfused": {"step_us": round(ms_unfused * 1e3, 2),
                     "int8_product_us": round(kern_ms * 1e3, 3),
                     "int8_product_gbs": round(step.gemv_bytes / (kern_ms * 1e-3) / 1e9, 1),
@@ -963,7 +1022,8 @@ def main():
         pre = {}
         for name, spec in (("llama-3.2-3b", synth.LLAMA_3B), ("llama-3.2-1b", synth.LLAMA_1B)):
             pre[name] = bench_prefill(sh, torch, dev, spec, 2048, args.seed)
-            log("prefill %s M=2048: %.1f TOPS" % (name, pre[name]["tops"]))
+            log("prefill %s M=2048: %.1f TOPS (dense int8 GEMM on unpacked weights: %.1f TOPS)" %
+                (name, pre[name]["tops"], pre[name]["dense_int8_ref"]["tops"]))
         out["prefill_m2048"] = pre
         grp = {}
         for name, spec in (("llama-3.2-3b", synth.LLAMA_3B), ("llama-3.2-1b", synth.LLAMA_1B)):

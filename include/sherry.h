@@ -151,6 +151,28 @@ int sherry_ternarize_pack(const float* w, int64_t n, int64_t k, uint8_t* packed,
 int sherry_quantize_act(const float* x, int64_t m, int64_t k, int8_t* q,
                         float* x_scale, void* stream);
 
+/* Many activation matrices in one launch (e.g. the inputs of every linear
+ * of a model step), each quantized exactly as sherry_quantize_act does. */
+typedef struct sherry_quant_desc {
+  const float* x;      /* device, fp32 [m][k], 16-byte aligned             */
+  int8_t* q;           /* device, int8 [m][k], 4-byte aligned              */
+  float* x_scale;      /* device, fp32 [m]                                 */
+  int32_t m, k;        /* m >= 1; k >= 4, k % 4 == 0, k <= SHERRY_MAX_K    */
+  int32_t row_begin;   /* written by sherry_quantize_act_batched_prepare   */
+  int32_t reserved;    /* set to 0                                         */
+} sherry_quant_desc;
+
+/* Host: validates descs[0..count) (count >= 1), fills each row_begin (the
+ * first row of that matrix in the launch), *total_rows (all rows) and
+ * *max_k (the longest row); pass both to sherry_quantize_act_batched. */
+int sherry_quantize_act_batched_prepare(sherry_quant_desc* descs, int count,
+                                        int64_t* total_rows, int32_t* max_k);
+
+/* Quantizes every row of descs_dev (device, a byte copy of a prepared
+ * array, 8-byte aligned) in one launch, one workgroup per row. */
+int sherry_quantize_act_batched(const sherry_quant_desc* descs_dev, int count,
+                                int64_t total_rows, int32_t max_k, void* stream);
+
 /* ---------------------------------------------------------------------- */
 /* Online products (Eq. 2).                                                */
 /* ---------------------------------------------------------------------- */

@@ -44,7 +44,8 @@ EXPORTS = [
     "sherry_gemm_channel", "sherry_gemv_f32_channel", "sherry_ternarize_pack",
     "sherry_gemm_group", "sherry_gemv_f32_group", "sherry_packed3_bytes", "sherry_pack3",
     "sherry_unpack3", "sherry_gemv3", "sherry_gemv2_batched_prepare", "sherry_gemv2_batched",
-    "sherry_gemv3_batched_prepare", "sherry_gemv3_batched",
+    "sherry_gemv3_batched_prepare", "sherry_gemv3_batched", "sherry_quantize_act_batched_prepare",
+    "sherry_quantize_act_batched",
 ]
 
 
@@ -82,6 +83,14 @@ class sherry_gemm_desc(ctypes.Structure):
         ("w_group_scales", ctypes.c_void_p),
         ("n", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32),
         ("w_scale", ctypes.c_float), ("block_begin", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+
+class sherry_quant_desc(ctypes.Structure):
+    _fields_ = [
+        ("x", ctypes.c_void_p), ("q", ctypes.c_void_p), ("x_scale", ctypes.c_void_p),
+        ("m", ctypes.c_int32), ("k", ctypes.c_int32), ("row_begin", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -142,6 +151,11 @@ def _load():
         "sherry_gemv3_batched_prepare": ([ctypes.POINTER(sherry_gemv_desc), ctypes.c_int, i64p],
                                          ctypes.c_int),
         "sherry_gemv3_batched": ([vp, ctypes.c_int, i64, vp], ctypes.c_int),
+        "sherry_quantize_act_batched_prepare": ([ctypes.POINTER(sherry_quant_desc), ctypes.c_int,
+                                                 i64p, ctypes.POINTER(ctypes.c_int32)],
+                                                ctypes.c_int),
+        "sherry_quantize_act_batched": ([vp, ctypes.c_int, i64, ctypes.c_int32, vp],
+                                        ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -311,6 +325,22 @@ def sherry_ternarize_pack(w, n: int, k: int, packed, alpha=None, stream=None):
     nbytes = packed.numel() * packed.element_size()
     _check(lib.sherry_ternarize_pack(_ptr(w), n, k, _ptr(packed), nbytes, _ptr(alpha),
                                      _stream(stream)), "sherry_ternarize_pack")
+
+
+def sherry_quantize_act_batched_prepare(descs):
+    """Fills row_begin of a ctypes array of sherry_quant_desc; returns (total_rows, max_k)."""
+    total, kk = ctypes.c_int64(0), ctypes.c_int32(0)
+    _check(lib.sherry_quantize_act_batched_prepare(descs, len(descs), ctypes.byref(total),
+                                                   ctypes.byref(kk)),
+           "sherry_quantize_act_batched_prepare")
+    return int(total.value), int(kk.value)
+
+
+def sherry_quantize_act_batched(descs_dev, count: int, total_rows: int, max_k: int,
+                                stream=None):
+    """descs_dev: device uint8 tensor holding a byte copy of prepared descriptors."""
+    _check(lib.sherry_quantize_act_batched(_ptr(descs_dev), count, total_rows, max_k,
+                                           _stream(stream)), "sherry_quantize_act_batched")
 
 
 def sherry_gemm_kernel_for(m: int, n: int, k: int) -> int:

@@ -82,6 +82,38 @@ extern "C" int sherry_quantize_act(const float* x, int64_t m, int64_t k, int8_t*
   return launch_quantize(x, m, k, q, x_scale, as_stream(stream));
 }
 
+static_assert(sizeof(sherry_quant_desc) == 40, "sherry_quant_desc layout");
+
+extern "C" int sherry_quantize_act_batched_prepare(sherry_quant_desc* descs, int count,
+                                                   int64_t* total_rows, int32_t* max_k) {
+  if (!descs || !total_rows || !max_k || count < 1) return SHERRY_E_INVALID;
+  int64_t rows = 0;
+  int32_t kk = 0;
+  for (int i = 0; i < count; ++i) {
+    sherry_quant_desc& d = descs[i];
+    if (!d.x || !d.q || !d.x_scale) return SHERRY_E_INVALID;
+    if (!shape_ok(d.m, 1, d.k)) return SHERRY_E_SHAPE;
+    if (!aligned(d.x, 16) || !aligned(d.q, 4) || !aligned(d.x_scale, 4)) return SHERRY_E_ALIGN;
+    d.row_begin = static_cast<int32_t>(rows);
+    d.reserved = 0;
+    rows += d.m;
+    if (rows > INT32_MAX) return SHERRY_E_SHAPE;
+    if (d.k > kk) kk = d.k;
+  }
+  *total_rows = rows;
+  *max_k = kk;
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_quantize_act_batched(const sherry_quant_desc* descs_dev, int count,
+                                           int64_t total_rows, int32_t max_k, void* stream) {
+  if (!descs_dev || count < 1 || total_rows < 1 || total_rows > INT32_MAX)
+    return SHERRY_E_INVALID;
+  if (max_k < 4 || max_k > SHERRY_MAX_K) return SHERRY_E_SHAPE;
+  if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  return launch_quantize_batched(descs_dev, count, total_rows, max_k, as_stream(stream));
+}
+
 extern "C" int sherry_gemm_kernel_for(int64_t m, int64_t n, int64_t k) {
   if (!shape_ok(m, n, k)) return -SHERRY_E_SHAPE;
   if (m <= kGemvMaxM) return SHERRY_KERNEL_GEMV;

@@ -176,6 +176,10 @@ struct WScale {
 
 int launch_quantize(const float* x, int64_t m, int64_t k, int8_t* q,
                     float* x_scale, hipStream_t s);
+// Every row of a prepared descriptor array (total_rows workgroups); max_k
+// selects how rows are held (registers or two passes).
+int launch_quantize_batched(const sherry_quant_desc* descs, int count, int64_t total_rows,
+                            int64_t max_k, hipStream_t s);
 
 int launch_gemv_valu(const uint8_t* w, const int8_t* x, const float* x_scale,
                      WScale ws, float* y, int32_t* acc, int64_t m,
