@@ -441,6 +441,17 @@ __device__ __forceinline__ void fill_lut(uint32_t* lut) {
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
 }
 
+// Block of a grouped launch that workgroup b runs.  Workgroups are dispatched
+// to the 8 XCDs in turn (b -> XCD b % 8), each with its own L2; XCD x takes
+// the x-th contiguous eighth of the blocks, so that the workgroups of one
+// product meet in few L2s and its activation row is fetched there once.
+__device__ __forceinline__ int32_t xcd_block(int32_t b, int32_t grid) {
+  constexpr int32_t kXcds = 8;
+  const int32_t q = grid / kXcds, r = grid % kXcds;
+  const int32_t x = b % kXcds, slot = b / kXcds;
+  return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
+}
+
 // Barrier for LDS traffic only: outstanding global loads (the weight ring)
 // stay in flight across it.
 __device__ __forceinline__ void lds_barrier() {
@@ -596,7 +607,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_batched_kernel(
   __shared__ int32_t red[kGemvWaves * 64];
   __shared__ float redf[kGemvWaves * 64];
   fill_lut(lut);
-  const int32_t blk = static_cast<int32_t>(blockIdx.x);
+  const int32_t blk = xcd_block(static_cast<int32_t>(blockIdx.x), static_cast<int32_t>(gridDim.x));
   // last descriptor with block_begin <= blk: block_begin strictly increases,
   // so the descriptors that qualify form a prefix; each lane tests one
   // descriptor and the prefix length comes from a ballot (one load round
@@ -774,7 +785,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
   __shared__ float part[kGemvWaves];
   __shared__ __attribute__((aligned(16))) int8_t xq[kFusedMaxK];
   fill_lut(lut);
-  const int32_t blk = static_cast<int32_t>(blockIdx.x);
+  const int32_t blk = xcd_block(static_cast<int32_t>(blockIdx.x), static_cast<int32_t>(gridDim.x));
   const int lane = threadIdx.x & 63;
   int lo = 0;
   for (int base = 0; base < count; base += 64) {
