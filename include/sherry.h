@@ -272,8 +272,9 @@ int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
 /* ---------------------------------------------------------------------- */
 /* Grouped products: many independent products (any m, e.g. the q, k and  */
 /* v projections of one layer) in one launch: up to 4 tokens each on the   */
-/* matrix-core GEMV (SHERRY_KERNEL_GEMV_TOK), else on the register-decoded */
-/* kernel (SHERRY_KERNEL_SKINNY); it runs token blocks of 32 when every    */
+/* matrix-core GEMV (SHERRY_KERNEL_GEMV_TOK), up to 16 on a 16-token       */
+/* window kernel, else on the register-decoded kernel                      */
+/* (SHERRY_KERNEL_SKINNY), which runs token blocks of 32 when every        */
 /* m <= 32 or a descriptor has per-group scales, else of 64.              */
 /* ---------------------------------------------------------------------- */
 
@@ -295,12 +296,15 @@ typedef struct sherry_gemm_desc {
 
 /* Host: validates descs[0..count), fills each block_begin, *total_blocks
  * and *max_m, the launch value that selects the kernel and its token
- * blocks.  When every m <= 4, no descriptor has per-group scales and every
+ * blocks.  Without per-group scales: when every m <= 4 and every
  * m * ceil(k/128) * 128 <= 32768, the products run on the matrix-core GEMV
- * (SHERRY_KERNEL_GEMV_TOK) and *max_m is the largest m (1..4); otherwise
- * they run on the register-decoded kernel and *max_m is the largest m, at
- * least 5, and at most 32 when a descriptor carries per-group scales (their
- * kernel runs 32-token blocks).  Pass it to sherry_gemm_batched unchanged. */
+ * (SHERRY_KERNEL_GEMV_TOK) and *max_m is the largest m (1..4); else, when
+ * every m <= 16, on the 16-token window kernel (weights as loaded, one int8
+ * MFMA per 4-code chunk for 16 tokens x 64 rows) and *max_m is the largest
+ * m, at least 5.  Otherwise they run on the register-decoded kernel and
+ * *max_m is the largest m, at least 17, and at most 32 when a descriptor
+ * carries per-group scales (their kernel runs 32-token blocks).  Pass it to
+ * sherry_gemm_batched unchanged. */
 int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
                                 int64_t* total_blocks, int32_t* max_m);
 

@@ -412,27 +412,30 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
     if (d.w_group_scales) grouped = true;
     if (d.m > mm) mm = d.m;
   }
-  // up to four tokens per product (and no per-group scales): the matrix-core
-  // GEMV, if every product's activations fit its LDS staging
+  // The launch value *max_m selects the kernel: 1-4 the 4-token matrix-core
+  // GEMV (every m <= 4 and every product's activations fit its LDS staging),
+  // 5-16 the 16-token window kernel (every m <= 16), 17 and more the
+  // register-decoded kernel (any m; the only one for per-group scales).
   bool tok = !grouped && mm <= 4;
   for (int i = 0; tok && i < count; ++i) tok = gemv_tok_fits(descs[i].m, descs[i].k);
+  const bool small = !grouped && mm <= 16;
   int64_t blocks = 0;
-  if (tok) {
+  if (tok || small) {
     for (int i = 0; i < count; ++i) {
       sherry_gemm_desc& d = descs[i];
       d.block_begin = static_cast<int32_t>(blocks);
       d.reserved = 0;
-      blocks += gemv_tok_blocks(d.n, d.k);
+      blocks += tok ? gemv_tok_blocks(d.n, d.k) : smallm_blocks(d.n);
       if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
     }
     *total_blocks = blocks;
-    *max_m = mm;
+    *max_m = tok ? mm : (mm < 5 ? 5 : mm);
     return SHERRY_OK;
   }
   // otherwise every product runs on the register-decoded kernel in token
   // blocks of the size the largest m selects (per-group scales: 32-token
-  // blocks); the launch value is at least 5, which keeps small m here
-  const int32_t sel = grouped && mm > 32 ? 32 : (mm < 5 ? 5 : mm);
+  // blocks)
+  const int32_t sel = grouped && mm > 32 ? 32 : (mm < 17 ? 17 : mm);
   const int64_t tokens = skinny_batched_tokens(sel);
   for (int i = 0; i < count; ++i) {
     sherry_gemm_desc& d = descs[i];
@@ -453,6 +456,7 @@ extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
   if (max_m < 1 || max_m > SHERRY_MAX_M) return SHERRY_E_SHAPE;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
   if (max_m <= 4) return launch_gemv_tok_batched(descs_dev, count, total_blocks, as_stream(stream));
+  if (max_m <= 16) return launch_smallm_batched(descs_dev, count, total_blocks, as_stream(stream));
   return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
 }
 

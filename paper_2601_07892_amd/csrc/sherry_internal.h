@@ -200,6 +200,13 @@ int64_t gemv_tok_blocks(int64_t n, int64_t k);
 int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
                             hipStream_t s);
 
+// Up to 16 tokens on the matrix cores, weights as loaded, activations
+// staged per K window (grouped launches): one product's workgroup count, and
+// the launch.
+int64_t smallm_blocks(int64_t n);
+int launch_smallm_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                          hipStream_t s);
+
 int skinny_blocks(int64_t n, bool group_scales = false);
 int skinny_batched_tokens(int max_m);
 int launch_skinny(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,

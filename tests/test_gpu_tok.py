@@ -1,7 +1,8 @@
-"""GPU parity of the matrix-core GEMV for up to four tokens
-(SHERRY_KERNEL_GEMV_TOK: activations staged in LDS, one int8 MFMA per 4-code
-chunk) against the CPU oracle, single and grouped launches: int32 accumulators
-bit-exact, fp32 outputs within 1e-5 relative."""
+"""GPU parity of the small-M matrix-core kernels against the CPU oracle: the
+GEMV for up to four tokens (SHERRY_KERNEL_GEMV_TOK: activations staged in
+LDS, one int8 MFMA per 4-code chunk), single and grouped launches, and the
+16-token window kernel of grouped launches: int32 accumulators bit-exact, fp32
+outputs within 1e-5 relative."""
 import sys
 
 import numpy as np
@@ -165,9 +166,61 @@ def test_tok_batched_model_step_full(dev, m):
     assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 74) == m
 
 
-def test_small_m_too_long_goes_to_register_decoded_kernel(dev):
+def test_small_m_too_long_goes_to_window_kernel(dev):
     # m <= 4 but one product cannot stage its activations: every product
-    # runs on the register-decoded kernel (launch value 5)
+    # runs on the 16-token window kernel (launch value 5)
     _say("small m, long k")
     cases = [(4, 64, 8320), (2, 130, 1028), (1, 65, 132)]
     assert _grouped(dev, cases, 75) == 5
+
+
+# 5-16 tokens: the window kernel (16 token rows staged per 1024-value window
+# of K, one 32x32x32 MFMA per 4-code chunk for 64 rows), with ragged n and k
+# (k % 16 != 0: the last piece of a row is read word by word), partial
+# windows, several windows, per-channel scales and products without acc
+WINDOW_CASES = [(5, 64, 128), (16, 65, 132), (9, 600, 2048), (16, 257, 3076), (12, 130, 1028),
+                (16, 3072, 8192), (7, 70, 4), (16, 1024, 3072), (6, 520, 14340)]
+
+
+@pytest.mark.parametrize("channel", [False, True])
+def test_window_kernel_grouped_parity(dev, channel):
+    _say("window kernel", channel)
+    assert _grouped(dev, WINDOW_CASES, 76, channel) == 16
+
+
+def test_window_kernel_many_products(dev):
+    # 70 products of 5-16 tokens (two ballot rounds of the descriptor search)
+    _say("window kernel, 70 products")
+    cases = [(5 + i % 12, 64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700)) for i in range(70)]
+    assert _grouped(dev, cases, 77) == 16
+
+
+@pytest.mark.parametrize("m", [8, 16])
+def test_window_kernel_model_step_full(dev, m):
+    # one LLaMA-3.2-3B layer at M tokens in one grouped launch, every output
+    _say("window kernel 3b layer", m)
+    spec = synth.LLAMA_3B
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 78) == m
+
+
+def test_window_kernel_extremes(dev):
+    # activations at -128 / 127 for all 16 tokens, k = 4096 (4 windows)
+    sh = _sh()
+    m, n, k = 16, 192, 4096
+    q = np.where(synth.int8_any(m, k, 79, "wext") >= 0, 127, -128).astype(np.int8)
+    t = synth.ternary_34(n, k, 79, "wext")
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    qd = torch.from_numpy(q).to(dev)
+    sxd = torch.ones(m, dtype=torch.float32, device=dev)
+    y = torch.empty((m, n), dtype=torch.float32, device=dev)
+    a = torch.empty((m, n), dtype=torch.int32, device=dev)
+    descs = (sh.sherry_gemm_desc * 1)()
+    d = descs[0]
+    d.w, d.x, d.x_scale, d.y, d.acc = w.data_ptr(), qd.data_ptr(), sxd.data_ptr(), y.data_ptr(), a.data_ptr()
+    d.n, d.k, d.m, d.w_scale = n, k, m, 1.0
+    total, max_m = sh.sherry_gemm_batched_prepare(descs)
+    assert max_m == 16
+    sh.sherry_gemm_batched(torch.from_numpy(sh.descs_to_bytes(descs)).to(dev), 1, total, max_m)
+    torch.cuda.synchronize()
+    assert np.array_equal(a.cpu().numpy(), oracle.gemm_i32(q, t, threads=ORACLE_THREADS))
