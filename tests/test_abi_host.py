@@ -270,10 +270,10 @@ def test_gemm_batched_prepare_picks_the_token_gemv():
     assert prep([(4, 3072, 3072), (2, 1024, 3072), (1, 3072, 8192)]) == ([0, 12, 16], 40, 4)
     assert prep([(1, 64, 128)]) == ([0], 1, 1)
     # too long for the staging, or 5-16 tokens: the 16-token window kernel
-    # (launch value 5-16; eight 64-row tiles per workgroup, whole K)
-    assert prep([(4, 3072, 8320), (1, 64, 128)]) == ([0, 6], 7, 5)
+    # (launch value 5-16; four 64-row tiles per workgroup, whole K)
+    assert prep([(4, 3072, 8320), (1, 64, 128)]) == ([0, 12], 13, 5)
     assert prep([(5, 64, 128)]) == ([0], 1, 5)
-    assert prep([(16, 3072, 8192), (9, 1024, 3072)]) == ([0, 6], 8, 16)
+    assert prep([(16, 3072, 8192), (9, 1024, 3072)]) == ([0, 12], 16, 16)
     # per-group scales, or more than 16 tokens: the register-decoded kernel
     # (launch value at least 17)
     assert prep([(2, 64, 128), (1, 64, 128)], group=True)[2] == 17
