@@ -21,18 +21,6 @@ namespace {
 constexpr int kAlutWaves = 8;
 constexpr int kAlutThreads = 64 * kAlutWaves;
 
-__device__ __forceinline__ void alut_load(uint32_t (&d)[5], __amdgpu_buffer_rsrc_t r, int c,
-                                          int lane) {
-  const u32x4 h =
-      __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, c * kUnitBytes, kLoadStream);
-  d[0] = h.x;
-  d[1] = h.y;
-  d[2] = h.z;
-  d[3] = h.w;
-  d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, c * kUnitBytes,
-                                              kLoadStream);
-}
-
 // Contribution of code j of a container (its 16 table rows at tb).
 template <int j>
 __device__ __forceinline__ int32_t alut_term(const uint32_t (&d)[5], const int16_t* tb) {
@@ -77,14 +65,12 @@ __global__ __launch_bounds__(kAlutThreads) void gemv_alut_kernel(
   const int lt = wave / S, part = wave - lt * S;
   const int r = blockIdx.x * tpb + lt;
   const int c0 = (r < R) ? (part * C) / S : 0, c1 = (r < R) ? ((part + 1) * C) / S : 0;
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(w) + (int64_t(r < R ? r : 0) * C + c0) * kUnitBytes, 0,
-      (c1 - c0) * kUnitBytes, kBufferWord3);
+  const UnitRun rs{w + (int64_t(r < R ? r : 0) * C + c0) * kUnitBytes, c1 - c0};
   int32_t acc = 0;
   uint32_t cur[5], nxt[5];
-  alut_load(cur, rs, 0, lane);  // past the range: zeros, no memory access
+  load_unit(cur, rs, 0, lane);  // past the range: zeros, no memory access
   for (int i = 0; i < c1 - c0; ++i) {
-    alut_load(nxt, rs, i + 1, lane);
+    load_unit(nxt, rs, i + 1, lane);
     acc += alut_container(cur, tab + (c0 + i) * 32 * 16, std::make_integer_sequence<int, 32>{});
 #pragma unroll
     for (int q = 0; q < 5; ++q) cur[q] = nxt[q];

@@ -38,8 +38,9 @@ struct TwoBit {
   static constexpr int kBytes = kUnit2Bytes;
   static constexpr int kTarget = 20;        // units per wave (1 KB units)
   static constexpr bool kSumCorrection = true;
-  __device__ static void load(uint32_t (&d)[5], __amdgpu_buffer_rsrc_t r, int c, int lane) {
-    const u32x4 h = __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, c * kBytes, kLoadStream);
+  __device__ static void load(uint32_t (&d)[5], const UnitRun& run, int c, int lane) {
+    const u32x4 h =
+        __builtin_amdgcn_raw_buffer_load_b128(run.unit<kBytes>(c), 16 * lane, 0, kLoadStream);
     d[0] = h.x;
     d[1] = h.y;
     d[2] = h.z;
@@ -65,13 +66,8 @@ struct Triple {
   static constexpr int kBytes = kUnitBytes;
   static constexpr int kTarget = 16;
   static constexpr bool kSumCorrection = false;
-  __device__ static void load(uint32_t (&d)[5], __amdgpu_buffer_rsrc_t r, int c, int lane) {
-    const u32x4 h = __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, c * kBytes, kLoadStream);
-    d[0] = h.x;
-    d[1] = h.y;
-    d[2] = h.z;
-    d[3] = h.w;
-    d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, c * kBytes, kLoadStream);
+  __device__ static void load(uint32_t (&d)[5], const UnitRun& run, int c, int lane) {
+    load_unit(d, run, c, lane);
   }
   // Activation bytes 3j .. 3j + 3 of the unit (byte 3 meets the table's zero).
   template <int j>
@@ -161,9 +157,7 @@ __device__ __forceinline__ void cmp_block(const uint8_t* w, const int8_t* x_, co
   const int part = wave - lt * S;
   const int r = g * tpb + lt;
   const int c0 = (r < R) ? (part * C) / S : 0, c1 = (r < R) ? ((part + 1) * C) / S : 0;
-  const __amdgpu_buffer_rsrc_t range = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(w) + (int64_t(r < R ? r : 0) * C + c0) * L::kBytes, 0,
-      (c1 - c0) * L::kBytes, kBufferWord3);
+  const UnitRun range{w + (int64_t(r < R ? r : 0) * C + c0) * L::kBytes, c1 - c0};
   const SHERRY_CONST int32_t* x = as_const(reinterpret_cast<const int32_t*>(x_));
   // 2-bit: sum of the activations of this wave's K range, read by the whole
   // wave before the stream starts

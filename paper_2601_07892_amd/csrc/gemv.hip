@@ -222,43 +222,28 @@ constexpr bool kMfmaSource<XFromLdsMfma> = true;
 template <>
 constexpr bool kMfmaSource<XFromLdsMfmaTok> = true;
 
-// Container c through a buffer resource spanning a wave's containers (reads
-// outside it return zero and never fault): 16-byte head at lane*16, 4-byte
-// tail at 1024 + lane*4, container offset in SGPRs.
-__device__ __forceinline__ void load_container(uint32_t (&d)[5], __amdgpu_buffer_rsrc_t r,
-                                               int c, int lane) {
-  const u32x4 h =
-      __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, c * kUnitBytes, kLoadStream);
-  d[0] = h.x;
-  d[1] = h.y;
-  d[2] = h.z;
-  d[3] = h.w;
-  d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, c * kUnitBytes,
-                                              kLoadStream);
-}
-
 // Streams containers [c0, c1) of one tile through a ring of kRing register
 // slots: slot u is decoded and immediately refilled with the container kRing
-// ahead, so kRing - 1 containers are always in flight.  The resource r spans
-// exactly [c0, c1) (container indices are relative to c0): refills past the
-// end are issued unconditionally and read zeros without touching memory,
-// which keeps the outstanding loads identical on every path so the compiler
-// waits on exact counts; only the decode is skipped past the end.
+// ahead, so kRing - 1 containers are always in flight.  The run spans exactly
+// [c0, c1) (container indices are relative to c0): refills past the end are
+// issued unconditionally and read zeros without touching memory, which keeps
+// the outstanding loads identical on every path so the compiler waits on
+// exact counts; only the decode is skipped past the end.
 // ring_fill issues the first kRing containers; ring_run decodes them all.
-__device__ __forceinline__ void ring_fill(uint32_t (&ring)[kRing][5], __amdgpu_buffer_rsrc_t r) {
+__device__ __forceinline__ void ring_fill(uint32_t (&ring)[kRing][5], const UnitRun& run) {
   const int lane = threadIdx.x & 63;
   // issue the slots strictly in order (head and tail of slot 0 first), so
   // that slot u's loads are always the oldest outstanding ones when it is
   // decoded
 #pragma unroll
   for (int u = 0; u < kRing; ++u) {
-    load_container(ring[u], r, u, lane);
+    load_unit(ring[u], run, u, lane);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 template <class X, class Acc>
-__device__ __forceinline__ void ring_run(uint32_t (&ring)[kRing][5], __amdgpu_buffer_rsrc_t r,
+__device__ __forceinline__ void ring_run(uint32_t (&ring)[kRing][5], const UnitRun& run,
                                          int c0, int c1, const X& xsrc, const uint32_t* lut,
                                          Acc& acc) {
   const int lane = threadIdx.x & 63;
@@ -268,7 +253,7 @@ __device__ __forceinline__ void ring_run(uint32_t (&ring)[kRing][5], __amdgpu_bu
     for (int u = 0; u < kRing; ++u) {
       if (i + u < n) xsrc.dot(ring[u], c0 + i + u, lut, acc);
       __builtin_amdgcn_sched_barrier(0);
-      load_container(ring[u], r, i + u + kRing, lane);
+      load_unit(ring[u], run, i + u + kRing, lane);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -286,7 +271,7 @@ __device__ __forceinline__ float load_group_scale(__amdgpu_buffer_rsrc_t gr, int
 
 template <int M, class X>
 __device__ __forceinline__ void ring_run_groups(uint32_t (&ring)[kRing][5],
-                                                __amdgpu_buffer_rsrc_t r,
+                                                const UnitRun& run,
                                                 __amdgpu_buffer_rsrc_t gr, int G, int c0, int c1,
                                                 const X& xsrc, const uint32_t* lut,
                                                 int32_t (&acc)[M], float (&accf)[M]) {
@@ -310,7 +295,7 @@ __device__ __forceinline__ void ring_run_groups(uint32_t (&ring)[kRing][5],
         }
       }
       __builtin_amdgcn_sched_barrier(0);
-      load_container(ring[u], r, i + u + kRing, lane);
+      load_unit(ring[u], run, i + u + kRing, lane);
       gring[u] = load_group_scale(gr, G, c0 + i + u + kRing, lane);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -345,9 +330,7 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
   for (int m = 0; m < M; ++m) acc[m] = 0;
   // a wave past the last tile streams an empty range (its loads read zeros)
   const int c0 = (r < R) ? (part * C) / S : 0, c1 = (r < R) ? ((part + 1) * C) / S : 0;
-  const __amdgpu_buffer_rsrc_t range = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(w_) + (int64_t(r < R ? r : 0) * C + c0) * kUnitBytes, 0,
-      (c1 - c0) * kUnitBytes, kBufferWord3);
+  const UnitRun range{w_ + (int64_t(r < R ? r : 0) * C + c0) * kUnitBytes, c1 - c0};
   // the prelude (e.g. quantizing the activations) runs to completion before
   // the first weight loads: its few loads then do not queue behind the
   // weight stream of every wave on the GPU; every thread of the block runs it

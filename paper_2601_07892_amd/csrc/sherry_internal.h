@@ -164,6 +164,36 @@ __device__ __forceinline__ SHERRY_GLOBAL T* as_global_mut(T* p) {
 
 // Weight scale of output row n: one per tensor, or, when rows is set, one
 // per output channel ([T alpha]_ij = T_ij alpha_j, the footnote to Eq. 2).
+// A wave's run of n consecutive weight units of B bytes each, from base.
+// Unit c is read through a buffer resource over that unit alone, and an
+// empty one for c >= n: its loads then return zeros without touching memory,
+// since the range check applies to the per-lane offset (soffset is left at
+// zero).  Reads past the run can so be issued on every path, which keeps the
+// compiler's waits on exact load counts; the resource costs scalar
+// instructions only.
+struct UnitRun {
+  const uint8_t* base;
+  int n;
+  template <int B>
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t unit(int c) const {
+    const bool in = c < n;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base) + int64_t(in ? c : 0) * B,
+                                             0, in ? B : 0, kBufferWord3);
+  }
+};
+
+// Unit c of a run in the tiled layout: 16-byte head at lane*16, 4-byte tail
+// at kHeadBytes + lane*4.
+__device__ __forceinline__ void load_unit(uint32_t (&d)[5], const UnitRun& run, int c, int lane) {
+  const __amdgpu_buffer_rsrc_t r = run.unit<kUnitBytes>(c);
+  const u32x4 h = __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, 0, kLoadStream);
+  d[0] = h.x;
+  d[1] = h.y;
+  d[2] = h.z;
+  d[3] = h.w;
+  d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, 0, kLoadStream);
+}
+
 struct WScale {
   const float* rows;
   float tensor;

@@ -73,18 +73,6 @@ __device__ __forceinline__ void sk_wait_vm() {
   __builtin_amdgcn_s_waitcnt(static_cast<int16_t>(kImm));
 }
 
-__device__ __forceinline__ void sk_load_container(uint32_t (&d)[5], __amdgpu_buffer_rsrc_t r,
-                                                  int c, int lane) {
-  const u32x4 h =
-      __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, c * kUnitBytes, kLoadStream);
-  d[0] = h.x;
-  d[1] = h.y;
-  d[2] = h.z;
-  d[3] = h.w;
-  d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, c * kUnitBytes,
-                                              kLoadStream);
-}
-
 // One 16-byte LDS-DMA load per lane: lane i's bytes land at dst + 16 i.
 __device__ __forceinline__ void sk_dma(__amdgpu_buffer_rsrc_t r, int8_t* dst, int voffset) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voffset, 0, 0, 0);
@@ -208,7 +196,8 @@ __device__ __forceinline__ void sk_stage_barrier() {
 //
 // Load order per container step: two weight loads (the ring), then this
 // step's share of the DMA for the chunk NST - 1 ahead.  Both are issued
-// unconditionally (past the end they read zeros or unused rows), so the
+// unconditionally (weight units past the split's end come through an empty
+// resource and read zeros; DMA pieces past k read zeros or unused rows), so the
 // number of loads issued after the last DMA of any chunk is fixed and the
 // wait before that chunk's barrier is a constant vmcnt.
 //
@@ -250,9 +239,8 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   const int sp = wave % S;
   const int u0 = sp * U, u1 = (u0 + U < C) ? u0 + U : C;
   const bool live = r < R && u0 < u1;
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(p.w) + (int64_t(r < R ? r : 0) * C + (live ? u0 : 0)) * kUnitBytes, 0,
-      live ? (u1 - u0) * kUnitBytes : 0, kBufferWord3);
+  const UnitRun rs{p.w + (int64_t(r < R ? r : 0) * C + (live ? u0 : 0)) * kUnitBytes,
+                   live ? u1 - u0 : 0};
   const int nch = (U + UPS - 1) / UPS;
   // the activations of the staged tokens; rows past m read zeros
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
@@ -346,7 +334,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   uint32_t ring[kSkRing][5];
 #pragma unroll
   for (int u = 0; u < kSkRing; ++u) {
-    sk_load_container(ring[u], rs, u, lane);
+    load_unit(ring[u], rs, u, lane);
     if constexpr (GR) load_scales(gsr[u], u);
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -383,7 +371,7 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
         if (ch == chl) clear_tail();
       }
       __builtin_amdgcn_sched_barrier(0);
-      sk_load_container(ring[u], rs, jj + kSkRing, lane);  // container jj's codes are used
+      load_unit(ring[u], rs, jj + kSkRing, lane);  // container jj's codes are used
       __builtin_amdgcn_sched_barrier(0);
       const int wb = sp * WIN / 16 + 8 * pos;  // window piece base (multiple of 8)
       const int8_t* xrow = xlane + (ch % NST) * G::STAGE + 128 * ((wb >> 3) ^ (sw >> 3));

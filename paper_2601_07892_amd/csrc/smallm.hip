@@ -45,23 +45,6 @@ constexpr int kWinPieces = kSmTok * kWinK / 16 / kSmThreads;  // 16-byte pieces 
 constexpr int kSmRing = 4;                      // units per wave in the register ring
 static_assert(kWinUnits % kSmRing == 0, "ring slots repeat in every window");
 
-__device__ __forceinline__ void sm_load(uint32_t (&d)[5], const uint8_t* tile, int c, int C,
-                                        int lane) {
-  // a resource over unit c alone, empty past the tile's last unit: its loads
-  // are issued on every path (the compiler then waits on exact counts) and
-  // past the end return zeros without touching memory
-  const bool in = c < C;
-  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(tile) + int64_t(in ? c : 0) * kUnitBytes, 0, in ? kUnitBytes : 0,
-      kBufferWord3);
-  const u32x4 h = __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane, 0, kLoadStream);
-  d[0] = h.x;
-  d[1] = h.y;
-  d[2] = h.z;
-  d[3] = h.w;
-  d[4] = __builtin_amdgcn_raw_buffer_load_b32(r, kHeadBytes + 4 * lane, 0, kLoadStream);
-}
-
 // Table lookups of codes j0 .. j0 + 15 of a unit row (lane i = row i):
 // wv[j] = the int8x4 weights of code j0 + j.
 template <int j0, int... js>
@@ -146,8 +129,7 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
   const int r = g * kSmWaves + wave;
   const bool live = r < R;
   // this wave's tile (dead waves: no units)
-  const uint8_t* tile = p.w + int64_t(live ? r : 0) * C * kUnitBytes;
-  const int Cw = live ? C : 0;
+  const UnitRun tile{p.w + int64_t(live ? r : 0) * C * kUnitBytes, live ? C : 0};
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<int8_t*>(p.x), 0, p.m * p.k, kBufferWord3);
   const int nwin = (C + kWinUnits - 1) / kWinUnits;
@@ -166,7 +148,7 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
   uint32_t ring[kSmRing][5];
 #pragma unroll
   for (int u = 0; u < kSmRing; ++u) {
-    sm_load(ring[u], tile, u, Cw, lane);
+    load_unit(ring[u], tile, u, lane);
     __builtin_amdgcn_sched_barrier(0);
   }
   if (tid < 32) lut[tid] = decode_word(tid);
@@ -203,7 +185,7 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
         }
       }
       __builtin_amdgcn_sched_barrier(0);
-      sm_load(ring[u % kSmRing], tile, j + kSmRing, Cw, lane);
+      load_unit(ring[u % kSmRing], tile, j + kSmRing, lane);
       __builtin_amdgcn_sched_barrier(0);
     }
     stage_store(sv, stages + ((w + 1) & 1) * kStageBytes);
