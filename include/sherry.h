@@ -227,9 +227,10 @@ int sherry_gemm_channel(const uint8_t* w, const int8_t* x, const float* x_scale,
  * x_scale * sum_g |acc_g * scale| of the exact value, G = ceil(k/128)).
  * acc, if not NULL, receives sum_g acc_g (the unscaled int32 product).
  * kernel: SHERRY_KERNEL_AUTO (GEMV for m <= 4, else register-decoded),
- * SHERRY_KERNEL_GEMV (m <= 4), SHERRY_KERNEL_SKINNY or SHERRY_KERNEL_MFMA
- * (its 128 x 128 tile); SHERRY_E_INVALID for SHERRY_KERNEL_ALUT and if
- * w_group_scales is NULL. */
+ * SHERRY_KERNEL_GEMV (m <= 4), SHERRY_KERNEL_GEMV_TOK (its limits, see
+ * above; the partial sums are the exact per-group products of the lane's
+ * row), SHERRY_KERNEL_SKINNY or SHERRY_KERNEL_MFMA (its 128 x 128 tile);
+ * SHERRY_E_INVALID for SHERRY_KERNEL_ALUT and if w_group_scales is NULL. */
 int sherry_gemm_group(const uint8_t* w, const int8_t* x, const float* x_scale,
                       const float* w_group_scales, float* y, int32_t* acc, int64_t m,
                       int64_t n, int64_t k, int kernel, void* stream);
@@ -272,11 +273,14 @@ int sherry_gemv_batched(const sherry_gemv_desc* descs_dev, int count,
 /* ---------------------------------------------------------------------- */
 /* Grouped products: many independent products (any m, e.g. the q, k and  */
 /* v projections of one layer) in one launch: up to 4 tokens each on the   */
-/* matrix-core GEMV (SHERRY_KERNEL_GEMV_TOK), up to 16 on a 16-token       */
-/* window kernel, else on the register-decoded kernel                      */
+/* matrix-core GEMV (SHERRY_KERNEL_GEMV_TOK), up to 16 (without per-group */
+/* scales) on a 16-token window kernel, else on the register-decoded kernel*/
 /* (SHERRY_KERNEL_SKINNY), which runs token blocks of 32 when every        */
 /* m <= 32 or a descriptor has per-group scales, else of 64.              */
 /* ---------------------------------------------------------------------- */
+
+/* Flag of a grouped launch value: some descriptor has per-group scales. */
+#define SHERRY_LAUNCH_GROUPS (1 << 30)
 
 typedef struct sherry_gemm_desc {
   const uint8_t* w;      /* device, packed n x k, 16-byte aligned          */
@@ -296,14 +300,16 @@ typedef struct sherry_gemm_desc {
 
 /* Host: validates descs[0..count), fills each block_begin, *total_blocks
  * and *max_m, the launch value that selects the kernel and its token
- * blocks.  Without per-group scales: when every m <= 4 and every
- * m * ceil(k/128) * 128 <= 32768, the products run on the matrix-core GEMV
- * (SHERRY_KERNEL_GEMV_TOK) and *max_m is the largest m (1..4); else, when
- * every m <= 16, on the 16-token window kernel (weights as loaded, one int8
- * MFMA per 4-code chunk for 16 tokens x 64 rows) and *max_m is the largest
- * m, at least 5.  Otherwise they run on the register-decoded kernel and
- * *max_m is the largest m, at least 17, and at most 32 when a descriptor
- * carries per-group scales (their kernel runs 32-token blocks).  Pass it to
+ * blocks.  When every m <= 4 and every m * ceil(k/128) * 128 <= 32768, the
+ * products run on the matrix-core GEMV (SHERRY_KERNEL_GEMV_TOK, any scales)
+ * and *max_m is the largest m (1..4); else, when every m <= 16 and no
+ * descriptor has per-group scales, on the 16-token window kernel (weights as
+ * loaded, one int8 MFMA per 4-code chunk for 16 tokens x 64 rows) and *max_m
+ * is the largest m, at least 5.  Otherwise they run on the register-decoded
+ * kernel and *max_m is the largest m, at least 17, and at most 32 when a
+ * descriptor carries per-group scales (their kernel runs 32-token blocks).
+ * When a descriptor carries per-group scales, *max_m also has the bit
+ * SHERRY_LAUNCH_GROUPS set (the kernels' per-group variants).  Pass it to
  * sherry_gemm_batched unchanged. */
 int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
                                 int64_t* total_blocks, int32_t* max_m);

@@ -29,6 +29,7 @@ SHERRY_KERNEL_MFMA = 2
 SHERRY_KERNEL_SKINNY = 3
 SHERRY_KERNEL_ALUT = 4
 SHERRY_KERNEL_GEMV_TOK = 5
+SHERRY_LAUNCH_GROUPS = 1 << 30  # flag of a grouped launch value: per-group scales
 SHERRY_ALUT_MAX_K = 8192
 SHERRY_MAX_K = 174720
 SHERRY_MAX_M = 1 << 24

@@ -161,7 +161,7 @@ int gemm_dispatch(const uint8_t* w, const int8_t* x, const float* x_scale, WScal
     if (st != SHERRY_OK) return st;
     if (!gemv_tok_fits(m, k)) return SHERRY_E_SHAPE;
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
-    return launch_gemv_tok(w, x, x_scale, ws, y, acc, m, n, k, as_stream(stream));
+    return launch_gemv_tok(w, x, x_scale, ws, nullptr, y, acc, m, n, k, as_stream(stream));
   }
   if (kernel == SHERRY_KERNEL_ALUT) {
     int st = check_product(w, x, x_scale, y, m, n, k, 4);
@@ -192,6 +192,14 @@ extern "C" int sherry_gemm_group(const uint8_t* w, const int8_t* x, const float*
     if (m > kGemvMaxM) return SHERRY_E_SHAPE;
     if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
     return launch_gemv_group(w, x, x_scale, w_group_scales, y, acc, m, n, k, as_stream(stream));
+  }
+  if (kernel == SHERRY_KERNEL_GEMV_TOK) {
+    int st = check_product(w, x, x_scale, y, m, n, k, 4);
+    if (st != SHERRY_OK) return st;
+    if (!gemv_tok_fits(m, k)) return SHERRY_E_SHAPE;
+    if (acc && !aligned(acc, 4)) return SHERRY_E_ALIGN;
+    return launch_gemv_tok(w, x, x_scale, WScale{nullptr, 0.0f}, w_group_scales, y, acc, m, n, k,
+                           as_stream(stream));
   }
   if (kernel == SHERRY_KERNEL_SKINNY) {
     int st = check_product(w, x, x_scale, y, m, n, k, 16);
@@ -413,10 +421,11 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
     if (d.m > mm) mm = d.m;
   }
   // The launch value *max_m selects the kernel: 1-4 the 4-token matrix-core
-  // GEMV (every m <= 4 and every product's activations fit its LDS staging),
-  // 5-16 the 16-token window kernel (every m <= 16), 17 and more the
-  // register-decoded kernel (any m; the only one for per-group scales).
-  bool tok = !grouped && mm <= 4;
+  // GEMV (every m <= 4 and every product's activations fit its LDS staging;
+  // any scales), 5-16 the 16-token window kernel (every m <= 16, no
+  // per-group scales), 17 and more the register-decoded kernel (any m, any
+  // scales).
+  bool tok = mm <= 4;
   for (int i = 0; tok && i < count; ++i) tok = gemv_tok_fits(descs[i].m, descs[i].k);
   const bool small = !grouped && mm <= 16;
   int64_t blocks = 0;
@@ -429,7 +438,7 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
       if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
     }
     *total_blocks = blocks;
-    *max_m = tok ? mm : (mm < 5 ? 5 : mm);
+    *max_m = (tok ? mm : (mm < 5 ? 5 : mm)) | (grouped ? SHERRY_LAUNCH_GROUPS : 0);
     return SHERRY_OK;
   }
   // otherwise every product runs on the register-decoded kernel in token
@@ -445,7 +454,7 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
     if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
   }
   *total_blocks = blocks;
-  *max_m = sel;
+  *max_m = sel | (grouped ? SHERRY_LAUNCH_GROUPS : 0);
   return SHERRY_OK;
 }
 
@@ -453,10 +462,16 @@ extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
                                    int64_t total_blocks, int32_t max_m, void* stream) {
   if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
     return SHERRY_E_INVALID;
+  const bool groups = (max_m & SHERRY_LAUNCH_GROUPS) != 0;
+  max_m &= ~SHERRY_LAUNCH_GROUPS;
   if (max_m < 1 || max_m > SHERRY_MAX_M) return SHERRY_E_SHAPE;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
-  if (max_m <= 4) return launch_gemv_tok_batched(descs_dev, count, total_blocks, as_stream(stream));
-  if (max_m <= 16) return launch_smallm_batched(descs_dev, count, total_blocks, as_stream(stream));
+  if (max_m <= 4)
+    return launch_gemv_tok_batched(descs_dev, count, total_blocks, groups, as_stream(stream));
+  if (max_m <= 16) {
+    if (groups) return SHERRY_E_INVALID;  // prepare never selects this
+    return launch_smallm_batched(descs_dev, count, total_blocks, as_stream(stream));
+  }
   return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
 }
 

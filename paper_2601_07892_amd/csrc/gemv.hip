@@ -121,8 +121,9 @@ __device__ __forceinline__ void dot_container_lds(const uint32_t (&d)[5], const 
 // every other lane, so D[i][t] sums row 16i + t of the tile and nothing else
 // (rows i >= 4 of D stay zero).  Only the lanes with own set read the
 // activations at xv into xw; the other lanes' xw hold zeros throughout.  Two
-// accumulators take alternate chunks.
-template <int g>
+// accumulators take alternate chunks; with kChain one accumulator takes all
+// of them, starting from zero (a container's sum on its own).
+template <int g, bool kChain = false>
 __device__ __forceinline__ void dot_container_mfma(const uint32_t (&d)[5], const u32x4* xv,
                                                    bool own, u32x4 (&xw)[4], const uint32_t* lut,
                                                    v4i (&acc)[2]) {
@@ -144,9 +145,14 @@ __device__ __forceinline__ void dot_container_mfma(const uint32_t (&d)[5], const
                      static_cast<int>(xw[q].z), static_cast<int>(xw[q].w)};
       const v4i b = {static_cast<int>(wv[4 * q]), static_cast<int>(wv[4 * q + 1]),
                      static_cast<int>(wv[4 * q + 2]), static_cast<int>(wv[4 * q + 3])};
-      acc[q & 1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc[q & 1], 0, 0, 0);
+      if constexpr (kChain) {
+        const v4i cin = (g == 0 && q == 0) ? v4i{0, 0, 0, 0} : acc[0];
+        acc[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, cin, 0, 0, 0);
+      } else {
+        acc[q & 1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc[q & 1], 0, 0, 0);
+      }
     }
-    dot_container_mfma<g + 16>(d, xv, own, xw, lut, acc);
+    dot_container_mfma<g + 16, kChain>(d, xv, own, xw, lut, acc);
   }
 }
 
@@ -212,6 +218,16 @@ struct XFromLdsMfmaTok {
     const bool own = m >= 0 && m < m_count;
     dot_container_mfma<0>(d, reinterpret_cast<const u32x4*>(xq + (own ? m : 0) * kp + c * kTileK),
                           own, xw, lut, acc);
+  }
+  // container c's sums alone, in acc[0]
+  __device__ __forceinline__ void dot_one(const uint32_t (&d)[5], int c, const uint32_t* lut,
+                                          v4i (&acc)[2]) const {
+    const int lane = threadIdx.x & 63;
+    const int m = (lane & 15) - 4 * (lane >> 4);
+    const bool own = m >= 0 && m < m_count;
+    dot_container_mfma<0, true>(
+        d, reinterpret_cast<const u32x4*>(xq + (own ? m : 0) * kp + c * kTileK), own, xw, lut,
+        acc);
   }
 };
 
@@ -302,6 +318,108 @@ __device__ __forceinline__ void ring_run_groups(uint32_t (&ring)[kRing][5],
   }
 }
 
+// Per-group scales on the 4-token matrix-core source: each container's MFMAs
+// run as one chain from zero (slot u of the ring accumulates in pend[u]),
+// and the lane's own row's M token sums (elements 0..M-1) are scaled by the
+// row's group scale into fp32 accumulators (ascending container order) and
+// added to the int32 totals, as in ring_run_groups.  A container is scaled
+// one step after its MFMAs were issued, once the next container's are in
+// flight, so the chain's latency is not waited for; the walk runs one step
+// past the last container for that (its loads read zeros).
+template <int M, class X>
+__device__ __forceinline__ void ring_run_groups_mfma(uint32_t (&ring)[kRing][5],
+                                                     const UnitRun& run,
+                                                     __amdgpu_buffer_rsrc_t gr, int G, int c0,
+                                                     int c1, const X& xsrc, const uint32_t* lut,
+                                                     int32_t (&acc)[M], float (&accf)[M]) {
+  const int lane = threadIdx.x & 63;
+  const int n = c1 - c0;
+  float gring[kRing], gpend[kRing] = {};
+  v4i pend[kRing][2] = {};
+#pragma unroll
+  for (int u = 0; u < kRing; ++u) gring[u] = load_group_scale(gr, G, c0 + u, lane);
+  for (int i = 0; i <= n; i += kRing) {
+#pragma unroll
+    for (int u = 0; u < kRing; ++u) {
+      const int j = i + u;
+      if (j < n) {
+        xsrc.dot_one(ring[u], c0 + j, lut, pend[u]);
+        gpend[u] = gring[u];
+      }
+      // container j - 1, in the previous slot
+      const int pu = (u + kRing - 1) % kRing;  // a constant once unrolled
+      if (j >= 1 && j <= n) {
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          const int32_t a = pend[pu][0][m];
+          accf[m] = __builtin_fmaf(static_cast<float>(a), gpend[pu], accf[m]);
+          acc[m] += a;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      load_unit(ring[u], run, j + kRing, lane);
+      gring[u] = load_group_scale(gr, G, c0 + j + kRing, lane);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// The same with 16-byte scale loads: a ring of four containers, and lane l
+// reads the scales of its row for four containers at once (one load per
+// round of four, issued two rounds ahead), which touches a quarter of the
+// cache lines of one 4-byte load per container.  Needs every row's scales
+// 16-byte aligned (G % 4 == 0, gs 16-byte aligned) and c0 % 4 == 0.
+constexpr int kGRing = 4;
+
+template <int M, class X>
+__device__ __forceinline__ void ring_run_groups_mfma4(const UnitRun& run,
+                                                      __amdgpu_buffer_rsrc_t gr, int G, int c0,
+                                                      int c1, const X& xsrc, const uint32_t* lut,
+                                                      int32_t (&acc)[M], float (&accf)[M]) {
+  const int lane = threadIdx.x & 63;
+  const int n = c1 - c0;
+  uint32_t ring[kGRing][5];
+#pragma unroll
+  for (int u = 0; u < kGRing; ++u) {
+    load_unit(ring[u], run, u, lane);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // scales of rounds 0 and 1 (containers c0 .. c0 + 7 of the lane's row)
+  u32x4 gq0 = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * G + c0), 0, 0);
+  u32x4 gq1 = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * G + c0 + kGRing), 0, 0);
+  // sums and scale of the current and the previous container
+  float gpend[2] = {0.0f, 0.0f};
+  v4i pend[2][2] = {};
+  for (int i = 0; i <= n; i += kGRing) {
+    const u32x4 gcur = gq0;
+    gq0 = gq1;
+    gq1 = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * G + c0 + i + 2 * kGRing), 0, 0);
+#pragma unroll
+    for (int u = 0; u < kGRing; ++u) {
+      const int j = i + u;
+      if (j < n) {
+        xsrc.dot_one(ring[u], c0 + j, lut, pend[u & 1]);
+        const uint32_t gbits = gcur[u];  // (a bit cast of the element itself
+                                         // reads element 0 with this compiler)
+        gpend[u & 1] = __uint_as_float(gbits);
+      }
+      // container j - 1, in the previous slot
+      const int pu = (u + 1) & 1;  // a constant once unrolled (kGRing is even)
+      if (j >= 1 && j <= n) {
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          const int32_t a = pend[pu][0][m];
+          accf[m] = __builtin_fmaf(static_cast<float>(a), gpend[pu], accf[m]);
+          acc[m] += a;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      load_unit(ring[u], run, j + kGRing, lane);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
 // One workgroup of a product: block g of a problem whose tiles are split
 // over S waves each.  prelude.issue() then prelude.finish(sx) run before the
 // weight stream; finish yields the tokens' activation scales sx[m].  lut and red are
@@ -346,8 +464,6 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
     if (r0 < R && row0 < n) sw0 = as_global(ws.rows)[row0];
   }
   __builtin_amdgcn_sched_barrier(0);
-  uint32_t ring[kRing][5];
-  ring_fill(ring, range);
   float accf[M];
   if constexpr (kGrp) {
     // scale rows of this wave's tile (rows past n read zero)
@@ -357,9 +473,34 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
         (rows < kTileRows ? rows : kTileRows) * C * 4, kBufferWord3);
 #pragma unroll
     for (int m = 0; m < M; ++m) accf[m] = 0.0f;
-    ring_run_groups<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
+    if constexpr (kMfmaSource<X>) {
+      static_assert(std::is_same_v<X, XFromLdsMfmaTok>,
+                    "per-group scales on the matrix cores: the token source only");
+      if (C % 4 == 0 && (reinterpret_cast<uintptr_t>(gs) & 15) == 0) {
+        // 16-byte scale loads: the parts of the tile start at multiples of
+        // four containers
+        auto bound = [&](int p) { return p >= S ? C : ((p * C) / S) & ~3; };
+        const int b0 = (r < R) ? bound(part) : 0, b1 = (r < R) ? bound(part + 1) : 0;
+        const UnitRun run4{w_ + (int64_t(r < R ? r : 0) * C + b0) * kUnitBytes, b1 - b0};
+        ring_run_groups_mfma4<M>(run4, gr, C, b0, b1, xsrc, lut, acc, accf);
+      } else {
+        uint32_t ring[kRing][5];
+        ring_fill(ring, range);
+        ring_run_groups_mfma<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
+      }
+      // the LDS of the activations is reused: every wave has finished reading it
+      __syncthreads();
+#pragma unroll
+      for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + lane] = acc[m];
+    } else {
+      uint32_t ring[kRing][5];
+      ring_fill(ring, range);
+      ring_run_groups<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
+    }
   } else if constexpr (kMfmaSource<X>) {
     static_assert(M <= 4 && !kGrp, "the matrix-core sources serve up to four tokens");
+    uint32_t ring[kRing][5];
+    ring_fill(ring, range);
     v4i macc[2] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
     ring_run(ring, range, c0, c1, xsrc, lut, macc);
     if constexpr (std::is_same_v<X, XFromLdsMfma>) {
@@ -375,6 +516,8 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
       for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + lane] = macc[0][m] + macc[1][m];
     }
   } else {
+    uint32_t ring[kRing][5];
+    ring_fill(ring, range);
     ring_run(ring, range, c0, c1, xsrc, lut, acc);
   }
 
@@ -502,33 +645,45 @@ struct StageRows {
   }
 };
 
-template <int M>
+// LDS of the 4-token kernels: the staged activation rows, which after the
+// stream hold the int32 partial sums (first 8 KB) and, with per-group scales,
+// the fp32 ones (next 8 KB).
+static_assert(2 * kGemvWaves * 4 * 64 * 4 <= kTokMaxBytes, "partial sums fit the staging");
+__device__ __forceinline__ float* tok_redf(int8_t* xq) {
+  return reinterpret_cast<float*>(xq + kGemvWaves * 4 * 64 * 4);
+}
+
+template <int M, bool kGrp>
 __global__ __launch_bounds__(kGemvThreads) void gemv_tok_kernel(
     const uint8_t* __restrict__ w, const int8_t* __restrict__ x,
-    const float* __restrict__ x_scale, WScale ws, float* __restrict__ y,
-    int32_t* __restrict__ acc, int64_t n, int64_t k, int split) {
+    const float* __restrict__ x_scale, WScale ws, const float* __restrict__ gs,
+    float* __restrict__ y, int32_t* __restrict__ acc, int64_t n, int64_t k, int split) {
   __shared__ uint32_t lut[32];
   __shared__ __attribute__((aligned(16))) int8_t xq[kTokMaxBytes];
   fill_lut(lut);
   const int kp = static_cast<int>((k + kTileK - 1) / kTileK) * kTileK;
-  gemv_block<M>(w, XFromLdsMfmaTok{xq, kp, M},
-                StageRows<M>{x, x_scale, static_cast<int>(k), kp, xq}, ws, y, acc, n,
-                static_cast<int>(k), blockIdx.x, split, lut, reinterpret_cast<int32_t*>(xq));
+  gemv_block<M, kGrp>(w, XFromLdsMfmaTok{xq, kp, M},
+                      StageRows<M>{x, x_scale, static_cast<int>(k), kp, xq}, ws, y, acc, n,
+                      static_cast<int>(k), blockIdx.x, split, lut,
+                      reinterpret_cast<int32_t*>(xq), gs, tok_redf(xq));
 }
 
-template <int M>
+template <int M, bool kGrp>
 __device__ __forceinline__ void tok_batched_block(const sherry_gemm_desc& d, int g,
                                                   const uint32_t* lut, int8_t* xq) {
   const int k = static_cast<int>(d.k);
   const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
   const int S = gemv_split((k + kTileK - 1) / kTileK);
-  gemv_block<M>(d.w, XFromLdsMfmaTok{xq, kp, M}, StageRows<M>{d.x, d.x_scale, k, kp, xq},
-                WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k, g, S, lut,
-                reinterpret_cast<int32_t*>(xq));
+  gemv_block<M, kGrp>(d.w, XFromLdsMfmaTok{xq, kp, M}, StageRows<M>{d.x, d.x_scale, k, kp, xq},
+                      WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k, g, S, lut,
+                      reinterpret_cast<int32_t*>(xq), d.w_group_scales, tok_redf(xq));
 }
 
-// Grouped products of up to four tokens each (sherry_gemm_desc, no
-// per-group scales, m * ceil(k/128) * 128 <= kTokMaxBytes).
+// Grouped products of up to four tokens each (sherry_gemm_desc,
+// m * ceil(k/128) * 128 <= kTokMaxBytes): per-tensor and per-channel scales,
+// and with kGroups also per-group ones (a kernel of its own, so that the
+// others keep the registers of the plain stream).
+template <bool kGroups>
 __global__ __launch_bounds__(kGemvThreads) void gemv_tok_batched_kernel(
     const sherry_gemm_desc* __restrict__ descs, int count) {
   __shared__ uint32_t lut[32];
@@ -547,11 +702,20 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_tok_batched_kernel(
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
   const int g = blk - d.block_begin;
-  switch (d.m) {
-    case 1: tok_batched_block<1>(d, g, lut, xq); break;
-    case 2: tok_batched_block<2>(d, g, lut, xq); break;
-    case 3: tok_batched_block<3>(d, g, lut, xq); break;
-    default: tok_batched_block<4>(d, g, lut, xq); break;
+  if (kGroups && d.w_group_scales) {
+    switch (d.m) {
+      case 1: tok_batched_block<1, kGroups>(d, g, lut, xq); break;
+      case 2: tok_batched_block<2, kGroups>(d, g, lut, xq); break;
+      case 3: tok_batched_block<3, kGroups>(d, g, lut, xq); break;
+      default: tok_batched_block<4, kGroups>(d, g, lut, xq); break;
+    }
+  } else {
+    switch (d.m) {
+      case 1: tok_batched_block<1, false>(d, g, lut, xq); break;
+      case 2: tok_batched_block<2, false>(d, g, lut, xq); break;
+      case 3: tok_batched_block<3, false>(d, g, lut, xq); break;
+      default: tok_batched_block<4, false>(d, g, lut, xq); break;
+    }
   }
 }
 
@@ -818,19 +982,28 @@ bool gemv_tok_fits(int64_t m, int64_t k) {
   return m >= 1 && m <= 4 && m * ceil_div(k, kTileK) * kTileK <= kTokMaxBytes;
 }
 
-int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws, float* y,
-                    int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s) {
+int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
+                    const float* gs, float* y, int32_t* acc, int64_t m, int64_t n, int64_t k,
+                    hipStream_t s) {
   if (!gemv_tok_fits(m, k)) return SHERRY_E_SHAPE;
   const int64_t R = ceil_div(n, kTileRows);
   const int C = static_cast<int>(ceil_div(k, kTileK));
   const int S = (R * gemv_split(C) >= 4096) ? gemv_split(C) : kGemvWaves;
   const dim3 grid(static_cast<unsigned>(ceil_div(R * S, kGemvWaves)));
   const dim3 block(kGemvThreads);
+  if (gs) {
+    switch (m) {
+      case 1: return launch(gemv_tok_kernel<1, true>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
+      case 2: return launch(gemv_tok_kernel<2, true>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
+      case 3: return launch(gemv_tok_kernel<3, true>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
+      default: return launch(gemv_tok_kernel<4, true>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
+    }
+  }
   switch (m) {
-    case 1: return launch(gemv_tok_kernel<1>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
-    case 2: return launch(gemv_tok_kernel<2>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
-    case 3: return launch(gemv_tok_kernel<3>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
-    default: return launch(gemv_tok_kernel<4>, grid, block, 0, s, w, x, x_scale, ws, y, acc, n, k, S);
+    case 1: return launch(gemv_tok_kernel<1, false>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
+    case 2: return launch(gemv_tok_kernel<2, false>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
+    case 3: return launch(gemv_tok_kernel<3, false>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
+    default: return launch(gemv_tok_kernel<4, false>, grid, block, 0, s, w, x, x_scale, ws, gs, y, acc, n, k, S);
   }
 }
 
@@ -840,8 +1013,11 @@ int64_t gemv_tok_blocks(int64_t n, int64_t k) {
 }
 
 int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
-                            hipStream_t s) {
-  return launch(gemv_tok_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
+                            bool groups, hipStream_t s) {
+  if (groups)
+    return launch(gemv_tok_batched_kernel<true>, dim3(static_cast<unsigned>(total_blocks)),
+                  dim3(kGemvThreads), 0, s, descs, count);
+  return launch(gemv_tok_batched_kernel<false>, dim3(static_cast<unsigned>(total_blocks)),
                 dim3(kGemvThreads), 0, s, descs, count);
 }
 

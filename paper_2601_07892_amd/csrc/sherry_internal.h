@@ -221,14 +221,15 @@ int launch_gemv_alut(const uint8_t* w, const int8_t* x, const float* x_scale, WS
 
 // Up to four tokens on the matrix cores, activations staged in LDS
 // (m * ceil(k/128) * 128 <= 32768 bytes, gemv_tok_fits): single and grouped
-// launches; gemv_tok_blocks is one product's workgroup count in a grouped
-// launch.
+// launches, per-tensor, per-channel or (gs != nullptr) per-group scales;
+// gemv_tok_blocks is one product's workgroup count in a grouped launch.
 bool gemv_tok_fits(int64_t m, int64_t k);
-int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws, float* y,
-                    int32_t* acc, int64_t m, int64_t n, int64_t k, hipStream_t s);
+int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WScale ws,
+                    const float* gs, float* y, int32_t* acc, int64_t m, int64_t n, int64_t k,
+                    hipStream_t s);
 int64_t gemv_tok_blocks(int64_t n, int64_t k);
 int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
-                            hipStream_t s);
+                            bool groups, hipStream_t s);
 
 // Up to 16 tokens on the matrix cores, weights as loaded, activations
 // staged per K window (grouped launches): one product's workgroup count, and

@@ -274,9 +274,13 @@ def test_gemm_batched_prepare_picks_the_token_gemv():
     assert prep([(4, 3072, 8320), (1, 64, 128)]) == ([0, 12], 13, 5)
     assert prep([(5, 64, 128)]) == ([0], 1, 5)
     assert prep([(16, 3072, 8192), (9, 1024, 3072)]) == ([0, 12], 16, 16)
-    # per-group scales, or more than 16 tokens: the register-decoded kernel
-    # (launch value at least 17)
-    assert prep([(2, 64, 128), (1, 64, 128)], group=True)[2] == 17
+    # per-group scales up to 4 tokens stay on the token GEMV; with more
+    # tokens, or more than 16 tokens, the register-decoded kernel (launch
+    # value at least 17)
+    G = sh.SHERRY_LAUNCH_GROUPS  # set in the launch value with per-group scales
+    assert prep([(2, 64, 128), (1, 64, 128)], group=True)[2] == 2 | G
+    assert prep([(5, 64, 128), (1, 64, 128)], group=True)[2] == 17 | G
+    assert prep([(4, 3072, 8320)], group=True)[2] == 17 | G
     assert prep([(17, 64, 128)])[2] == 17
 
 
@@ -379,6 +383,12 @@ def test_skinny_validation_without_launch():
     assert L.sherry_gemm_batched(FAKE, 1, 1, 0, None) == sh.SHERRY_E_SHAPE
     assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 16, None) == sh.SHERRY_E_ALIGN
     assert L.sherry_gemm_batched(None, 1, 1, 16, None) == sh.SHERRY_E_INVALID
+    # the per-group flag: never with the window kernel's values (5-16), and
+    # the value under it is checked as without it
+    G = sh.SHERRY_LAUNCH_GROUPS
+    assert L.sherry_gemm_batched(FAKE, 1, 1, 16 | G, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_gemm_batched(FAKE, 1, 1, 0 | G, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 4 | G, None) == sh.SHERRY_E_ALIGN
 
 
 def test_channel_and_ternarize_validation_without_launch():
@@ -475,7 +485,7 @@ def test_grouped_per_group_scales_validation():
     # a descriptor with per-group scales makes the launch run 32-token blocks
     # and splits its tiles' K in two (4 tiles per workgroup):
     # 32 tiles -> 4 x 1 block; 128 tiles -> 32 x 4 token blocks; 2 tiles -> 1
-    assert max_m == 32
+    assert max_m == 32 | sh.SHERRY_LAUNCH_GROUPS
     assert [d.block_begin for d in descs] == [0, 4, 132] and total == 133
     descs[1].acc = FAKE  # no int32 totals with per-group scales
     with pytest.raises(sh.SherryError):

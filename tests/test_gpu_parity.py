@@ -864,7 +864,7 @@ def test_skinny_batched_group_scales(dev):
             d.acc = a.data_ptr()
         keep.append((t, q, sx, w, qd, sxd, y, a, extra))
     total, max_m = sh.sherry_gemm_batched_prepare(descs)
-    assert max_m == 32
+    assert max_m == 32 | sh.SHERRY_LAUNCH_GROUPS
     dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
     sh.sherry_gemm_batched(dd, len(cases), total, max_m)
     torch.cuda.synchronize()

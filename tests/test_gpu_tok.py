@@ -1,8 +1,9 @@
 """GPU parity of the small-M matrix-core kernels against the CPU oracle: the
 GEMV for up to four tokens (SHERRY_KERNEL_GEMV_TOK: activations staged in
-LDS, one int8 MFMA per 4-code chunk), single and grouped launches, and the
-16-token window kernel of grouped launches: int32 accumulators bit-exact, fp32
-outputs within 1e-5 relative."""
+LDS, one int8 MFMA per 4-code chunk), single and grouped launches, with
+per-tensor, per-channel and per-group scales, and the 16-token window kernel
+of grouped launches: int32 accumulators bit-exact, fp32 outputs within 1e-5
+relative (per-group scales: within the fp32-sum bound of sherry_gemm_group)."""
 import sys
 
 import numpy as np
@@ -113,7 +114,55 @@ def test_tok_kernel_rejects_what_it_cannot_stage(dev):
             sh.SHERRY_E_SHAPE
 
 
-def _grouped(dev, cases, seed, channel=False):
+def _group_scales(n, k, seed):
+    rng = np.random.default_rng(seed)
+    return (rng.random((n, (k + 127) // 128)) * 0.05 + 0.001).astype(np.float32)
+
+
+def _group_ok(y, y_ref, mag, k):
+    # fp32 summation in any order: |y - y_ref| <= (G + 4) * 2^-24 * mag
+    bound = ((k + 127) // 128 + 4) * 2.0 ** -24 * mag + 1e-30
+    return bool(np.all(np.abs(np.asarray(y, np.float64) - y_ref) <= bound))
+
+
+# per-group scales on the token kernel: ragged n, a partial last group, K
+# split over several waves, the longest k each m can stage
+GROUP_TOK_CASES = [(1, 70, 132), (2, 65, 1028), (3, 130, 3076), (4, 600, 2048), (4, 3072, 8192),
+                   (1, 64, 32768), (2, 257, 16380)]
+
+
+@pytest.mark.parametrize("m,n,k", GROUP_TOK_CASES)
+def test_tok_kernel_group_scales(dev, m, n, k):
+    sh = _sh()
+    _say("tok group", m, n, k)
+    t = synth.ternary_34(n, k, 81, "tgr", n, k)
+    q = synth.int8_any(m, k, 81, "tgrq", m, k)
+    sx = _scales(m, 81, "tgrs%d" % m)
+    gs = _group_scales(n, k, 81 + n)
+    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
+    acc = torch.full((m, n), -7, dtype=torch.int32, device=dev)
+    sh.sherry_gemm_group(w, torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev),
+                         torch.from_numpy(gs).to(dev), y, acc, m, n, k, sh.SHERRY_KERNEL_GEMV_TOK)
+    torch.cuda.synchronize()
+    y_ref, mag, acc_ref = oracle.product_groups(q, t, sx, gs, threads=ORACLE_THREADS)
+    assert np.array_equal(acc.cpu().numpy(), acc_ref)
+    assert _group_ok(y.cpu().numpy(), y_ref, mag, k)
+
+
+def test_tok_kernel_group_scales_rejects_long_rows(dev):
+    sh = _sh()
+    w = torch.zeros(sh.sherry_packed_bytes(64, 8320), dtype=torch.uint8, device=dev)
+    x = torch.zeros((4, 8320), dtype=torch.int8, device=dev)
+    sx = torch.ones(4, dtype=torch.float32, device=dev)
+    gs = torch.ones((64, 65), dtype=torch.float32, device=dev)
+    y = torch.empty((4, 64), dtype=torch.float32, device=dev)
+    assert sh.lib.sherry_gemm_group(w.data_ptr(), x.data_ptr(), sx.data_ptr(), gs.data_ptr(),
+                                    y.data_ptr(), None, 4, 64, 8320, sh.SHERRY_KERNEL_GEMV_TOK,
+                                    None) == sh.SHERRY_E_SHAPE
+
+
+def _grouped(dev, cases, seed, channel=False, groups=False):
     sh = _sh()
     descs = (sh.sherry_gemm_desc * len(cases))()
     keep = []
@@ -134,12 +183,22 @@ def _grouped(dev, cases, seed, channel=False):
             sw = (np.random.default_rng(seed + i).random(n) * 0.05 + 0.001).astype(np.float32)
             hold = torch.from_numpy(sw).to(dev)
             d.w_scales = hold.data_ptr()
+        elif groups and i % 3 != 2:
+            # per-group scales (no int32 totals with them)
+            sw = ("groups", _group_scales(n, k, seed + i))
+            hold = torch.from_numpy(sw[1]).to(dev)
+            d.w_group_scales, d.acc = hold.data_ptr(), None
         keep.append((t, q, sx, sw, d.acc is not None, w, qd, sxd, y, a, hold))
     total, max_m = sh.sherry_gemm_batched_prepare(descs)
     dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
     sh.sherry_gemm_batched(dd, len(cases), total, max_m)
     torch.cuda.synchronize()
     for t, q, sx, sw, has_acc, w, qd, sxd, y, a, hold in keep:
+        if isinstance(sw, tuple):
+            y_ref, mag, _ = oracle.product_groups(q, t, sx, sw[1], threads=ORACLE_THREADS)
+            assert (a.cpu().numpy() == -7).all()
+            assert _group_ok(y.cpu().numpy(), y_ref, mag, t.shape[1])
+            continue
         acc_ref = oracle.gemm_i32(q, t, threads=ORACLE_THREADS)
         if has_acc:
             assert np.array_equal(a.cpu().numpy(), acc_ref)
@@ -155,6 +214,23 @@ def test_tok_batched_parity(dev, channel):
     _say("tok batched", channel)
     cases = [(1 + i % 4, 64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700)) for i in range(70)]
     assert _grouped(dev, cases, 73, channel) == 4
+
+
+def test_tok_batched_group_scales(dev):
+    # 70 products of 1-4 tokens, two in three with per-group scales, the
+    # rest per-channel or per-tensor: all on the token kernel
+    _say("tok batched groups")
+    cases = [(1 + i % 4, 64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700)) for i in range(70)]
+    assert _grouped(dev, cases, 82, channel=False, groups=True) == 4 | _sh().SHERRY_LAUNCH_GROUPS
+
+
+def test_tok_batched_group_scales_model_step_full(dev):
+    # one LLaMA-3.2-3B layer at 4 tokens with per-group scales, every output
+    _say("tok batched groups 3b layer")
+    spec = synth.LLAMA_3B
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    assert _grouped(dev, [(4, lin.n, lin.k) for lin in blk], 83, groups=True) == \
+        4 | _sh().SHERRY_LAUNCH_GROUPS
 
 
 @pytest.mark.parametrize("m", [2, 4])
