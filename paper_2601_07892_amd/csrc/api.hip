@@ -422,12 +422,20 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
   }
   // The launch value *max_m selects the kernel: 1-4 the 4-token matrix-core
   // GEMV (every m <= 4 and every product's activations fit its LDS staging;
-  // any scales), 5-16 the 16-token window kernel (every m <= 16, no
-  // per-group scales), 17 and more the register-decoded kernel (any m, any
-  // scales).
+  // any scales), 5-16 the 16-token window kernel (every m <= 16; per-group
+  // scales with k % 512 == 0, 16-byte aligned), 17 and more the
+  // register-decoded kernel (any m, any scales); SHERRY_LAUNCH_GROUPS marks
+  // per-group scales.
   bool tok = mm <= 4;
   for (int i = 0; tok && i < count; ++i) tok = gemv_tok_fits(descs[i].m, descs[i].k);
-  const bool small = !grouped && mm <= 16;
+  // the window kernel takes per-group scales of 16-byte aligned rows of a
+  // multiple of 4 units (k % 512 == 0)
+  bool small = mm <= 16;
+  for (int i = 0; small && i < count; ++i) {
+    const sherry_gemm_desc& d = descs[i];
+    if (d.w_group_scales && (ceil_div(int64_t(d.k), kTileK) % 4 != 0 || !aligned(d.w_group_scales, 16)))
+      small = false;
+  }
   int64_t blocks = 0;
   if (tok || small) {
     for (int i = 0; i < count; ++i) {
@@ -468,10 +476,8 @@ extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
   if (max_m <= 4)
     return launch_gemv_tok_batched(descs_dev, count, total_blocks, groups, as_stream(stream));
-  if (max_m <= 16) {
-    if (groups) return SHERRY_E_INVALID;  // prepare never selects this
-    return launch_smallm_batched(descs_dev, count, total_blocks, as_stream(stream));
-  }
+  if (max_m <= 16)
+    return launch_smallm_batched(descs_dev, count, total_blocks, groups, as_stream(stream));
   return launch_skinny_batched(descs_dev, count, total_blocks, max_m, as_stream(stream));
 }
 

@@ -236,7 +236,7 @@ int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t to
 // the launch.
 int64_t smallm_blocks(int64_t n);
 int launch_smallm_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
-                          hipStream_t s);
+                          bool groups, hipStream_t s);
 
 int skinny_blocks(int64_t n, bool group_scales = false);
 int skinny_batched_tokens(int max_m);

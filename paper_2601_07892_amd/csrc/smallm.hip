@@ -114,12 +114,22 @@ struct SmProblem {
   int32_t* acc;
   int n, k, m;
   WScale ws;
+  const float* gs;  // per-group scales [n][k/128], or nullptr
 };
 
 // One workgroup: tiles kSmWaves*g .. kSmWaves*g + kSmWaves - 1 of the
 // problem.  lds: the table (128 bytes), two stages, a zero row (the A
 // operand of lanes that carry no token, read like a token row so that no
 // lane branches) and the tokens' activation scales.
+//
+// kG: per-group scales (one per row and unit; k % 512 == 0 and p.gs 16-byte
+// aligned, so that a lane reads four units' scales of its row at once).
+// Each unit's MFMAs then run as one chain from zero into c[u & 1], and the
+// unit is scaled one unit later (its chain has completed by then) into fp32
+// accumulators: element e < 8 of a lane belongs to row l % 32 of the tile,
+// e >= 8 to row l % 32 + 32, whose scales a lane-half swap of the loaded
+// ones provides.
+template <bool kG>
 __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lut,
                                          int8_t* stages, int8_t* zrow, float* xs) {
   const int tid = threadIdx.x, lane = tid & 63;
@@ -157,6 +167,22 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
   stage_store(sv, stages);
   sm_lds_barrier();  // window 0, the table, the zero row and the scales are ready
 
+  // per-group scales: lane l reads row l of the tile, four units per load,
+  // two chunks ahead; slo / shi hold the current chunk's scales of rows
+  // l % 32 and l % 32 + 32, plo / phi the previous chunk's last ones
+  const int grows =
+      kG && live ? (p.n - r * kTileRows < kTileRows ? p.n - r * kTileRows : kTileRows) : 0;
+  const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(p.gs) + int64_t(live ? r : 0) * kTileRows * C, 0, grows * C * 4,
+      kBufferWord3);
+  u32x4 gqa{}, gqb{};
+  float slo[4] = {}, shi[4] = {}, plo = 0.0f, phi = 0.0f;
+  float accf[16] = {};
+  if constexpr (kG) {
+    gqa = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * C), 0, 0);
+    gqb = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * C + 4), 0, 0);
+  }
+
   v16i c[2] = {v16i{}, v16i{}};
   for (int w = 0; w < nwin; ++w) {
     // the next window's activations are in flight during this one
@@ -167,6 +193,21 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
 #pragma unroll
     for (int u = 0; u < kWinUnits; ++u) {
       const int j = w * kWinUnits + u;  // unit of the tile
+      if constexpr (kG) {
+        if (u % 4 == 0) {  // a new chunk of four units (issued on every path)
+          plo = slo[3];
+          phi = shi[3];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t own = gqa[e];
+            const auto sw = __builtin_amdgcn_permlane32_swap(own, own, false, false);
+            slo[e] = __uint_as_float(sw[0]);
+            shi[e] = __uint_as_float(sw[1]);
+          }
+          gqa = gqb;
+          gqb = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * C + j + 8), 0, 0);
+        }
+      }
       if (j < C) {
         // codes 16h .. 16h + 15: 16 table reads in flight, then 4 chunks
 #pragma unroll
@@ -180,8 +221,23 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
             const v4i a = *reinterpret_cast<const v4i*>(arow + 16 * (8 * u + 4 * h + q));
             const v4i b = {static_cast<int>(wv[4 * q]), static_cast<int>(wv[4 * q + 1]),
                            static_cast<int>(wv[4 * q + 2]), static_cast<int>(wv[4 * q + 3])};
-            c[q & 1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c[q & 1], 0, 0, 0);
+            if constexpr (kG) {
+              const v16i cin = (h == 0 && q == 0) ? v16i{} : c[u & 1];
+              c[u & 1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, cin, 0, 0, 0);
+            } else {
+              c[q & 1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c[q & 1], 0, 0, 0);
+            }
           }
+        }
+      }
+      if constexpr (kG) {
+        if (j >= 1 && j <= C) {  // unit j - 1, in c[(u + 1) & 1]
+          const float sl = (u % 4 == 0) ? plo : slo[(u + 3) % 4];
+          const float sh = (u % 4 == 0) ? phi : shi[(u + 3) % 4];
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            accf[e] = __builtin_fmaf(static_cast<float>(c[(u + 1) & 1][e]), e < 8 ? sl : sh,
+                                     accf[e]);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -192,10 +248,30 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
     sm_lds_barrier();
   }
 
+  if constexpr (kG) {
+    // the last unit (C % 8 == 0: the walk ended on it), in c[1]
+    if (C % kWinUnits == 0) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        accf[e] = __builtin_fmaf(static_cast<float>(c[1][e]), e < 8 ? slo[3] : shi[3], accf[e]);
+    }
+  }
+
   // epilogue: lane l, element e holds D[i][l % 32] with i = 8(e/4) + 4(l/32)
   // + e%4: token i % 16 of tile row (l % 32) + 32 (i / 16).  The scales are
   // fetched once (two rows per lane), then every element is stored.
   if (!live) return;
+  if constexpr (kG) {
+    __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int i = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+      const int t = i & 15;
+      const int64_t row = int64_t(r) * kTileRows + (lane & 31) + 32 * (i >> 4);
+      if (t < p.m && row < p.n) as_global_mut(p.y)[int64_t(t) * p.n + row] = accf[e] * xs[t];
+    }
+    return;
+  }
   const int64_t row0 = int64_t(r) * kTileRows + (lane & 31);
   const float ws0 = p.ws.at(row0 < p.n ? row0 : p.n - 1);
   const float ws1 = p.ws.at(row0 + 32 < p.n ? row0 + 32 : p.n - 1);
@@ -216,7 +292,10 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
   }
 }
 
-__global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(4))) void smallm_batched_kernel(
+// kGroups: some descriptor carries per-group scales (a kernel of its own,
+// so that the other keeps its registers).
+template <bool kGroups>
+__global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(kGroups ? 3 : 4))) void smallm_batched_kernel(
     const sherry_gemm_desc* __restrict__ descs, int count) {
   __shared__ uint32_t lut[32];
   __shared__ __attribute__((aligned(16))) int8_t stages[2 * kStageBytes];
@@ -235,8 +314,9 @@ __global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(4)))
   lo = __builtin_amdgcn_readfirstlane(lo);
   const sherry_gemm_desc& d = descs[lo];
   const SmProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m,
-                    WScale{d.w_scales, d.w_scale}};
-  sm_block(p, blk - d.block_begin, lut, stages, zrow, xs);
+                    WScale{d.w_scales, d.w_scale}, d.w_group_scales};
+  if (kGroups && p.gs) sm_block<kGroups>(p, blk - d.block_begin, lut, stages, zrow, xs);
+  else sm_block<false>(p, blk - d.block_begin, lut, stages, zrow, xs);
 }
 
 }  // namespace
@@ -244,8 +324,11 @@ __global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(4)))
 int64_t smallm_blocks(int64_t n) { return ceil_div(ceil_div(n, kTileRows), kSmWaves); }
 
 int launch_smallm_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
-                          hipStream_t s) {
-  return launch(smallm_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
+                          bool groups, hipStream_t s) {
+  if (groups)
+    return launch(smallm_batched_kernel<true>, dim3(static_cast<unsigned>(total_blocks)),
+                  dim3(kSmThreads), 0, s, descs, count);
+  return launch(smallm_batched_kernel<false>, dim3(static_cast<unsigned>(total_blocks)),
                 dim3(kSmThreads), 0, s, descs, count);
 }
 

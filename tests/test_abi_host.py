@@ -281,6 +281,9 @@ def test_gemm_batched_prepare_picks_the_token_gemv():
     assert prep([(2, 64, 128), (1, 64, 128)], group=True)[2] == 2 | G
     assert prep([(5, 64, 128), (1, 64, 128)], group=True)[2] == 17 | G
     assert prep([(4, 3072, 8320)], group=True)[2] == 17 | G
+    # the window kernel takes per-group scales of whole 512-value chunks
+    assert prep([(16, 3072, 8192), (9, 1024, 3072)], group=True) == ([0, 12], 16, 16 | G)
+    assert prep([(5, 64, 512), (1, 64, 128)], group=True)[2] == 5 | G
     assert prep([(17, 64, 128)])[2] == 17
 
 
@@ -383,11 +386,11 @@ def test_skinny_validation_without_launch():
     assert L.sherry_gemm_batched(FAKE, 1, 1, 0, None) == sh.SHERRY_E_SHAPE
     assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 16, None) == sh.SHERRY_E_ALIGN
     assert L.sherry_gemm_batched(None, 1, 1, 16, None) == sh.SHERRY_E_INVALID
-    # the per-group flag: never with the window kernel's values (5-16), and
-    # the value under it is checked as without it
+    # the value under the per-group flag is checked as without it
     G = sh.SHERRY_LAUNCH_GROUPS
-    assert L.sherry_gemm_batched(FAKE, 1, 1, 16 | G, None) == sh.SHERRY_E_INVALID
     assert L.sherry_gemm_batched(FAKE, 1, 1, 0 | G, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_batched(FAKE, 1, 1, (sh.SHERRY_MAX_M + 1) | G, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 16 | G, None) == sh.SHERRY_E_ALIGN
     assert L.sherry_gemm_batched(FAKE + 4, 1, 1, 4 | G, None) == sh.SHERRY_E_ALIGN
 
 

@@ -280,6 +280,33 @@ def test_window_kernel_model_step_full(dev, m):
     assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 78) == m
 
 
+def test_window_kernel_group_scales(dev):
+    # 5-16 tokens, per-group scales on every other product (k % 512 == 0),
+    # per-channel or per-tensor on the rest: one window-kernel launch
+    _say("window kernel groups")
+    cases = [(5, 64, 512), (16, 65, 1024), (9, 600, 2048), (16, 257, 3072), (12, 130, 4096),
+             (16, 3072, 8192), (7, 70, 1536), (6, 520, 14336)]
+    G = _sh().SHERRY_LAUNCH_GROUPS
+    assert _grouped(dev, cases, 84, groups=True) == 16 | G
+
+
+def test_window_kernel_group_scales_model_step_full(dev):
+    # one LLaMA-3.2-3B layer at 16 tokens with per-group scales, every output
+    _say("window kernel groups 3b layer")
+    spec = synth.LLAMA_3B
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    assert _grouped(dev, [(16, lin.n, lin.k) for lin in blk], 85, groups=True) == \
+        16 | _sh().SHERRY_LAUNCH_GROUPS
+
+
+def test_window_kernel_group_scales_need_whole_chunks(dev):
+    # a per-group product with k % 512 != 0 sends the launch to the
+    # register-decoded kernel (launch value 17 with the flag)
+    _say("window kernel groups, ragged k")
+    cases = [(8, 64, 1028), (5, 130, 512)]
+    assert _grouped(dev, cases, 86, groups=True) == 17 | _sh().SHERRY_LAUNCH_GROUPS
+
+
 def test_window_kernel_extremes(dev):
     # activations at -128 / 127 for all 16 tokens, k = 4096 (4 windows)
     sh = _sh()
