@@ -121,6 +121,21 @@ int sherry_pack(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
 int sherry_unpack(const uint8_t* packed, size_t packed_bytes, int64_t n,
                   int64_t k, int8_t* t_out);
 
+/* Lane-interleaved layout: the same 5-bit codes, units and byte size as the
+ * tiled layout, with the codes of each unit assigned to lanes for the int8
+ * matrix cores.  Container l = 16b + t of a unit (head bytes 16l..16l+15,
+ * tail bytes 1024+4l..1024+4l+3, code j at stream bits [5j, 5j+5) as in the
+ * tiled layout) holds as code j = 4(2g + p) + c the code of row 16g + t of
+ * the unit and of its block 16p + 4b + c (weights 4(16p+4b+c) .. +3 of the
+ * unit's 128), for g, b in 0..3, p in 0..1, c in 0..3.  So a lane's codes
+ * 4(2g+p) .. 4(2g+p)+3 are row 16g + t's 16 weights of chunk 4p + b.
+ * sherry_pack_il / sherry_unpack_il: as sherry_pack / sherry_unpack, in this
+ * layout.  Read by the *_il products only. */
+int sherry_pack_il(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                   size_t out_bytes, int64_t* bad_block);
+int sherry_unpack_il(const uint8_t* packed, size_t packed_bytes, int64_t n,
+                     int64_t k, int8_t* t_out);
+
 /* Sparse-AbsMean ternarization and packing on the GPU (Eq. 4, Eq. 5), the
  * step that turns full-precision weights into the packed layout.
  * w: device, fp32 [n][k] row-major (row = output channel, blocks of 4 along
@@ -369,6 +384,18 @@ int sherry_gemv_f32_batched_prepare(sherry_gemv_f32_desc* descs, int count,
                                     int64_t* total_blocks);
 int sherry_gemv_f32_batched(const sherry_gemv_f32_desc* descs_dev, int count,
                             int64_t total_blocks, void* stream);
+
+/* The same fused products on lane-interleaved weights (sherry_pack_il): each
+ * 4-code chunk slot of a lane is the B operand of one int8 MFMA over 16 rows
+ * and 64 weights, whose activation operand serves the unit's four row
+ * groups.  Results bit-identical to sherry_gemv_f32_batched on the tiled
+ * layout of the same matrix.  Per-tensor or per-channel scales only:
+ * _prepare returns SHERRY_E_INVALID for a descriptor with per-group scales,
+ * otherwise it is sherry_gemv_f32_batched_prepare; pass its total_blocks. */
+int sherry_gemv_f32_il_batched_prepare(sherry_gemv_f32_desc* descs, int count,
+                                       int64_t* total_blocks);
+int sherry_gemv_f32_il_batched(const sherry_gemv_f32_desc* descs_dev, int count,
+                               int64_t total_blocks, void* stream);
 
 /* ---------------------------------------------------------------------- */
 /* Comparison layouts (Sec. 2.3): the "2-bit strategy" and the "1.67-bit   */

@@ -27,6 +27,9 @@ Parity status of each piece (what pins it, in ``tests/test_oracle.py``):
                          32 codes used (3^3 triples, Sec. 2.3), mirror
                          code(-t) = 26 - code(t), rejection of the unused
                          codes, round trips.
+* lane-interleaved   -- pinned: hand-derived bytes (tests/golden), round
+  layout                 trips, the same multiset of codes per unit as the
+                         tiled layout, 3:4 rejection.
 """
 from __future__ import annotations
 
@@ -114,6 +117,10 @@ def lib():
         L.oracle_pack3.restype = i64
         L.oracle_unpack3.argtypes = [u8p, i64, i64, i8p]
         L.oracle_unpack3.restype = ctypes.c_int
+        L.oracle_pack_il.argtypes = [i8p, i64, i64, u8p]
+        L.oracle_pack_il.restype = i64
+        L.oracle_unpack_il.argtypes = [u8p, i64, i64, i8p]
+        L.oracle_unpack_il.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -183,6 +190,31 @@ def unpack(p: np.ndarray, n: int, k: int) -> np.ndarray:
         raise OracleError("packed buffer too small")
     t = np.zeros((n, k), dtype=np.int8)
     if lib().oracle_unpack(_p(p, ctypes.c_uint8), n, k, _p(t, ctypes.c_int8)) != 0:
+        raise OracleError("bad shape")
+    return t
+
+
+# ---- (ix) lane-interleaved layout (this project's own) ---------------------
+
+def pack_il(t: np.ndarray) -> np.ndarray:
+    t = np.ascontiguousarray(t, dtype=np.int8)
+    n, k = t.shape
+    nb = packed_bytes(n, k)
+    if nb == 0:
+        raise OracleError("bad shape %s" % (t.shape,))
+    out = np.zeros(nb, dtype=np.uint8)
+    rc = lib().oracle_pack_il(_p(t, ctypes.c_int8), n, k, _p(out, ctypes.c_uint8))
+    if rc != 0:
+        raise OracleError("block %d is not 3:4" % (-rc - 1))
+    return out
+
+
+def unpack_il(p: np.ndarray, n: int, k: int) -> np.ndarray:
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    if p.size < packed_bytes(n, k):
+        raise OracleError("packed buffer too small")
+    t = np.zeros((n, k), dtype=np.int8)
+    if lib().oracle_unpack_il(_p(p, ctypes.c_uint8), n, k, _p(t, ctypes.c_int8)) != 0:
         raise OracleError("bad shape")
     return t
 

@@ -45,6 +45,12 @@
  *                         Built by enumerating the 27 triples.  Comparison
  *                         layout only.
  *
+ *  (ix)  lane-interleaved layout -- this project's own placement of the codes
+ *                         of (ii) for the int8 matrix-core products: same
+ *                         units, containers and stream bits, another
+ *                         assignment of a unit's (row, block) pairs to
+ *                         (container, code) slots.  Written out below.
+ *
  *  Parity unpinned: the bit assignment inside a code (i) and the placement of
  *  the codes in the stream (ii).  The paper prints no packed example, so the
  *  tests pin them only to the written reading (a hand-written code table and
@@ -549,6 +555,82 @@ int oracle_unpack3(const uint8_t* p, int64_t n, int64_t k, int8_t* t) {
       if (code > 26) return -2;
       for (int q = 0; q < 3; ++q)
         if (3 * b + q < k) t[row * k + 3 * b + q] = g_table3[code][q];
+    }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* (ix) lane-interleaved layout                                             */
+/*                                                                          */
+/* Units, containers (16-byte head at 16*l, 4-byte tail at 1024 + 4*l for    */
+/* container l = 0..63) and the 160-bit stream of a container are those of   */
+/* (ii).  Only the slot of each code differs: row i of a unit, written       */
+/* i = 16g + t (g = 0..3, t = 0..15), and block b of the unit (weights        */
+/* 4b..4b+3 of its 128), written b = 16p + 4h + c (p = 0..1, h = 0..3,        */
+/* c = 0..3), go to container 16h + t as code 4(2g + p) + c.                  */
+/* ------------------------------------------------------------------------ */
+
+static void il_slot(int i, int b, int* container, int* code) {
+  int g = i / 16, t = i % 16;
+  int p = b / 16, h = (b / 4) % 4, c = b % 4;
+  *container = 16 * h + t;
+  *code = 4 * (2 * g + p) + c;
+}
+
+/* Byte and bit of stream bit sp of container l of unit (r, c). */
+static void il_bit_addr(int64_t r, int64_t c, int l, int sp, int64_t C, int64_t* byte,
+                        int* bit) {
+  int64_t unit = (r * C + c) * 1280;
+  if (sp < 128) {
+    *byte = unit + 16 * l + sp / 8;
+    *bit = sp % 8;
+  } else {
+    *byte = unit + 1024 + 4 * l + (sp - 128) / 8;
+    *bit = (sp - 128) % 8;
+  }
+}
+
+/* As oracle_pack, in the lane-interleaved layout. */
+int64_t oracle_pack_il(const int8_t* t, int64_t n, int64_t k, uint8_t* out) {
+  int64_t bytes = oracle_packed_bytes(n, k);
+  if (bytes == 0) return -((int64_t)1 << 62);
+  memset(out, 0, (size_t)bytes);
+  int64_t C = ceil_to(k, 128) / 128;
+  int64_t nb = k / 4;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t b = 0; b < nb; ++b) {
+      int code = oracle_encode_block(t + row * k + 4 * b);
+      if (code < 0) return -(row * nb + b + 1);
+      int l, j;
+      il_slot((int)(row % 64), (int)(b % 32), &l, &j);
+      for (int q = 0; q < 5; ++q) {
+        int64_t byte;
+        int bit;
+        il_bit_addr(row / 64, b / 32, l, 5 * j + q, C, &byte, &bit);
+        if ((code >> q) & 1) out[byte] |= (uint8_t)(1u << bit);
+      }
+    }
+  }
+  return 0;
+}
+
+/* Inverse of oracle_pack_il for the first n rows and k weights. */
+int oracle_unpack_il(const uint8_t* p, int64_t n, int64_t k, int8_t* t) {
+  if (oracle_packed_bytes(n, k) == 0) return -1;
+  int64_t C = ceil_to(k, 128) / 128;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t b = 0; b < k / 4; ++b) {
+      int l, j;
+      il_slot((int)(row % 64), (int)(b % 32), &l, &j);
+      int code = 0;
+      for (int q = 0; q < 5; ++q) {
+        int64_t byte;
+        int bit;
+        il_bit_addr(row / 64, b / 32, l, 5 * j + q, C, &byte, &bit);
+        code |= ((p[byte] >> bit) & 1) << q;
+      }
+      oracle_decode_code(code, t + row * k + 4 * b);
     }
   }
   return 0;

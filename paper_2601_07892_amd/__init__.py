@@ -46,7 +46,8 @@ EXPORTS = [
     "sherry_gemm_group", "sherry_gemv_f32_group", "sherry_packed3_bytes", "sherry_pack3",
     "sherry_unpack3", "sherry_gemv3", "sherry_gemv2_batched_prepare", "sherry_gemv2_batched",
     "sherry_gemv3_batched_prepare", "sherry_gemv3_batched", "sherry_quantize_act_batched_prepare",
-    "sherry_quantize_act_batched",
+    "sherry_quantize_act_batched", "sherry_pack_il", "sherry_unpack_il",
+    "sherry_gemv_f32_il_batched_prepare", "sherry_gemv_f32_il_batched",
 ]
 
 
@@ -113,6 +114,8 @@ def _load():
         "sherry_last_error": ([], ctypes.c_char_p),
         "sherry_packed_bytes": ([i64, i64], ctypes.c_size_t),
         "sherry_pack": ([vp, i64, i64, vp, ctypes.c_size_t, i64p], ctypes.c_int),
+        "sherry_pack_il": ([vp, i64, i64, vp, ctypes.c_size_t, i64p], ctypes.c_int),
+        "sherry_unpack_il": ([vp, ctypes.c_size_t, i64, i64, vp], ctypes.c_int),
         "sherry_unpack": ([vp, ctypes.c_size_t, i64, i64, vp], ctypes.c_int),
         "sherry_quantize_act": ([vp, i64, i64, vp, vp, vp], ctypes.c_int),
         "sherry_gemv": ([vp, vp, vp, f32, vp, vp, i64, i64, vp], ctypes.c_int),
@@ -131,7 +134,10 @@ def _load():
         "sherry_gemv_f32": ([vp, vp, vp, f32, vp, vp, i64, i64, vp], ctypes.c_int),
         "sherry_gemv_f32_batched_prepare": ([ctypes.POINTER(sherry_gemv_f32_desc), ctypes.c_int,
                                              i64p], ctypes.c_int),
+        "sherry_gemv_f32_il_batched_prepare": ([ctypes.POINTER(sherry_gemv_f32_desc), ctypes.c_int,
+                                             i64p], ctypes.c_int),
         "sherry_gemv_f32_batched": ([vp, ctypes.c_int, i64, vp], ctypes.c_int),
+        "sherry_gemv_f32_il_batched": ([vp, ctypes.c_int, i64, vp], ctypes.c_int),
         "sherry_gemm_batched_prepare": ([ctypes.POINTER(sherry_gemm_desc), ctypes.c_int, i64p,
                                          ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
         "sherry_gemm_batched": ([vp, ctypes.c_int, i64, ctypes.c_int32, vp], ctypes.c_int),
@@ -233,6 +239,30 @@ def sherry_unpack(p: np.ndarray, n: int, k: int) -> np.ndarray:
     p = _host(p, np.uint8)
     t = np.empty((n, k), np.int8)
     _check(lib.sherry_unpack(p.ctypes.data, p.nbytes, n, k, t.ctypes.data), "sherry_unpack")
+    return t
+
+
+def sherry_pack_il(t: np.ndarray, out: np.ndarray | None = None) -> np.ndarray:
+    """int8 [n][k] ternary 3:4 -> uint8 packed bytes, lane-interleaved layout (host)."""
+    t = _host(t, np.int8)
+    n, k = t.shape
+    nb = sherry_packed_bytes(n, k)
+    if out is None:
+        out = np.empty(max(nb, 1), np.uint8)
+    bad = ctypes.c_int64(-1)
+    st = lib.sherry_pack_il(t.ctypes.data, n, k, out.ctypes.data, out.nbytes, ctypes.byref(bad))
+    if st == SHERRY_E_NOT_3_4:
+        e = SherryError(st, "sherry_pack_il")
+        e.bad_block = int(bad.value)
+        raise e
+    _check(st, "sherry_pack_il")
+    return out
+
+
+def sherry_unpack_il(p: np.ndarray, n: int, k: int) -> np.ndarray:
+    p = _host(p, np.uint8)
+    t = np.empty((n, k), np.int8)
+    _check(lib.sherry_unpack_il(p.ctypes.data, p.nbytes, n, k, t.ctypes.data), "sherry_unpack_il")
     return t
 
 
@@ -387,6 +417,20 @@ def sherry_gemv_f32_batched(descs_dev, count: int, total_blocks: int, stream=Non
     """descs_dev: device uint8 tensor holding a byte copy of prepared f32 descriptors."""
     _check(lib.sherry_gemv_f32_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
            "sherry_gemv_f32_batched")
+
+
+def sherry_gemv_f32_il_batched_prepare(descs) -> int:
+    """As sherry_gemv_f32_batched_prepare, for lane-interleaved weights."""
+    total = ctypes.c_int64(0)
+    _check(lib.sherry_gemv_f32_il_batched_prepare(descs, len(descs), ctypes.byref(total)),
+           "sherry_gemv_f32_il_batched_prepare")
+    return int(total.value)
+
+
+def sherry_gemv_f32_il_batched(descs_dev, count: int, total_blocks: int, stream=None):
+    """Fused products on lane-interleaved weights (descriptors from the _il prepare)."""
+    _check(lib.sherry_gemv_f32_il_batched(_ptr(descs_dev), count, total_blocks, _stream(stream)),
+           "sherry_gemv_f32_il_batched")
 
 
 def sherry_gemm_batched_prepare(descs) -> tuple[int, int]:

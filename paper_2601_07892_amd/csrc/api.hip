@@ -401,7 +401,23 @@ extern "C" int sherry_gemv_f32_batched(const sherry_gemv_f32_desc* descs_dev, in
   if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
     return SHERRY_E_INVALID;
   if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
-  return launch_gemv_f32_batched(descs_dev, count, total_blocks, as_stream(stream));
+  return launch_gemv_f32_batched(descs_dev, count, total_blocks, false, as_stream(stream));
+}
+
+extern "C" int sherry_gemv_f32_il_batched_prepare(sherry_gemv_f32_desc* descs, int count,
+                                                  int64_t* total_blocks) {
+  if (!descs || count < 1) return SHERRY_E_INVALID;
+  for (int i = 0; i < count; ++i)
+    if (descs[i].w_group_scales) return SHERRY_E_INVALID;  // tiled units only
+  return sherry_gemv_f32_batched_prepare(descs, count, total_blocks);
+}
+
+extern "C" int sherry_gemv_f32_il_batched(const sherry_gemv_f32_desc* descs_dev, int count,
+                                          int64_t total_blocks, void* stream) {
+  if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
+    return SHERRY_E_INVALID;
+  if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  return launch_gemv_f32_batched(descs_dev, count, total_blocks, true, as_stream(stream));
 }
 
 extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,

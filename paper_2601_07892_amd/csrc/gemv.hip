@@ -231,12 +231,68 @@ struct XFromLdsMfmaTok {
   }
 };
 
+// Lane-interleaved units (sherry_pack_il): lane 16b + t holds, as its codes
+// 4(2g + p) .. 4(2g + p) + 3, row 16g + t's 16 weights of chunk 4p + b
+// (g, b = 0..3; p = 0, 1).  So for chunk slot (g, p) the looked-up words are
+// the B operand of one v_mfma_i32_16x16x64_i8 over 16 rows (16g + t, column
+// t) and 64 weights (chunks 4p .. 4p + 3, k block b), and the A operand,
+// token m's activations of those chunks in lanes 16b + m, serves all four
+// row groups: two 16-byte activation reads per container instead of eight.
+// D[m][t] = x_m . w(16g + t) lands in lane 16(m/4) + t, element m % 4 of
+// accumulator g.
+template <int G2>
+__device__ __forceinline__ void dot_il(const uint32_t (&d)[5], const u32x4 (&xa)[2],
+                                       const uint32_t* lut, v4i (&acc)[4]) {
+  __builtin_amdgcn_sched_barrier(0);
+  uint32_t a4[16];
+  group_offsets<16 * G2>(d, a4, std::make_integer_sequence<int, 16>{});
+  uint32_t wv[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j)
+    wv[j] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + a4[j]);
+  // slots (g, p) = (2 G2 + (s >> 1), s & 1), issued alternating accumulators
+  constexpr int order[4] = {0, 2, 1, 3};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int s = order[i];
+    const int g = 2 * G2 + (s >> 1), p = s & 1;
+    const v4i a = {static_cast<int>(xa[p].x), static_cast<int>(xa[p].y),
+                   static_cast<int>(xa[p].z), static_cast<int>(xa[p].w)};
+    const v4i b = {static_cast<int>(wv[4 * s]), static_cast<int>(wv[4 * s + 1]),
+                   static_cast<int>(wv[4 * s + 2]), static_cast<int>(wv[4 * s + 3])};
+    acc[g] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc[g], 0, 0, 0);
+  }
+}
+
+// Activation source of the lane-interleaved units: up to 16 token rows in
+// LDS (kp bytes each, zero past k); lanes 16b + m with m < m_count read token
+// m's chunks b and 4 + b of the container, every other lane keeps zeros.
+struct XFromLdsMfmaIL {
+  const int8_t* xq;
+  int kp, m_count;
+  mutable u32x4 xa[2] = {};
+  __device__ __forceinline__ void dot(const uint32_t (&d)[5], int c, const uint32_t* lut,
+                                      v4i (&acc)[4]) const {
+    const int lane = threadIdx.x & 63;
+    const int m = lane & 15, b = lane >> 4;
+    if (m < m_count) {
+      const u32x4* xv = reinterpret_cast<const u32x4*>(xq + m * kp + c * kTileK);
+      xa[0] = xv[b];
+      xa[1] = xv[4 + b];
+    }
+    dot_il<0>(d, xa, lut, acc);
+    dot_il<1>(d, xa, lut, acc);
+  }
+};
+
 template <class X>
 constexpr bool kMfmaSource = false;
 template <>
 constexpr bool kMfmaSource<XFromLdsMfma> = true;
 template <>
 constexpr bool kMfmaSource<XFromLdsMfmaTok> = true;
+template <>
+constexpr bool kMfmaSource<XFromLdsMfmaIL> = true;
 
 // Streams containers [c0, c1) of one tile through a ring of kRing register
 // slots: slot u is decoded and immediately refilled with the container kRing
@@ -496,6 +552,17 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
       uint32_t ring[kRing][5];
       ring_fill(ring, range);
       ring_run_groups<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
+    }
+  } else if constexpr (std::is_same_v<X, XFromLdsMfmaIL>) {
+    static_assert(M == 1, "the lane-interleaved source serves one token here");
+    uint32_t ring[kRing][5];
+    ring_fill(ring, range);
+    v4i macc[4] = {};
+    ring_run(ring, range, c0, c1, xsrc, lut, macc);
+    // lane l < 16 holds row 16g + l of the tile in accumulator g
+    if (lane < 16) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) red[wave * 64 + 16 * g + lane] = macc[g][0];
     }
   } else if constexpr (kMfmaSource<X>) {
     static_assert(M <= 4 && !kGrp, "the matrix-core sources serve up to four tokens");
@@ -864,7 +931,7 @@ struct QuantizeRow {
 
 // Fused product of one block: the row length picks the quantizer (rows up
 // to 2048, 8192 and 16384 values from registers, longer ones in two passes).
-template <bool kGrp = false>
+template <bool kGrp = false, bool kIL = false>
 __device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, float* x_scale,
                                             bool write_scale, WScale ws, float* y,
                                             int32_t* acc, int64_t n, int k, int g, int S,
@@ -873,9 +940,12 @@ __device__ __forceinline__ void fused_block(const uint8_t* w, const float* x, fl
                                             float* redf = nullptr) {
   const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
   // per-tensor and per-channel scales sum a tile row's containers in int32 on
-  // the matrix cores; per-group scales need each container's sum per lane
+  // the matrix cores; per-group scales need each container's sum per lane;
+  // kIL: lane-interleaved units
+  static_assert(!(kGrp && kIL), "per-group scales: tiled units only");
   const auto xsrc = [&] {
     if constexpr (kGrp) return XFromLds{xq};
+    else if constexpr (kIL) return XFromLdsMfmaIL{xq, kp, 1};
     else return XFromLdsMfma{xq};
   }();
   if (kp <= 4 * kGemvThreads) {
@@ -924,6 +994,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_group_kernel(
                     static_cast<int>(k), blockIdx.x, split, lut, red, part, xq, gs, redf);
 }
 
+template <bool kIL>
 __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
     const sherry_gemv_f32_desc* __restrict__ descs, int count) {
   __shared__ uint32_t lut[32];
@@ -948,7 +1019,11 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_f32_batched_kernel(
   const int k = static_cast<int>(d.k);
   const int C = (k + kTileK - 1) / kTileK;
   const int S = fused_split(C);
-  if (d.w_group_scales) {
+  if constexpr (kIL) {
+    fused_block<false, true>(d.w, d.x, d.x_scale, blk == d.block_begin,
+                             WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k,
+                             blk - d.block_begin, S, lut, red, part, xq);
+  } else if (d.w_group_scales) {
     fused_block<true>(d.w, d.x, d.x_scale, blk == d.block_begin, WScale{nullptr, 0.0f}, d.y,
                       d.acc, d.n, k, blk - d.block_begin, S, lut, red, part, xq,
                       d.w_group_scales, redf);
@@ -1062,8 +1137,11 @@ int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, WScale ws,
 }
 
 int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_t total_blocks,
-                            hipStream_t s) {
-  return launch(gemv_f32_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
+                            bool il, hipStream_t s) {
+  if (il)
+    return launch(gemv_f32_batched_kernel<true>, dim3(static_cast<unsigned>(total_blocks)),
+                  dim3(kGemvThreads), 0, s, descs, count);
+  return launch(gemv_f32_batched_kernel<false>, dim3(static_cast<unsigned>(total_blocks)),
                 dim3(kGemvThreads), 0, s, descs, count);
 }
 

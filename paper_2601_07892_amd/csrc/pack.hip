@@ -1,9 +1,11 @@
 // Offline packing (Appendix A, offline phase): host code.
 //
 // sherry_pack turns a ternary 3:4 matrix into the 5-bit tiled layout that the
-// device products stream; sherry_unpack is its exact inverse.  sherry_pack2
-// and sherry_pack3 write the two comparison layouts (2 bits per weight, and
-// three weights per 5-bit code).  Layouts are defined in sherry.h.
+// device products stream; sherry_unpack is its exact inverse.  sherry_pack_il
+// writes the same codes lane-interleaved for the matrix-core products.
+// sherry_pack2 and sherry_pack3 write the two comparison layouts (2 bits per
+// weight, and three weights per 5-bit code).  Layouts are defined in
+// sherry.h.
 #include <algorithm>
 #include <atomic>
 #include <cstring>
@@ -104,6 +106,18 @@ inline void get_container(const uint8_t* head, const uint8_t* tail, uint32_t* co
     else v = hi >> (b - 128);
     codes[j] = static_cast<uint32_t>(v & 31u);
   }
+}
+
+// Lane-interleaved units: the container of lane l = 16b + t holds, as code
+// j = 4(2g + p) + c, the code of row 16g + t and block 16p + 4b + c of the
+// unit (g, b = 0..3, p = 0..1, c = 0..3).  il_source gives, for (l, j), the
+// row and block of the unit that the tiled layout keeps in lane `row`, code
+// `block`.
+inline void il_source(int l, int j, int* row, int* block) {
+  const int b = l >> 4, t = l & 15;
+  const int g = j >> 3, p = (j >> 2) & 1, c = j & 3;
+  *row = 16 * g + t;
+  *block = 16 * p + 4 * b + c;
 }
 
 }  // namespace
@@ -328,4 +342,60 @@ extern "C" int sherry_unpack3(const uint8_t* packed, size_t packed_bytes, int64_
     }
   });
   return bad.load() ? SHERRY_E_INVALID : SHERRY_OK;
+}
+
+extern "C" int sherry_pack_il(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
+                              size_t out_bytes, int64_t* bad_block) {
+  // the tiled units first, then each unit's codes moved to their lanes
+  const int st = sherry_pack(t, n, k, out, out_bytes, bad_block);
+  if (st != SHERRY_OK) return st;
+  const int64_t units = ceil_div(n, kTileRows) * ceil_div(k, kTileK);
+  parallel_ranges(units, [&](int64_t u0, int64_t u1) {
+    uint32_t tiled[kTileRows][32], codes[32];
+    for (int64_t u = u0; u < u1; ++u) {
+      uint8_t* unit = out + static_cast<size_t>(u) * kUnitBytes;
+      for (int i = 0; i < kTileRows; ++i)
+        get_container(unit + 16 * i, unit + kHeadBytes + 4 * i, tiled[i]);
+      for (int l = 0; l < kTileRows; ++l) {
+        for (int j = 0; j < 32; ++j) {
+          int row, block;
+          il_source(l, j, &row, &block);
+          codes[j] = tiled[row][block];
+        }
+        put_container(codes, unit + 16 * l, unit + kHeadBytes + 4 * l);
+      }
+    }
+  });
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_unpack_il(const uint8_t* packed, size_t packed_bytes, int64_t n,
+                                int64_t k, int8_t* t_out) {
+  if (!packed || !t_out) return SHERRY_E_INVALID;
+  const size_t need = sherry_packed_bytes(n, k);
+  if (need == 0) return SHERRY_E_SHAPE;
+  if (packed_bytes < need) return SHERRY_E_BUFSIZE;
+  // back to tiled units in a copy, then the tiled unpacker
+  std::vector<uint8_t> tiled(need);
+  const int64_t units = ceil_div(n, kTileRows) * ceil_div(k, kTileK);
+  parallel_ranges(units, [&](int64_t u0, int64_t u1) {
+    uint32_t il[kTileRows][32];
+    for (int64_t u = u0; u < u1; ++u) {
+      const uint8_t* src = packed + static_cast<size_t>(u) * kUnitBytes;
+      uint8_t* dst = tiled.data() + static_cast<size_t>(u) * kUnitBytes;
+      for (int l = 0; l < kTileRows; ++l)
+        get_container(src + 16 * l, src + kHeadBytes + 4 * l, il[l]);
+      uint32_t rows[kTileRows][32];
+      for (int l = 0; l < kTileRows; ++l) {
+        for (int j = 0; j < 32; ++j) {
+          int row, block;
+          il_source(l, j, &row, &block);
+          rows[row][block] = il[l][j];
+        }
+      }
+      for (int i = 0; i < kTileRows; ++i)
+        put_container(rows[i], dst + 16 * i, dst + kHeadBytes + 4 * i);
+    }
+  });
+  return sherry_unpack(tiled.data(), need, n, k, t_out);
 }

@@ -248,8 +248,9 @@ int launch_gemv_batched(const sherry_gemv_desc* descs, int count,
                         int64_t total_blocks, hipStream_t s);
 int launch_gemv_f32(const uint8_t* w, const float* x, float* x_scale, WScale ws, float* y,
                     int32_t* acc, int64_t n, int64_t k, hipStream_t s);
+// il: lane-interleaved units (sherry_pack_il; no per-group scales).
 int launch_gemv_f32_batched(const sherry_gemv_f32_desc* descs, int count, int64_t total_blocks,
-                            hipStream_t s);
+                            bool il, hipStream_t s);
 // Per-group weight scales gs: fp32 [n][ceil(k/128)] (one per 128 weights of
 // a row).
 int launch_gemv_group(const uint8_t* w, const int8_t* x, const float* x_scale, const float* gs,

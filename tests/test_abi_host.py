@@ -124,6 +124,63 @@ def test_pack_hand_derived_fixtures(idx):
     assert nz == {int(a): b for a, b in fx["nonzero"].items()}
 
 
+@pytest.mark.parametrize("idx", [0, 1])
+def test_pack_il_hand_derived_fixtures(idx):
+    with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
+        fx = json.load(f)["lane_interleaved"][idx]
+    g = oracle.code_table()
+    t = np.tile(np.array([0, 1, 1, 1], np.int8), (fx["n"], fx["k"] // 4))
+    for row, blk, code in fx["blocks"]:
+        t[row, 4 * blk:4 * blk + 4] = g[code]
+    p = sh.sherry_pack_il(t)
+    assert p.size == fx["total_bytes"]
+    nz = {int(i): int(p[i]) for i in np.nonzero(p)[0]}
+    assert nz == {int(a): b for a, b in fx["nonzero"].items()}
+
+
+@pytest.mark.parametrize("n,k", [(1, 4), (64, 128), (65, 132), (130, 1028), (300, 3076),
+                                 (2100, 2048)])
+def test_pack_il_matches_oracle(n, k):
+    t = synth.ternary_34(n, k, 23, "il", n, k)
+    p = sh.sherry_pack_il(t)
+    assert np.array_equal(p, oracle.pack_il(t))
+    assert np.array_equal(sh.sherry_unpack_il(p, n, k), t)
+    assert np.array_equal(oracle.unpack_il(p, n, k), t)
+
+
+def test_pack_il_errors():
+    t = synth.ternary_34(5, 64, 24, "ile")
+    t[3, 20:24] = [1, 1, 0, 0]
+    with pytest.raises(sh.SherryError) as e:
+        sh.sherry_pack_il(t)
+    assert e.value.status == sh.SHERRY_E_NOT_3_4 and e.value.bad_block == 3 * 16 + 5
+    L = sh.lib
+    good = synth.ternary_34(5, 64, 24, "ilg")
+    out = np.zeros(sh.sherry_packed_bytes(5, 64), np.uint8)
+    assert L.sherry_pack_il(good.ctypes.data, 5, 64, out.ctypes.data, out.nbytes - 1,
+                            None) == sh.SHERRY_E_BUFSIZE
+    assert L.sherry_pack_il(good.ctypes.data, 5, 66, out.ctypes.data, out.nbytes,
+                            None) == sh.SHERRY_E_SHAPE
+    t_out = np.zeros((5, 64), np.int8)
+    assert L.sherry_unpack_il(out.ctypes.data, out.nbytes - 1, 5, 64,
+                              t_out.ctypes.data) == sh.SHERRY_E_BUFSIZE
+    assert L.sherry_unpack_il(None, out.nbytes, 5, 64, t_out.ctypes.data) == sh.SHERRY_E_INVALID
+
+
+def test_il_fused_prepare_rejects_group_scales():
+    descs = (sh.sherry_gemv_f32_desc * 2)()
+    for d in descs:
+        d.w, d.x, d.y = FAKE, FAKE, FAKE
+        d.n, d.k, d.w_scale = 64, 128, 1.0
+    assert sh.sherry_gemv_f32_il_batched_prepare(descs) == sh.sherry_gemv_f32_batched_prepare(descs)
+    descs[1].w_group_scales = FAKE
+    with pytest.raises(sh.SherryError):
+        sh.sherry_gemv_f32_il_batched_prepare(descs)
+    L = sh.lib
+    assert L.sherry_gemv_f32_il_batched(None, 1, 1, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_gemv_f32_il_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
+
+
 def test_pack_large_multithreaded():
     n, k = 4096, 2048  # many row tiles -> several host threads
     t = synth.ternary_34(n, k, 22, "big")

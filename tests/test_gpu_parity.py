@@ -650,7 +650,8 @@ def test_fused_gemv_zero_row_and_no_outputs(dev):
     assert _y_ok(y.cpu().numpy(), y_ref[0])
 
 
-def _fused_batched(dev, shapes, seed, with_scale=True, channel=False):
+def _fused_batched(dev, shapes, seed, with_scale=True, channel=False, il=False):
+    # il: lane-interleaved weights (sherry_pack_il) on sherry_gemv_f32_il_batched
     sh = _sh()
     descs = (sh.sherry_gemv_f32_desc * len(shapes))()
     keep, hold = [], []
@@ -658,7 +659,7 @@ def _fused_batched(dev, shapes, seed, with_scale=True, channel=False):
         t = synth.ternary_34(n, k, seed, "fb", i)
         x = synth.activations(1, k, seed, "fbx", i, outlier_frac=0.01)
         sw = synth.weight_scale(seed, "fbs", i)
-        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        w = torch.from_numpy(sh.sherry_pack_il(t) if il else sh.sherry_pack(t)).to(dev)
         xd = torch.from_numpy(x).to(dev)
         sxd = torch.full((1,), float("nan"), dtype=torch.float32, device=dev)
         y = torch.full((n,), float("nan"), dtype=torch.float32, device=dev)
@@ -669,31 +670,38 @@ def _fused_batched(dev, shapes, seed, with_scale=True, channel=False):
         d.n, d.k, d.w_scale = n, k, sw
         swc = _desc_scale(d, dev, hold, n, seed, i, channel, k)
         keep.append((t, x, sw if swc is None else swc, w, xd, sxd, y, a))
-    total = sh.sherry_gemv_f32_batched_prepare(descs)
-    dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
-    sh.sherry_gemv_f32_batched(dd, len(shapes), total)
+    if il:
+        total = sh.sherry_gemv_f32_il_batched_prepare(descs)
+        dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+        sh.sherry_gemv_f32_il_batched(dd, len(shapes), total)
+    else:
+        total = sh.sherry_gemv_f32_batched_prepare(descs)
+        dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+        sh.sherry_gemv_f32_batched(dd, len(shapes), total)
     torch.cuda.synchronize()
     return keep
 
 
-def test_fused_batched_parity(dev):
-    _say("fused batched")
+@pytest.mark.parametrize("il", [False, True])
+def test_fused_batched_parity(dev, il):
+    _say("fused batched", "il" if il else "tiled")
     # rows of 17-32 units run unsplit in one wave (3072: 24 units; 4000: a
     # ragged 32nd unit), 2176 (17 units) is the shortest such row
     shapes = [(64, 128), (65, 132), (2048, 2048), (512, 2048), (300, 8192), (1, 4), (70, 1032),
               (100, 8196), (65, 14336), (3, 32768), (96, 3072), (33, 4000), (130, 2176),
               (64, 4224)]
-    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 49):
+    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 49, il=il):
         sx_ref, acc_ref, y_ref = _fused_ref(x, t, sw)
         assert sxd.cpu().numpy()[0] == sx_ref[0]
         assert np.array_equal(a.cpu().numpy(), acc_ref[0])
         assert _y_ok(y.cpu().numpy(), y_ref[0])
 
 
-def test_fused_batched_channel_scales(dev):
-    _say("fused batched channel scales")
+@pytest.mark.parametrize("il", [False, True])
+def test_fused_batched_channel_scales(dev, il):
+    _say("fused batched channel scales", "il" if il else "tiled")
     shapes = [(64, 128), (65, 132), (2048, 2048), (300, 8192), (1, 4), (100, 8196)]
-    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 51, channel=True):
+    for t, x, sw, w, xd, sxd, y, a in _fused_batched(dev, shapes, 51, channel=True, il=il):
         q, sx = oracle.quantize_act(x)
         assert sxd.cpu().numpy()[0] == sx[0]
         acc_ref = oracle.gemm_i32(q, t, threads=8)
@@ -713,12 +721,28 @@ def test_fused_batched_mixed_scales(dev):
         _check_mixed(q, t, sx, sw, y.cpu().numpy(), a.cpu().numpy())
 
 
-def test_fused_batched_decode_step_llama_1b(dev):
+def test_fused_batched_layouts_agree(dev):
+    # tiled and lane-interleaved weights of the same matrices: the same bits
+    # (int32 sums are exact; the epilogue is the same arithmetic)
+    _say("fused batched tiled vs il")
+    shapes = [(64, 128), (65, 132), (2048, 2048), (300, 8192), (1, 4), (70, 1032), (3, 32768),
+              (130, 2176), (64, 4224)] + [(64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700))
+                                          for i in range(60)]
+    a = _fused_batched(dev, shapes, 53, channel="mixed_no_groups")
+    b = _fused_batched(dev, shapes, 53, channel="mixed_no_groups", il=True)
+    for ka, kb in zip(a, b):
+        assert np.array_equal(ka[6].cpu().numpy().view(np.uint32), kb[6].cpu().numpy().view(np.uint32))
+        assert np.array_equal(ka[7].cpu().numpy(), kb[7].cpu().numpy())
+        assert ka[5].cpu().numpy()[0] == kb[5].cpu().numpy()[0]
+
+
+@pytest.mark.parametrize("il", [False, True])
+def test_fused_batched_decode_step_llama_1b(dev, il):
     # the benchmark's decode step: 112 products of LLaMA-3.2-1B, one fused
     # launch; every int32 accumulator and fp32 output against the oracle
-    _say("fused batched llama-1b step")
+    _say("fused batched llama-1b step", "il" if il else "tiled")
     shapes = [(lin.n, lin.k) for _, lin in synth.model_linears(synth.LLAMA_1B)]
-    keep = _fused_batched(dev, shapes, 50, with_scale=False)
+    keep = _fused_batched(dev, shapes, 50, with_scale=False, il=il)
     assert len(keep) == 112
     for t, x, sw, w, xd, sxd, y, a in keep:
         q, sx = oracle.quantize_act(x)

@@ -114,6 +114,48 @@ def test_pack_hand_derived_bytes(idx):
 
 
 @pytest.mark.parametrize("idx", [0, 1])
+def test_pack_il_hand_derived_bytes(idx):
+    with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
+        fx = json.load(f)["lane_interleaved"][idx]
+    t = _fixture_t(fx)
+    p = oracle.pack_il(t)
+    assert p.size == fx["total_bytes"] == oracle.packed_bytes(fx["n"], fx["k"])
+    nz = {int(i): int(p[i]) for i in np.nonzero(p)[0]}
+    assert nz == {int(a): b for a, b in fx["nonzero"].items()}
+    assert np.array_equal(oracle.unpack_il(p, fx["n"], fx["k"]), t)
+
+
+@pytest.mark.parametrize("n,k", [(1, 4), (64, 128), (65, 132), (130, 1028), (200, 260)])
+def test_pack_il_round_trip_and_same_codes(n, k):
+    # the interleaved layout is a per-unit permutation of the tiled one: the
+    # same bytes size, every unit holding the same multiset of 5-bit codes,
+    # and the matrix read back exactly
+    t = synth.ternary_34(n, k, 8, "il", n, k)
+    a, b = oracle.pack(t), oracle.pack_il(t)
+    assert a.size == b.size
+    assert np.array_equal(oracle.unpack_il(b, n, k), t)
+
+    def unit_codes(p):
+        bits = np.unpackbits(p.reshape(-1, 1280), axis=1, bitorder="little")
+        head = bits[:, :1024 * 8].reshape(-1, 64, 128)
+        tail = bits[:, 1024 * 8:].reshape(-1, 64, 32)
+        stream = np.concatenate([head, tail], axis=2).reshape(-1, 64, 32, 5)
+        codes = (stream * (1 << np.arange(5))).sum(-1)
+        return np.sort(codes.reshape(codes.shape[0], -1), axis=1)
+    assert np.array_equal(unit_codes(a), unit_codes(b))
+    if n > 1:
+        assert not np.array_equal(a, b)
+
+
+def test_pack_il_rejects_non_34():
+    t = np.zeros((3, 8), np.int8)
+    t.reshape(3, 2, 4)[:, :, 1:] = 1
+    t[2, 4:8] = [1, 1, 1, 1]
+    with pytest.raises(oracle.OracleError):
+        oracle.pack_il(t)
+
+
+@pytest.mark.parametrize("idx", [0, 1])
 def test_pack2_hand_derived_bytes(idx):
     with open(os.path.join(GOLDEN, "packed_fixtures.json")) as f:
         fx = json.load(f)["two_bit"][idx]
