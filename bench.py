@@ -7,14 +7,16 @@ o 2048x2048, gate/up 8192x2048, down 2048x8192} -- as 3:4 ternary weights
 packed at 1.25 bits, per-tensor scales U(0.01, 0.05), a fresh fp32 N(0,1)
 activation vector per projection.  A step is the whole hot path on device in
 one launch: per-token int8 quantization of each of the 112 activation vectors
-fused with its product (sherry_gemv_f32_batched).  Weights and activations are
-rotated over 16 copies (2.4 GB, about 10x the 256 MB Infinity Cache, so cache
-hits cannot inflate the figures).
+fused with its product, on lane-interleaved weights (sherry_pack_il,
+sherry_gemv_f32_il_batched).  Weights and activations are rotated over 16
+copies (2.4 GB, about 10x the 256 MB Infinity Cache, so cache hits cannot
+inflate the figures).
 
 Prints one JSON line.  `value` = algorithmic bytes of a step / step time
 (GB/s), timed with HIP events around back-to-back steps on the stream the
 kernel runs on, after a heat-up; `roofline` is that same fused kernel;
-`unfused` times the same step as separate quantize and int8 product launches;
+`fused_tiled` times the same step on the tiled layout; `unfused` times it as
+separate quantize and int8 product launches;
 `cpu_baseline` is the CPU oracle on the host cores over full steps.  Unless
 --no-extra, the M = 2048 prefill GEMM on the LLaMA-3.2-3B and -1B shapes is
 timed too (dense-equivalent TOPS).
@@ -69,11 +71,13 @@ class DecodeStep:
         self.packed = []   # device packed weights, [copy][i]
         self.scales = []
         host_packed = []
+        host_il = []       # the same matrices, lane-interleaved (sherry_pack_il)
         for i, (layer, lin) in enumerate(self.lins):
             t = synth.ternary_34(lin.n, lin.k, seed, "w", layer, lin.name)
             if keep_host:
                 self.t.append(t)
             host_packed.append(sh.sherry_pack(t))
+            host_il.append(sh.sherry_pack_il(t))
             self.scales.append(synth.weight_scale(seed, "s", layer, lin.name))
         log("generated+packed %d weights in %.1fs" % (sum(l.n * l.k for _, l in self.lins),
                                                        time.time() - t0))
@@ -115,9 +119,19 @@ class DecodeStep:
                 f.n, f.k, f.w_scale = d.n, d.k, d.w_scale
             ftotal = sh.sherry_gemv_f32_batched_prepare(fdescs)
             fdev = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
+            # the same fused step on lane-interleaved weights (same buffers
+            # otherwise): the timed headline step
+            w_il = [torch.from_numpy(p).to(dev) for p in host_il]
+            for i in range(self.count):
+                fdescs[i].w = w_il[i].data_ptr()
+            ftotal_il = sh.sherry_gemv_f32_il_batched_prepare(fdescs)
+            fdev_il = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
             # the same step with one weight scale per output channel (Eq. 5)
             for i in range(self.count):
                 fdescs[i].w_scales = self.channel_scales[i].data_ptr()
+            fdev_ch_il = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
+            for i in range(self.count):
+                fdescs[i].w = w[i].data_ptr()
             fdev_ch = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
             # every activation matrix of the step in one quantize launch
             qdescs = (sh.sherry_quant_desc * len(self.ks))()
@@ -128,8 +142,9 @@ class DecodeStep:
                 qd.m, qd.k = xs[kk].shape[0], kk
             qrows, qmaxk = sh.sherry_quantize_act_batched_prepare(qdescs)
             qdev = torch.from_numpy(sh.descs_to_bytes(qdescs)).to(dev)
-            cp = dict(w=w, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total,
-                      fdescs=fdev, ftotal=ftotal, fdescs_ch=fdev_ch, qdescs=qdev,
+            cp = dict(w=w, w_il=w_il, xs=xs, qs=qs, sxs=sxs, ys=ys, descs=ddev, total=total,
+                      fdescs=fdev, ftotal=ftotal, fdescs_ch=fdev_ch, fdescs_il=fdev_il,
+                      ftotal_il=ftotal_il, fdescs_ch_il=fdev_ch_il, qdescs=qdev,
                       qrows=qrows, qmaxk=qmaxk)
             if c == 0:
                 # the same fused step with int32 outputs as well (parity check)
@@ -138,8 +153,9 @@ class DecodeStep:
                 for i in range(self.count):
                     fdescs[i].w_scales = None
                     fdescs[i].acc = accs[i].data_ptr()
+                    fdescs[i].w = w_il[i].data_ptr()
                 cp["accs"] = accs
-                cp["fdescs_acc"] = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
+                cp["fdescs_acc_il"] = torch.from_numpy(sh.descs_to_bytes(fdescs)).to(dev)
             self.copies.append(cp)
         torch.cuda.synchronize()
         self.total_blocks = self.copies[0]["total"]
@@ -171,12 +187,18 @@ class DecodeStep:
         self.sh.sherry_gemv_batched(cp["descs"], self.count, cp["total"])
 
     def fused(self, c):
+        # the headline step: fused quantization + products, lane-interleaved
         cp = self.copies[c]
-        self.sh.sherry_gemv_f32_batched(cp["fdescs"], self.count, cp["ftotal"])
+        self.sh.sherry_gemv_f32_il_batched(cp["fdescs_il"], self.count, cp["ftotal_il"])
 
     def fused_channel(self, c):
         cp = self.copies[c]
-        self.sh.sherry_gemv_f32_batched(cp["fdescs_ch"], self.count, cp["ftotal"])
+        self.sh.sherry_gemv_f32_il_batched(cp["fdescs_ch_il"], self.count, cp["ftotal_il"])
+
+    def fused_tiled(self, c):
+        # the same step on the tiled layout
+        cp = self.copies[c]
+        self.sh.sherry_gemv_f32_batched(cp["fdescs"], self.count, cp["ftotal"])
 
 
 def _events(torch):
@@ -196,11 +218,12 @@ def settle(run, torch, seconds=0.02):
         torch.cuda.synchronize()
 
 
-def bench_fused(step: DecodeStep, torch, steps, warmup, channel=False):
+def bench_fused(step: DecodeStep, torch, steps, warmup, channel=False, tiled=False):
     """ms per decode step (one fused launch), back to back after a heat-up;
-    channel=True runs the step with per-channel weight scales."""
+    channel=True runs the step with per-channel weight scales, tiled=True on
+    the tiled layout instead of the lane-interleaved one."""
     ncp = len(step.copies)
-    run = step.fused_channel if channel else step.fused
+    run = step.fused_tiled if tiled else (step.fused_channel if channel else step.fused)
     heat(step.sh, torch, step.dev)
     settle(lambda i: run(i % ncp), torch)
     for i in range(warmup):
@@ -802,7 +825,7 @@ def step_parity(sh, step: DecodeStep, torch, ref):
     cp = step.copies[0]
     ys = step.timed_y
     torch.cuda.synchronize()
-    sh.sherry_gemv_f32_batched(cp["fdescs_acc"], step.count, cp["ftotal"])
+    sh.sherry_gemv_f32_il_batched(cp["fdescs_acc_il"], step.count, cp["ftotal_il"])
     torch.cuda.synchronize()
     accs = [a.cpu().numpy() for a in cp["accs"]]
     sxs = {kk: cp["sxs"][kk].cpu().numpy() for kk in step.ks}
@@ -961,10 +984,12 @@ def main():
     log("decode step (fused quantize + product, one launch) %.2f us, %.0f GB/s" %
         (ms_step * 1e3, value))
     if args.only == "decode":
-        print(json.dumps({"kernel": "gemv_f32_batched_kernel", "launches": args.steps,
+        print(json.dumps({"kernel": "gemv_f32_batched_kernel<true>", "launches": args.steps,
                           "avg_launch_us": round(ms_step * 1e3, 3),
                           "bytes_per_launch": step.fused_bytes}), flush=True)
         return
+    ms_tiled = bench_fused(step, torch, args.steps, args.warmup, tiled=True)
+    log("the same step on the tiled layout %.2f us" % (ms_tiled * 1e3))
     ms_unfused = bench_unfused(step, torch, args.steps, args.warmup)
     ms_two = bench_two_launch(step, torch, args.steps, args.warmup)
     kern_ms = bench_product_only(step, torch, args.product_launches)
@@ -983,13 +1008,18 @@ def main():
                    "weights_mb_per_copy": round(step.weight_bytes / 1e6, 2),
                    "working_set_mb": round(step.weight_bytes * args.copies / 1e6, 1),
                    "step": "1 launch: per-token int8 quantization fused with the 112 products",
+                   "weights": "lane-interleaved units (sherry_pack_il)",
                    "seed": args.seed},
         "roofline": {"bound": "hbm", "achieved": round(value, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 4),
                      "traffic": load_traffic(src_hash),
-                     "kernel": "gemv_f32_batched_kernel", "bytes_per_launch": step.fused_bytes,
+                     "kernel": "gemv_f32_batched_kernel<true>",
+                     "bytes_per_launch": step.fused_bytes,
                      "avg_launch_us": round(ms_step * 1e3, 3),
                      "kernel_source_hash": src_hash},
+        "fused_tiled": {"step_us": round(ms_tiled * 1e3, 2),
+                        "gbs": round(step.fused_bytes / (ms_tiled * 1e-3) / 1e9, 1),
+                        "what": "the same fused step on the tiled layout (sherry_gemv_f32_batched)"},
         "two_launch": {"step_us": round(ms_two * 1e3, 2),
                        "gbs": round(step.fused_bytes / (ms_two * 1e-3) / 1e9, 1),
                        "launches": "sherry_quantize_act_batched (112 rows) + "
