@@ -524,13 +524,15 @@ def bench_model_step(sh, torch, dev, spec, seed, copies, steps=100):
     return out
 
 
-def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20, group_scales=False):
+def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20, group_scales=False,
+                       il=False):
     """All linears of the model at M tokens in one grouped launch
     (sherry_gemm_batched, small-M MFMA kernel), int8 activations ready; with
-    group_scales every product carries per-group (128 along K) scales."""
+    group_scales every product carries per-group (128 along K) scales; with
+    il the weights are lane-interleaved (sherry_gemm_il_batched, M <= 16)."""
     lins = synth.model_linears(spec)
-    host = [sh.sherry_pack(synth.ternary_34(l.n, l.k, seed, "w", layer, l.name))
-            for layer, l in lins]
+    pack = sh.sherry_pack_il if il else sh.sherry_pack
+    host = [pack(synth.ternary_34(l.n, l.k, seed, "w", layer, l.name)) for layer, l in lins]
     sets = []
     for c in range(copies):
         w = [torch.from_numpy(p).to(dev) for p in host]
@@ -548,11 +550,13 @@ def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20, group_sca
             d.n, d.k, d.m, d.w_scale = l.n, l.k, m, 0.02
             if group_scales:
                 d.w_group_scales = gsc[i].data_ptr()
-        total, max_m = sh.sherry_gemm_batched_prepare(descs)
+        prep = sh.sherry_gemm_il_batched_prepare if il else sh.sherry_gemm_batched_prepare
+        total, max_m = prep(descs)
         dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
         sets.append((w, q, sx, ys, dd, total, max_m, gsc))
-    run = lambda i: sh.sherry_gemm_batched(sets[i % copies][4], len(lins), sets[i % copies][5],
-                                           sets[i % copies][6])
+    launch = sh.sherry_gemm_il_batched if il else sh.sherry_gemm_batched
+    run = lambda i: launch(sets[i % copies][4], len(lins), sets[i % copies][5],
+                           sets[i % copies][6])
     settle(run, torch, 0.02)
     a, b = _events(torch)
     a.record()
@@ -568,6 +572,7 @@ def bench_model_step_m(sh, torch, dev, spec, seed, m, copies, reps=20, group_sca
     del sets
     torch.cuda.empty_cache()
     return {"m": m, "products": len(lins), "group_scales": group_scales,
+            "weights": "lane-interleaved" if il else "tiled",
             "step_us": round(us, 2), "bytes_per_step": byts,
             "gbs": round(byts / (us * 1e-6) / 1e9, 1),
             "tops": round(sum(2.0 * m * l.n * l.k for _, l in lins) / (us * 1e-6) / 1e12, 1)}
@@ -948,6 +953,8 @@ def main():
     if args.only == "grouped":
         rows = [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2)
                 for mm in (4, 16)]
+        rows += [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2, il=True)
+                 for mm in (4, 8, 16)]
         rows.append(bench_model_step_m(sh, torch, dev, synth.STRESS_8B, args.seed, 64, 1))
         rows += [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2,
                                     group_scales=True) for mm in (4, 16)]
@@ -1074,7 +1081,11 @@ def main():
                    "llama-3.2-3b-group128": [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B,
                                                                 args.seed, mm, 2,
                                                                 group_scales=True)
-                                             for mm in (4, 16)]}
+                                             for mm in (4, 16)],
+                   "llama-3.2-3b-interleaved": [bench_model_step_m(sh, torch, dev,
+                                                                   synth.LLAMA_3B, args.seed,
+                                                                   mm, 2, il=True)
+                                                for mm in (4, 8, 16)]}
         for name, rows in grouped.items():
             for r in rows:
                 log("grouped step %s M=%d: %.2f us, %.0f GB/s, %.1f TOPS" %

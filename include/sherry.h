@@ -335,6 +335,20 @@ int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
 int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
                         int64_t total_blocks, int32_t max_m, void* stream);
 
+/* Grouped products of up to 16 tokens on lane-interleaved weights
+ * (sherry_pack_il), per-tensor or per-channel scales: the 4-token GEMV
+ * (every m <= 4 and m * ceil(k/128) * 128 <= 32768; launch value = the
+ * largest m) or the 16-token window kernel (launch value = the largest m,
+ * at least 5), each with one int8 MFMA per chunk slot and two activation
+ * reads per unit.  _prepare validates as sherry_gemm_batched_prepare and
+ * returns SHERRY_E_SHAPE for m > 16 and SHERRY_E_INVALID for per-group
+ * scales.  Results bit-identical to sherry_gemm_batched on the tiled layout
+ * of the same matrices (int32 sums exact, same epilogue). */
+int sherry_gemm_il_batched_prepare(sherry_gemm_desc* descs, int count,
+                                   int64_t* total_blocks, int32_t* max_m);
+int sherry_gemm_il_batched(const sherry_gemm_desc* descs_dev, int count,
+                           int64_t total_blocks, int32_t max_m, void* stream);
+
 /* ---------------------------------------------------------------------- */
 /* Fused quantization + M = 1 product: fp32 activations in, one launch.    */
 /* Each workgroup quantizes the activation row (exactly as                 */

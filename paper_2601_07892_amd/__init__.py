@@ -48,6 +48,7 @@ EXPORTS = [
     "sherry_gemv3_batched_prepare", "sherry_gemv3_batched", "sherry_quantize_act_batched_prepare",
     "sherry_quantize_act_batched", "sherry_pack_il", "sherry_unpack_il",
     "sherry_gemv_f32_il_batched_prepare", "sherry_gemv_f32_il_batched",
+    "sherry_gemm_il_batched_prepare", "sherry_gemm_il_batched",
 ]
 
 
@@ -141,6 +142,9 @@ def _load():
         "sherry_gemm_batched_prepare": ([ctypes.POINTER(sherry_gemm_desc), ctypes.c_int, i64p,
                                          ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
         "sherry_gemm_batched": ([vp, ctypes.c_int, i64, ctypes.c_int32, vp], ctypes.c_int),
+        "sherry_gemm_il_batched_prepare": ([ctypes.POINTER(sherry_gemm_desc), ctypes.c_int, i64p,
+                                            ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+        "sherry_gemm_il_batched": ([vp, ctypes.c_int, i64, ctypes.c_int32, vp], ctypes.c_int),
         "sherry_gemm_channel": ([vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp],
                                 ctypes.c_int),
         "sherry_gemv_f32_channel": ([vp, vp, vp, vp, vp, vp, i64, i64, vp], ctypes.c_int),
@@ -447,6 +451,20 @@ def sherry_gemm_batched(descs_dev, count: int, total_blocks: int, max_m: int, st
     """descs_dev: device uint8 tensor holding a byte copy of prepared descriptors."""
     _check(lib.sherry_gemm_batched(_ptr(descs_dev), count, total_blocks, max_m, _stream(stream)),
            "sherry_gemm_batched")
+
+
+def sherry_gemm_il_batched_prepare(descs) -> tuple[int, int]:
+    """As sherry_gemm_batched_prepare, for lane-interleaved weights (m <= 16)."""
+    total = ctypes.c_int64(0)
+    mm = ctypes.c_int32(0)
+    _check(lib.sherry_gemm_il_batched_prepare(descs, len(descs), ctypes.byref(total),
+                                              ctypes.byref(mm)), "sherry_gemm_il_batched_prepare")
+    return int(total.value), int(mm.value)
+
+
+def sherry_gemm_il_batched(descs_dev, count: int, total_blocks: int, max_m: int, stream=None):
+    _check(lib.sherry_gemm_il_batched(_ptr(descs_dev), count, total_blocks, max_m,
+                                      _stream(stream)), "sherry_gemm_il_batched")
 
 
 def sherry_gemv2(w2, x, x_scale, w_scale: float, y, acc, n: int, k: int, stream=None):

@@ -482,6 +482,47 @@ extern "C" int sherry_gemm_batched_prepare(sherry_gemm_desc* descs, int count,
   return SHERRY_OK;
 }
 
+extern "C" int sherry_gemm_il_batched_prepare(sherry_gemm_desc* descs, int count,
+                                              int64_t* total_blocks, int32_t* max_m) {
+  if (!descs || !total_blocks || !max_m || count < 1) return SHERRY_E_INVALID;
+  int32_t mm = 0;
+  for (int i = 0; i < count; ++i) {
+    const sherry_gemm_desc& d = descs[i];
+    int st = check_product(d.w, d.x, d.x_scale, d.y, d.m, d.n, d.k, 16);
+    if (st != SHERRY_OK) return st;
+    if (d.m > 16) return SHERRY_E_SHAPE;
+    if ((d.acc && !aligned(d.acc, 4)) || (d.w_scales && !aligned(d.w_scales, 4)))
+      return SHERRY_E_ALIGN;
+    if (d.w_group_scales) return SHERRY_E_INVALID;  // tiled units only
+    if (d.m > mm) mm = d.m;
+  }
+  // launch value 1-4: the 4-token GEMV (every m <= 4, every product's rows fit
+  // its LDS staging); 5-16: the 16-token window kernel
+  bool tok = mm <= 4;
+  for (int i = 0; tok && i < count; ++i) tok = gemv_tok_fits(descs[i].m, descs[i].k);
+  int64_t blocks = 0;
+  for (int i = 0; i < count; ++i) {
+    sherry_gemm_desc& d = descs[i];
+    d.block_begin = static_cast<int32_t>(blocks);
+    d.reserved = 0;
+    blocks += tok ? gemv_tok_blocks(d.n, d.k) : smallm_blocks(d.n);
+    if (blocks > INT32_MAX) return SHERRY_E_SHAPE;
+  }
+  *total_blocks = blocks;
+  *max_m = tok ? mm : (mm < 5 ? 5 : mm);
+  return SHERRY_OK;
+}
+
+extern "C" int sherry_gemm_il_batched(const sherry_gemm_desc* descs_dev, int count,
+                                      int64_t total_blocks, int32_t max_m, void* stream) {
+  if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)
+    return SHERRY_E_INVALID;
+  if (max_m < 1 || max_m > 16) return SHERRY_E_SHAPE;
+  if (!aligned(descs_dev, 8)) return SHERRY_E_ALIGN;
+  if (max_m <= 4) return launch_gemv_tok_il_batched(descs_dev, count, total_blocks, as_stream(stream));
+  return launch_smallm_il_batched(descs_dev, count, total_blocks, as_stream(stream));
+}
+
 extern "C" int sherry_gemm_batched(const sherry_gemm_desc* descs_dev, int count,
                                    int64_t total_blocks, int32_t max_m, void* stream) {
   if (!descs_dev || count < 1 || total_blocks < 1 || total_blocks > INT32_MAX)

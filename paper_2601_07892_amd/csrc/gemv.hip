@@ -554,15 +554,20 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
       ring_run_groups<M>(ring, range, gr, C, c0, c1, xsrc, lut, acc, accf);
     }
   } else if constexpr (std::is_same_v<X, XFromLdsMfmaIL>) {
-    static_assert(M == 1, "the lane-interleaved source serves one token here");
+    static_assert(M <= 4, "the lane-interleaved source serves up to four tokens here");
     uint32_t ring[kRing][5];
     ring_fill(ring, range);
     v4i macc[4] = {};
     ring_run(ring, range, c0, c1, xsrc, lut, macc);
-    // lane l < 16 holds row 16g + l of the tile in accumulator g
+    // lane l < 16 holds token m of row 16g + l of the tile in element m of
+    // accumulator g; red may be the LDS of the staged rows, reused once every
+    // wave has finished reading it
+    __syncthreads();
     if (lane < 16) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) red[wave * 64 + 16 * g + lane] = macc[g][0];
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int m = 0; m < M; ++m) red[(wave * M + m) * 64 + 16 * g + lane] = macc[g][m];
     }
   } else if constexpr (kMfmaSource<X>) {
     static_assert(M <= 4 && !kGrp, "the matrix-core sources serve up to four tokens");
@@ -744,6 +749,46 @@ __device__ __forceinline__ void tok_batched_block(const sherry_gemm_desc& d, int
   gemv_block<M, kGrp>(d.w, XFromLdsMfmaTok{xq, kp, M}, StageRows<M>{d.x, d.x_scale, k, kp, xq},
                       WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k, g, S, lut,
                       reinterpret_cast<int32_t*>(xq), d.w_group_scales, tok_redf(xq));
+}
+
+// The same on lane-interleaved weights (per-tensor and per-channel scales).
+template <int M>
+__device__ __forceinline__ void tok_il_batched_block(const sherry_gemm_desc& d, int g,
+                                                     const uint32_t* lut, int8_t* xq) {
+  const int k = static_cast<int>(d.k);
+  const int kp = ((k + kTileK - 1) / kTileK) * kTileK;
+  const int S = gemv_split((k + kTileK - 1) / kTileK);
+  gemv_block<M>(d.w, XFromLdsMfmaIL{xq, kp, M}, StageRows<M>{d.x, d.x_scale, k, kp, xq},
+                WScale{d.w_scales, d.w_scale}, d.y, d.acc, d.n, k, g, S, lut,
+                reinterpret_cast<int32_t*>(xq));
+}
+
+// Grouped products of up to four tokens each on lane-interleaved weights
+// (m * ceil(k/128) * 128 <= kTokMaxBytes, no per-group scales).
+__global__ __launch_bounds__(kGemvThreads) void gemv_tok_il_batched_kernel(
+    const sherry_gemm_desc* __restrict__ descs, int count) {
+  __shared__ uint32_t lut[32];
+  __shared__ __attribute__((aligned(16))) int8_t xq[kTokMaxBytes];
+  fill_lut(lut);
+  const int32_t blk = static_cast<int32_t>(blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  int lo = 0;
+  for (int base = 0; base < count; base += 64) {
+    const int i = base + lane;
+    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
+    const int len = __popcll(__ballot(ok));
+    lo = base + len - 1;
+    if (len < 64) break;
+  }
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  const sherry_gemm_desc& d = descs[lo];
+  const int g = blk - d.block_begin;
+  switch (d.m) {
+    case 1: tok_il_batched_block<1>(d, g, lut, xq); break;
+    case 2: tok_il_batched_block<2>(d, g, lut, xq); break;
+    case 3: tok_il_batched_block<3>(d, g, lut, xq); break;
+    default: tok_il_batched_block<4>(d, g, lut, xq); break;
+  }
 }
 
 // Grouped products of up to four tokens each (sherry_gemm_desc,
@@ -1085,6 +1130,12 @@ int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WSc
 int64_t gemv_tok_blocks(int64_t n, int64_t k) {
   return ceil_div(ceil_div(n, kTileRows) * gemv_split(static_cast<int>(ceil_div(k, kTileK))),
                   kGemvWaves);
+}
+
+int launch_gemv_tok_il_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                               hipStream_t s) {
+  return launch(gemv_tok_il_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
+                dim3(kGemvThreads), 0, s, descs, count);
 }
 
 int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,

@@ -228,12 +228,17 @@ int launch_gemv_tok(const uint8_t* w, const int8_t* x, const float* x_scale, WSc
                     const float* gs, float* y, int32_t* acc, int64_t m, int64_t n, int64_t k,
                     hipStream_t s);
 int64_t gemv_tok_blocks(int64_t n, int64_t k);
+// The same products on lane-interleaved weights (no per-group scales).
+int launch_gemv_tok_il_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                               hipStream_t s);
 int launch_gemv_tok_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
                             bool groups, hipStream_t s);
 
 // Up to 16 tokens on the matrix cores, weights as loaded, activations
 // staged per K window (grouped launches): one product's workgroup count, and
 // the launch.
+int launch_smallm_il_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                             hipStream_t s);
 int64_t smallm_blocks(int64_t n);
 int launch_smallm_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
                           bool groups, hipStream_t s);

@@ -129,7 +129,14 @@ struct SmProblem {
 // accumulators: element e < 8 of a lane belongs to row l % 32 of the tile,
 // e >= 8 to row l % 32 + 32, whose scales a lane-half swap of the loaded
 // ones provides.
-template <bool kG>
+//
+// kIL: lane-interleaved weights (sherry_pack_il; not with kG).  Lane 16b + t
+// holds, as chunk slot (g, p), row 16g + t's weights of chunk 4p + b, the B
+// operand of one v_mfma_i32_16x16x64_i8 over 16 rows and 64 weights; its A
+// operand, token m = lane % 16's chunks b and 4 + b of the unit, is read once
+// per unit and serves the four row groups.  D[m][t] lands in lane
+// 16(m/4) + t, element m % 4 of accumulator g.
+template <bool kG, bool kIL = false>
 __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lut,
                                          int8_t* stages, int8_t* zrow, float* xs) {
   const int tid = threadIdx.x, lane = tid & 63;
@@ -183,7 +190,9 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
     gqb = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * C + 4), 0, 0);
   }
 
+  static_assert(!(kG && kIL), "per-group scales: tiled units only");
   v16i c[2] = {v16i{}, v16i{}};
+  v4i acc4[4] = {};  // kIL accumulators, one per row group
   for (int w = 0; w < nwin; ++w) {
     // the next window's activations are in flight during this one
     stage_load(sv, rx, p.k, w + 1);
@@ -208,7 +217,30 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
           gqb = __builtin_amdgcn_raw_buffer_load_b128(gr, 4 * (lane * C + j + 8), 0, 0);
         }
       }
-      if (j < C) {
+      if (kIL && j < C) {
+        // the unit's activation operands: token lane % 16 (rows past m are
+        // zero in the stage), chunks b and 4 + b, b = lane / 16
+        const int8_t* ar = stages + (w & 1) * kStageBytes + (lane & 15) * kRowStride +
+                           16 * (8 * u + (lane >> 4));
+        const v4i xa[2] = {*reinterpret_cast<const v4i*>(ar),
+                           *reinterpret_cast<const v4i*>(ar + 64)};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          __builtin_amdgcn_sched_barrier(0);
+          uint32_t wv[16];
+          if (h == 0) sm_lookup<0>(ring[u % kSmRing], lut, wv, std::make_integer_sequence<int, 16>{});
+          else sm_lookup<16>(ring[u % kSmRing], lut, wv, std::make_integer_sequence<int, 16>{});
+          // slots (g, p) = (2h + (s >> 1), s & 1), alternating accumulators
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int sl = (i & 1) * 2 + (i >> 1);  // 0, 2, 1, 3
+            const v4i b = {static_cast<int>(wv[4 * sl]), static_cast<int>(wv[4 * sl + 1]),
+                           static_cast<int>(wv[4 * sl + 2]), static_cast<int>(wv[4 * sl + 3])};
+            acc4[2 * h + (sl >> 1)] =
+                __builtin_amdgcn_mfma_i32_16x16x64_i8(xa[sl & 1], b, acc4[2 * h + (sl >> 1)], 0, 0, 0);
+          }
+        }
+      } else if (j < C) {
         // codes 16h .. 16h + 15: 16 table reads in flight, then 4 chunks
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -272,6 +304,32 @@ __device__ __forceinline__ void sm_block(const SmProblem& p, int g, uint32_t* lu
     }
     return;
   }
+  if constexpr (kIL) {
+    // lane l, accumulator g, element e: token 4(l / 16) + e of tile row
+    // 16g + l % 16
+    float wsg[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int64_t row = int64_t(r) * kTileRows + 16 * g + (lane & 15);
+      wsg[g] = p.ws.at(row < p.n ? row : p.n - 1);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int t = 4 * (lane >> 4) + e;
+        const int64_t row = int64_t(r) * kTileRows + 16 * g + (lane & 15);
+        const int32_t v = acc4[g][e];
+        const float sc = xs[t] * wsg[g];
+        if (t < p.m && row < p.n) {
+          as_global_mut(p.y)[int64_t(t) * p.n + row] = static_cast<float>(v) * sc;
+          if (p.acc) as_global_mut(p.acc)[int64_t(t) * p.n + row] = v;
+        }
+      }
+    }
+    return;
+  }
   const int64_t row0 = int64_t(r) * kTileRows + (lane & 31);
   const float ws0 = p.ws.at(row0 < p.n ? row0 : p.n - 1);
   const float ws1 = p.ws.at(row0 + 32 < p.n ? row0 + 32 : p.n - 1);
@@ -319,7 +377,37 @@ __global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(kGro
   else sm_block<false>(p, blk - d.block_begin, lut, stages, zrow, xs);
 }
 
+// Grouped products of up to 16 tokens on lane-interleaved weights.
+__global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(4))) void smallm_il_batched_kernel(
+    const sherry_gemm_desc* __restrict__ descs, int count) {
+  __shared__ uint32_t lut[32];
+  __shared__ __attribute__((aligned(16))) int8_t stages[2 * kStageBytes];
+  __shared__ __attribute__((aligned(16))) int8_t zrow[kWinK];
+  __shared__ float xs[kSmTok];
+  const int32_t blk = static_cast<int32_t>(blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  int lo = 0;
+  for (int base = 0; base < count; base += 64) {
+    const int i = base + lane;
+    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
+    const int len = __popcll(__ballot(ok));
+    lo = base + len - 1;
+    if (len < 64) break;
+  }
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  const sherry_gemm_desc& d = descs[lo];
+  const SmProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m,
+                    WScale{d.w_scales, d.w_scale}, nullptr};
+  sm_block<false, true>(p, blk - d.block_begin, lut, stages, zrow, xs);
+}
+
 }  // namespace
+
+int launch_smallm_il_batched(const sherry_gemm_desc* descs, int count, int64_t total_blocks,
+                             hipStream_t s) {
+  return launch(smallm_il_batched_kernel, dim3(static_cast<unsigned>(total_blocks)),
+                dim3(kSmThreads), 0, s, descs, count);
+}
 
 int64_t smallm_blocks(int64_t n) { return ceil_div(ceil_div(n, kTileRows), kSmWaves); }
 

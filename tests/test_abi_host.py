@@ -181,6 +181,34 @@ def test_il_fused_prepare_rejects_group_scales():
     assert L.sherry_gemv_f32_il_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
 
 
+def test_il_grouped_prepare_without_launch():
+    def prep(cases, group=False):
+        descs = (sh.sherry_gemm_desc * len(cases))()
+        for i, (m, n, k) in enumerate(cases):
+            d = descs[i]
+            d.w, d.x, d.x_scale, d.y = FAKE, FAKE, FAKE, FAKE
+            d.n, d.k, d.m, d.w_scale = n, k, m, 0.02
+            if group and i == 0:
+                d.w_group_scales = FAKE
+        total, max_m = sh.sherry_gemm_il_batched_prepare(descs)
+        return [d.block_begin for d in descs], total, max_m
+    # the same block counts and launch values as the tiled grouped launches
+    assert prep([(4, 3072, 3072), (2, 1024, 3072), (1, 3072, 8192)]) == ([0, 12, 16], 40, 4)
+    assert prep([(4, 3072, 8320), (1, 64, 128)]) == ([0, 12], 13, 5)
+    assert prep([(16, 3072, 8192), (9, 1024, 3072)]) == ([0, 12], 16, 16)
+    with pytest.raises(sh.SherryError) as e:
+        prep([(17, 64, 128)])
+    assert e.value.status == sh.SHERRY_E_SHAPE
+    with pytest.raises(sh.SherryError) as e:
+        prep([(2, 64, 128)], group=True)
+    assert e.value.status == sh.SHERRY_E_INVALID
+    L = sh.lib
+    assert L.sherry_gemm_il_batched(None, 1, 1, 4, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_gemm_il_batched(FAKE, 1, 1, 17, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_il_batched(FAKE, 1, 1, 0, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_gemm_il_batched(FAKE + 4, 1, 1, 16, None) == sh.SHERRY_E_ALIGN
+
+
 def test_pack_large_multithreaded():
     n, k = 4096, 2048  # many row tiles -> several host threads
     t = synth.ternary_34(n, k, 22, "big")

@@ -162,7 +162,9 @@ def test_tok_kernel_group_scales_rejects_long_rows(dev):
                                     None) == sh.SHERRY_E_SHAPE
 
 
-def _grouped(dev, cases, seed, channel=False, groups=False):
+def _grouped(dev, cases, seed, channel=False, groups=False, il=False, outs=None):
+    # il: lane-interleaved weights on sherry_gemm_il_batched; outs: a list that
+    # receives each product's (y, acc) as host arrays
     sh = _sh()
     descs = (sh.sherry_gemm_desc * len(cases))()
     keep = []
@@ -170,7 +172,7 @@ def _grouped(dev, cases, seed, channel=False, groups=False):
         t = synth.ternary_34(n, k, seed, "tg", i)
         q = synth.int8_any(m, k, seed, "tgq", i)
         sx = _scales(m, seed, "tgs%d" % i)
-        w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+        w = torch.from_numpy(sh.sherry_pack_il(t) if il else sh.sherry_pack(t)).to(dev)
         qd, sxd = torch.from_numpy(q).to(dev), torch.from_numpy(sx).to(dev)
         y = torch.full((m, n), float("nan"), dtype=torch.float32, device=dev)
         a = torch.full((m, n), -7, dtype=torch.int32, device=dev)
@@ -189,10 +191,17 @@ def _grouped(dev, cases, seed, channel=False, groups=False):
             hold = torch.from_numpy(sw[1]).to(dev)
             d.w_group_scales, d.acc = hold.data_ptr(), None
         keep.append((t, q, sx, sw, d.acc is not None, w, qd, sxd, y, a, hold))
-    total, max_m = sh.sherry_gemm_batched_prepare(descs)
-    dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
-    sh.sherry_gemm_batched(dd, len(cases), total, max_m)
+    if il:
+        total, max_m = sh.sherry_gemm_il_batched_prepare(descs)
+        dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+        sh.sherry_gemm_il_batched(dd, len(cases), total, max_m)
+    else:
+        total, max_m = sh.sherry_gemm_batched_prepare(descs)
+        dd = torch.from_numpy(sh.descs_to_bytes(descs)).to(dev)
+        sh.sherry_gemm_batched(dd, len(cases), total, max_m)
     torch.cuda.synchronize()
+    if outs is not None:
+        outs.extend((y.cpu().numpy(), a.cpu().numpy()) for *_, y, a, hold in keep)
     for t, q, sx, sw, has_acc, w, qd, sxd, y, a, hold in keep:
         if isinstance(sw, tuple):
             y_ref, mag, _ = oracle.product_groups(q, t, sx, sw[1], threads=ORACLE_THREADS)
@@ -208,12 +217,13 @@ def _grouped(dev, cases, seed, channel=False, groups=False):
     return max_m
 
 
+@pytest.mark.parametrize("il", [False, True])
 @pytest.mark.parametrize("channel", [False, True])
-def test_tok_batched_parity(dev, channel):
+def test_tok_batched_parity(dev, channel, il):
     # 70 products of 1-4 tokens (two ballot rounds of the descriptor search)
-    _say("tok batched", channel)
+    _say("tok batched", channel, "il" if il else "tiled")
     cases = [(1 + i % 4, 64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700)) for i in range(70)]
-    assert _grouped(dev, cases, 73, channel) == 4
+    assert _grouped(dev, cases, 73, channel, il=il) == 4
 
 
 def test_tok_batched_group_scales(dev):
@@ -233,21 +243,23 @@ def test_tok_batched_group_scales_model_step_full(dev):
         4 | _sh().SHERRY_LAUNCH_GROUPS
 
 
+@pytest.mark.parametrize("il", [False, True])
 @pytest.mark.parametrize("m", [2, 4])
-def test_tok_batched_model_step_full(dev, m):
+def test_tok_batched_model_step_full(dev, m, il):
     # one LLaMA-3.2-3B layer at M tokens in one grouped launch, every output
-    _say("tok batched 3b layer", m)
+    _say("tok batched 3b layer", m, "il" if il else "tiled")
     spec = synth.LLAMA_3B
     blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
-    assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 74) == m
+    assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 74, il=il) == m
 
 
-def test_small_m_too_long_goes_to_window_kernel(dev):
+@pytest.mark.parametrize("il", [False, True])
+def test_small_m_too_long_goes_to_window_kernel(dev, il):
     # m <= 4 but one product cannot stage its activations: every product
     # runs on the 16-token window kernel (launch value 5)
-    _say("small m, long k")
+    _say("small m, long k", "il" if il else "tiled")
     cases = [(4, 64, 8320), (2, 130, 1028), (1, 65, 132)]
-    assert _grouped(dev, cases, 75) == 5
+    assert _grouped(dev, cases, 75, il=il) == 5
 
 
 # 5-16 tokens: the window kernel (16 token rows staged per 1024-value window
@@ -258,26 +270,29 @@ WINDOW_CASES = [(5, 64, 128), (16, 65, 132), (9, 600, 2048), (16, 257, 3076), (1
                 (16, 3072, 8192), (7, 70, 4), (16, 1024, 3072), (6, 520, 14340)]
 
 
+@pytest.mark.parametrize("il", [False, True])
 @pytest.mark.parametrize("channel", [False, True])
-def test_window_kernel_grouped_parity(dev, channel):
-    _say("window kernel", channel)
-    assert _grouped(dev, WINDOW_CASES, 76, channel) == 16
+def test_window_kernel_grouped_parity(dev, channel, il):
+    _say("window kernel", channel, "il" if il else "tiled")
+    assert _grouped(dev, WINDOW_CASES, 76, channel, il=il) == 16
 
 
-def test_window_kernel_many_products(dev):
+@pytest.mark.parametrize("il", [False, True])
+def test_window_kernel_many_products(dev, il):
     # 70 products of 5-16 tokens (two ballot rounds of the descriptor search)
-    _say("window kernel, 70 products")
+    _say("window kernel, 70 products", "il" if il else "tiled")
     cases = [(5 + i % 12, 64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700)) for i in range(70)]
-    assert _grouped(dev, cases, 77) == 16
+    assert _grouped(dev, cases, 77, il=il) == 16
 
 
+@pytest.mark.parametrize("il", [False, True])
 @pytest.mark.parametrize("m", [8, 16])
-def test_window_kernel_model_step_full(dev, m):
+def test_window_kernel_model_step_full(dev, m, il):
     # one LLaMA-3.2-3B layer at M tokens in one grouped launch, every output
-    _say("window kernel 3b layer", m)
+    _say("window kernel 3b layer", m, "il" if il else "tiled")
     spec = synth.LLAMA_3B
     blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
-    assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 78) == m
+    assert _grouped(dev, [(m, lin.n, lin.k) for lin in blk], 78, il=il) == m
 
 
 def test_window_kernel_group_scales(dev):
@@ -327,3 +342,17 @@ def test_window_kernel_extremes(dev):
     sh.sherry_gemm_batched(torch.from_numpy(sh.descs_to_bytes(descs)).to(dev), 1, total, max_m)
     torch.cuda.synchronize()
     assert np.array_equal(a.cpu().numpy(), oracle.gemm_i32(q, t, threads=ORACLE_THREADS))
+
+
+@pytest.mark.parametrize("mmax", [4, 16])
+def test_grouped_layouts_agree(dev, mmax):
+    # the same grouped products on tiled and on lane-interleaved weights:
+    # the same bits, y and int32 accumulators
+    _say("grouped tiled vs il", mmax)
+    cases = [(1 + i % mmax, 64 + 37 * (i % 5), 4 * (1 + (i * 97) % 700)) for i in range(40)]
+    a, b = [], []
+    _grouped(dev, cases, 87, channel=True, outs=a)
+    _grouped(dev, cases, 87, channel=True, il=True, outs=b)
+    for (ya, aa), (yb, ab) in zip(a, b):
+        assert np.array_equal(ya.view(np.uint32), yb.view(np.uint32))
+        assert np.array_equal(aa, ab)
