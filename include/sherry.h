@@ -136,6 +136,12 @@ int sherry_pack_il(const int8_t* t, int64_t n, int64_t k, uint8_t* out,
 int sherry_unpack_il(const uint8_t* packed, size_t packed_bytes, int64_t n,
                      int64_t k, int8_t* t_out);
 
+/* Device: rewrites tiled units (tiled, e.g. from sherry_ternarize_pack) as
+ * lane-interleaved units (il), both sherry_packed_bytes(n, k) bytes,
+ * 16-byte aligned and distinct; one wave per unit.  SHERRY_E_SHAPE as
+ * sherry_packed_bytes, SHERRY_E_INVALID for NULL or tiled == il. */
+int sherry_interleave(const uint8_t* tiled, uint8_t* il, int64_t n, int64_t k, void* stream);
+
 /* Sparse-AbsMean ternarization and packing on the GPU (Eq. 4, Eq. 5), the
  * step that turns full-precision weights into the packed layout.
  * w: device, fp32 [n][k] row-major (row = output channel, blocks of 4 along

@@ -48,7 +48,7 @@ EXPORTS = [
     "sherry_gemv3_batched_prepare", "sherry_gemv3_batched", "sherry_quantize_act_batched_prepare",
     "sherry_quantize_act_batched", "sherry_pack_il", "sherry_unpack_il",
     "sherry_gemv_f32_il_batched_prepare", "sherry_gemv_f32_il_batched",
-    "sherry_gemm_il_batched_prepare", "sherry_gemm_il_batched",
+    "sherry_gemm_il_batched_prepare", "sherry_gemm_il_batched", "sherry_interleave",
 ]
 
 
@@ -117,6 +117,7 @@ def _load():
         "sherry_pack": ([vp, i64, i64, vp, ctypes.c_size_t, i64p], ctypes.c_int),
         "sherry_pack_il": ([vp, i64, i64, vp, ctypes.c_size_t, i64p], ctypes.c_int),
         "sherry_unpack_il": ([vp, ctypes.c_size_t, i64, i64, vp], ctypes.c_int),
+        "sherry_interleave": ([vp, vp, i64, i64, vp], ctypes.c_int),
         "sherry_unpack": ([vp, ctypes.c_size_t, i64, i64, vp], ctypes.c_int),
         "sherry_quantize_act": ([vp, i64, i64, vp, vp, vp], ctypes.c_int),
         "sherry_gemv": ([vp, vp, vp, f32, vp, vp, i64, i64, vp], ctypes.c_int),
@@ -268,6 +269,12 @@ def sherry_unpack_il(p: np.ndarray, n: int, k: int) -> np.ndarray:
     t = np.empty((n, k), np.int8)
     _check(lib.sherry_unpack_il(p.ctypes.data, p.nbytes, n, k, t.ctypes.data), "sherry_unpack_il")
     return t
+
+
+def sherry_interleave(tiled, il, n: int, k: int, stream=None):
+    """Device: tiled packed bytes -> lane-interleaved packed bytes."""
+    _check(lib.sherry_interleave(_ptr(tiled), _ptr(il), n, k, _stream(stream)),
+           "sherry_interleave")
 
 
 def sherry_packed2_bytes(n: int, k: int) -> int:

@@ -399,3 +399,4 @@ extern "C" int sherry_unpack_il(const uint8_t* packed, size_t packed_bytes, int6
   });
   return sherry_unpack(tiled.data(), need, n, k, t_out);
 }
+

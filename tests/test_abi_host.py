@@ -209,6 +209,14 @@ def test_il_grouped_prepare_without_launch():
     assert L.sherry_gemm_il_batched(FAKE + 4, 1, 1, 16, None) == sh.SHERRY_E_ALIGN
 
 
+def test_interleave_validation_without_launch():
+    L = sh.lib
+    assert L.sherry_interleave(None, FAKE, 64, 128, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_interleave(FAKE, FAKE, 64, 128, None) == sh.SHERRY_E_INVALID
+    assert L.sherry_interleave(FAKE, FAKE + 4096, 64, 130, None) == sh.SHERRY_E_SHAPE
+    assert L.sherry_interleave(FAKE + 4, FAKE + 4096, 64, 128, None) == sh.SHERRY_E_ALIGN
+
+
 def test_pack_large_multithreaded():
     n, k = 4096, 2048  # many row tiles -> several host threads
     t = synth.ternary_34(n, k, 22, "big")

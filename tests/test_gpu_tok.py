@@ -356,3 +356,32 @@ def test_grouped_layouts_agree(dev, mmax):
     for (ya, aa), (yb, ab) in zip(a, b):
         assert np.array_equal(ya.view(np.uint32), yb.view(np.uint32))
         assert np.array_equal(aa, ab)
+
+
+@pytest.mark.parametrize("n,k", [(1, 4), (64, 128), (65, 132), (300, 3076), (2048, 8192)])
+def test_interleave_on_device_matches_host(dev, n, k):
+    # the device converter writes what the host interleaved packer writes;
+    # from GPU-ternarized weights too
+    sh = _sh()
+    _say("interleave", n, k)
+    t = synth.ternary_34(n, k, 88, "ilv", n, k)
+    tiled = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    il = torch.full_like(tiled, 0xA5)
+    sh.sherry_interleave(tiled, il, n, k)
+    torch.cuda.synchronize()
+    assert np.array_equal(il.cpu().numpy(), sh.sherry_pack_il(t))
+
+
+def test_interleave_after_gpu_ternarize(dev):
+    sh = _sh()
+    n, k = 300, 3076
+    w = torch.from_numpy(synth.dense_weights(n, k, 89, "tpil")).to(dev)
+    packed = torch.empty(sh.sherry_packed_bytes(n, k), dtype=torch.uint8, device=dev)
+    alpha = torch.empty(n, dtype=torch.float32, device=dev)
+    sh.sherry_ternarize_pack(w, n, k, packed, alpha)
+    il = torch.empty_like(packed)
+    sh.sherry_interleave(packed, il, n, k)
+    torch.cuda.synchronize()
+    t = sh.sherry_unpack(packed.cpu().numpy(), n, k)
+    assert np.array_equal(il.cpu().numpy(), sh.sherry_pack_il(t))
+    assert np.array_equal(sh.sherry_unpack_il(il.cpu().numpy(), n, k), t)
