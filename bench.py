@@ -885,14 +885,18 @@ def bench_config0(sh, torch, dev, seed, reps=3):
             "note": "one launch per GEMV; 665 KB per call, so launch latency dominates"}
 
 
-def load_traffic(src_hash: str):
+# the kernel of the headline step (the fused product on lane-interleaved units)
+DECODE_KERNEL = "gemv_f32_batched_kernel<true>"
+
+
+def load_traffic(src_hash: str, kernel: str):
     path = os.path.join(ROOT, "profiles", "traffic_gemv_f32_batched.json")
     try:
         with open(path) as f:
             d = json.load(f)
     except (OSError, ValueError):
         return None
-    if d.get("kernel_source_hash") != src_hash:
+    if d.get("kernel_source_hash") != src_hash or d.get("kernel") != kernel:
         return None
     return d.get("bytes_per_launch")
 
@@ -1019,8 +1023,8 @@ def main():
                    "seed": args.seed},
         "roofline": {"bound": "hbm", "achieved": round(value, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 4),
-                     "traffic": load_traffic(src_hash),
-                     "kernel": "gemv_f32_batched_kernel<true>",
+                     "traffic": load_traffic(src_hash, DECODE_KERNEL),
+                     "kernel": DECODE_KERNEL,
                      "bytes_per_launch": step.fused_bytes,
                      "avg_launch_us": round(ms_step * 1e3, 3),
                      "kernel_source_hash": src_hash},

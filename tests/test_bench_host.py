@@ -39,6 +39,7 @@ def test_traffic_record_is_gated_by_the_kernel_source():
     h = bench.kernel_source_hash(["gemv.hip", "sherry_internal.h"])
     assert len(h) == 16 and h == bench.kernel_source_hash(["gemv.hip", "sherry_internal.h"])
     assert h != bench.kernel_source_hash(["gemv.hip"])
-    assert bench.load_traffic("0" * 16) is None
-    got = bench.load_traffic(h)
+    assert bench.load_traffic("0" * 16, bench.DECODE_KERNEL) is None
+    assert bench.load_traffic(h, "gemv_f32_batched_kernel<false>") is None
+    got = bench.load_traffic(h, bench.DECODE_KERNEL)
     assert got is None or got > 154_862_016  # counters see at least the algorithmic bytes
