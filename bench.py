@@ -362,6 +362,28 @@ def bench_stream_ceiling(sh, torch, dev, nbytes=2 << 30, reps=20):
     return nbytes / (ms * 1e-3) / 1e9
 
 
+def bench_stream_same_bytes(sh, torch, dev, nbytes, copies=16, launches=400):
+    """The same streaming read over as many bytes per launch as the decode
+    step moves, rotated over copies like its weights and launched back to
+    back: the read ceiling at this transfer size, launch and ramp included."""
+    stride = (nbytes + 255) // 256 * 256
+    src = torch.empty(stride * copies, dtype=torch.uint8, device=dev)
+    sink = torch.empty(sh.sherry_stream_read_groups(nbytes), dtype=torch.int32, device=dev)
+    run = lambda i: sh.sherry_stream_read(src[(i % copies) * stride:], nbytes, sink)
+    settle(run, torch)
+    a, b = _events(torch)
+    torch.cuda.synchronize()
+    a.record()
+    for i in range(launches):
+        run(i)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) / launches * 1e3
+    del src, sink
+    return {"bytes": nbytes, "copies": copies, "us": round(us, 2),
+            "gbs": round(nbytes / (us * 1e-6) / 1e9, 1)}
+
+
 # ---------------------------------------------------------------------------
 # prefill GEMM (M = 2048)
 # ---------------------------------------------------------------------------
@@ -1057,6 +1079,11 @@ def main():
         for r in out["ternarize_pack"]:
             log("ternarize+pack %s: %.1f us, %.0f GB/s" % (r["shape"], r["us"], r["gbs"]))
         out["hbm_read_ceiling_gbs"] = round(bench_stream_ceiling(sh, torch, dev), 1)
+        same = bench_stream_same_bytes(sh, torch, dev, step.fused_bytes)
+        same["decode_step_over_read"] = round(same["us"] / (ms_step * 1e3), 4)
+        out["hbm_read_same_bytes"] = same
+        log("streaming read of the step's %d bytes: %.2f us, %.0f GB/s" %
+            (same["bytes"], same["us"], same["gbs"]))
         out["config0_single_gemv"] = bench_config0(sh, torch, dev, args.seed)
         log("config 0 single GEMV: %.2f us, %.0f GB/s" % (out["config0_single_gemv"]["us"],
                                                        out["config0_single_gemv"]["gbs"]))
