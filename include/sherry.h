@@ -138,8 +138,10 @@ int sherry_unpack_il(const uint8_t* packed, size_t packed_bytes, int64_t n,
 
 /* Device: rewrites tiled units (tiled, e.g. from sherry_ternarize_pack) as
  * lane-interleaved units (il), both sherry_packed_bytes(n, k) bytes,
- * 16-byte aligned and distinct; one wave per unit.  SHERRY_E_SHAPE as
- * sherry_packed_bytes, SHERRY_E_INVALID for NULL or tiled == il. */
+ * 16-byte aligned, and not overlapping (overlapping buffers give undefined
+ * results; only tiled == il is detected); one wave per unit.
+ * SHERRY_E_SHAPE as sherry_packed_bytes, SHERRY_E_INVALID for NULL or
+ * tiled == il, SHERRY_E_ALIGN for a misaligned buffer. */
 int sherry_interleave(const uint8_t* tiled, uint8_t* il, int64_t n, int64_t k, void* stream);
 
 /* Sparse-AbsMean ternarization and packing on the GPU (Eq. 4, Eq. 5), the
