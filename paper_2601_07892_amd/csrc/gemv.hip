@@ -20,6 +20,12 @@
 // any 64 lookups are free of bank conflicts.  The fused quantize + product
 // kernels (one token) accumulate on the matrix cores instead of with v_dot4
 // (dot_container_mfma).
+//
+// Lane-interleaved units (sherry_pack_il): the same stream, with each lane's
+// 4-code chunks arranged as B operands of v_mfma_i32_16x16x64_i8 over 16 rows
+// and 64 weights (dot_il), so that one activation operand per half unit
+// serves all four row groups; the fused one-token step and the grouped
+// products of up to four tokens have variants on them.
 #include <type_traits>
 #include <utility>
 

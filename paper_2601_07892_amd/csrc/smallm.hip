@@ -26,6 +26,12 @@
 // stays zero.  So D[m][t] = x_m . w(row t) and D[16 + m][t] = x_m . w(row
 // 32 + t): one MFMA per chunk serves 64 rows and 16 tokens, with no lane
 // exchange of the weights.
+//
+// On lane-interleaved units (kIL) each 4-code chunk slot of a lane is the B
+// operand of a v_mfma_i32_16x16x64_i8 over 16 rows and 64 weights instead;
+// lane 16b + m reads token m's chunks b and 4 + b of the unit from the
+// stage, an A operand that serves all four row groups (two 16-byte LDS reads
+// per unit and lane), and D[m][t] of row group g lands in lane 16(m/4) + t.
 #include "sherry_internal.h"
 
 namespace sherry {
