@@ -17,9 +17,13 @@ Prints one JSON line.  `value` = algorithmic bytes of a step / step time
 kernel runs on, after a heat-up; `roofline` is that same fused kernel;
 `fused_tiled` times the same step on the tiled layout; `unfused` times it as
 separate quantize and int8 product launches;
-`cpu_baseline` is the CPU oracle on the host cores over full steps.  Unless
---no-extra, the M = 2048 prefill GEMM on the LLaMA-3.2-3B and -1B shapes is
-timed too (dense-equivalent TOPS).
+`cpu_baseline` is the CPU oracle on the host cores over full steps;
+`parity` checks the timed step against the oracle.  Unless --no-extra, the
+M = 2048 prefill GEMM on the LLaMA-3.2-3B and -1B shapes is timed too
+(dense-equivalent TOPS), with context lines: streaming reads of 2 GiB and of
+the step's own bytes per launch (`hbm_read_same_bytes`), the 3B and 8B-scale
+decode steps, grouped small-M steps, the 1.25 / 1.67 / 2-bit layouts of one
+8B-scale step, GPU ternarize + pack and a single q-projection GEMV.
 """
 from __future__ import annotations
 
