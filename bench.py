@@ -938,11 +938,12 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="skip the M=2048 GEMM and ceiling")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", choices=["decode", "product", "prefill", "grouped", "ternarize",
-                                       "tables", "layouts"],
+                                       "tables", "layouts", "read"],
                     default=None,
                     help="run only one part (for profiler runs): the timed decode steps, the "
                          "back-to-back product launches, the M=2048 LLaMA-3.2-3B layer, the "
-                         "grouped small-M steps, or ternarize + pack")
+                         "grouped small-M steps, ternarize + pack, or the streaming read of "
+                         "the decode step's bytes per launch")
     ap.add_argument("--product-launches", type=int, default=1000,
                     help="back-to-back grouped product launches timed for the roofline")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -989,6 +990,12 @@ def main():
         rows += [bench_model_step_m(sh, torch, dev, synth.LLAMA_3B, args.seed, mm, 2,
                                     group_scales=True) for mm in (4, 16)]
         print(json.dumps({"decode_small_m_grouped": rows}), flush=True)
+        return
+    if args.only == "read":
+        nbytes = sum(sh.sherry_packed_bytes(l.n, l.k) + 4 * l.k + 4 + 4 * l.n
+                     for _, l in synth.model_linears(synth.LLAMA_1B))
+        print(json.dumps({"hbm_read_same_bytes": bench_stream_same_bytes(sh, torch, dev, nbytes)}),
+              flush=True)
         return
     if args.only == "tables":
         print(json.dumps({"activation_vs_weight_tables_3b": bench_activation_tables(
