@@ -322,13 +322,24 @@ def test_window_kernel_group_scales_need_whole_chunks(dev):
     assert _grouped(dev, cases, 86, groups=True) == 17 | _sh().SHERRY_LAUNCH_GROUPS
 
 
-def test_window_kernel_extremes(dev):
-    # activations at -128 / 127 for all 16 tokens, k = 4096 (4 windows)
+@pytest.mark.parametrize("il", [False, True])
+@pytest.mark.parametrize("m,k", [(16, 4096), (4, 8192)])
+def test_window_kernel_extremes(dev, m, k, il):
+    # activations at -128 / 127 for every token, k = 4096 (4 windows) at 16
+    # tokens and the longest k four tokens can stage (token kernels); row 0
+    # follows token 0's signs (three of every four weights), row 1 their
+    # opposite: the largest sums the activations allow
+    _say("extremes", m, k, "il" if il else "tiled")
     sh = _sh()
-    m, n, k = 16, 192, 4096
+    n = 192
     q = np.where(synth.int8_any(m, k, 79, "wext") >= 0, 127, -128).astype(np.int8)
     t = synth.ternary_34(n, k, 79, "wext")
-    w = torch.from_numpy(sh.sherry_pack(t)).to(dev)
+    sg = np.where(q[0] >= 0, 1, -1).astype(np.int8).reshape(-1, 4)
+    aligned = sg.copy()
+    aligned[:, 0] = 0
+    t[0] = aligned.reshape(-1)
+    t[1] = -aligned.reshape(-1)
+    w = torch.from_numpy(sh.sherry_pack_il(t) if il else sh.sherry_pack(t)).to(dev)
     qd = torch.from_numpy(q).to(dev)
     sxd = torch.ones(m, dtype=torch.float32, device=dev)
     y = torch.empty((m, n), dtype=torch.float32, device=dev)
@@ -337,11 +348,15 @@ def test_window_kernel_extremes(dev):
     d = descs[0]
     d.w, d.x, d.x_scale, d.y, d.acc = w.data_ptr(), qd.data_ptr(), sxd.data_ptr(), y.data_ptr(), a.data_ptr()
     d.n, d.k, d.m, d.w_scale = n, k, m, 1.0
-    total, max_m = sh.sherry_gemm_batched_prepare(descs)
-    assert max_m == 16
-    sh.sherry_gemm_batched(torch.from_numpy(sh.descs_to_bytes(descs)).to(dev), 1, total, max_m)
+    prep = sh.sherry_gemm_il_batched_prepare if il else sh.sherry_gemm_batched_prepare
+    launch = sh.sherry_gemm_il_batched if il else sh.sherry_gemm_batched
+    total, max_m = prep(descs)
+    assert max_m == m
+    launch(torch.from_numpy(sh.descs_to_bytes(descs)).to(dev), 1, total, max_m)
     torch.cuda.synchronize()
-    assert np.array_equal(a.cpu().numpy(), oracle.gemm_i32(q, t, threads=ORACLE_THREADS))
+    acc_ref = oracle.gemm_i32(q, t, threads=ORACLE_THREADS)
+    assert acc_ref[0, 0] == np.abs(q[0].astype(np.int64)).reshape(-1, 4)[:, 1:].sum()
+    assert np.array_equal(a.cpu().numpy(), acc_ref)
 
 
 @pytest.mark.parametrize("mmax", [4, 16])
