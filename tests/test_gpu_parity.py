@@ -578,14 +578,18 @@ def test_gemv2_parity(dev, n, k):
 
 def test_stream_read_checksum(dev):
     sh = _sh()
-    nbytes = 3 * 256 * 1024 + 4096
+    # the slice a workgroup reads: the smallest power of two past which a
+    # second workgroup is needed
+    slice_bytes = next(1 << i for i in range(10, 31) if sh.sherry_stream_read_groups((1 << i) + 1) == 2)
+    nbytes = 3 * slice_bytes + 4096
     src = torch.randint(0, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, device=dev)
     groups = sh.sherry_stream_read_groups(nbytes)
     sink = torch.empty(groups, dtype=torch.int32, device=dev)
     sh.sherry_stream_read(src, nbytes, sink)
     torch.cuda.synchronize()
     h = src.cpu().numpy().view(np.uint32)
-    per = 256 * 1024 // 4
+    per = slice_bytes // 4
+    assert groups == 4
     ref = [np.bitwise_xor.reduce(h[g * per:(g + 1) * per]) for g in range(groups)]
     assert np.array_equal(sink.cpu().numpy().view(np.uint32), np.array(ref, np.uint32))
 
