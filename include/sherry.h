@@ -317,13 +317,16 @@ typedef struct sherry_gemm_desc {
                          /* with w_scales, and acc must then be NULL       */
   int32_t n, k, m;       /* 1 <= m <= SHERRY_MAX_M                         */
   float w_scale;
-  int32_t block_begin;   /* written by sherry_gemm_batched_prepare         */
-  int32_t reserved;      /* set to 0                                       */
+  int32_t block_begin;   /* written by prepare: the product's first block  */
+  int32_t block_count;   /* written by prepare: its number of blocks       */
 } sherry_gemm_desc;
 
-/* Host: validates descs[0..count), fills each block_begin, *total_blocks
- * and *max_m, the launch value that selects the kernel and its token
- * blocks.  When every m <= 4 and every m * ceil(k/128) * 128 <= 32768, the
+/* Host: validates descs[0..count), fills each block_begin and block_count,
+ * *total_blocks and *max_m, the launch value that selects the kernel and its
+ * token blocks.  The blocks of the products are numbered in order of
+ * decreasing k (ties in array order), whatever the order of the array: the
+ * workgroups with the longest rows are dispatched first and the shorter ones
+ * fill in behind them.  When every m <= 4 and every m * ceil(k/128) * 128 <= 32768, the
  * products run on the matrix-core GEMV (SHERRY_KERNEL_GEMV_TOK, any scales)
  * and *max_m is the largest m (1..4); else, when every m <= 16 and no
  * descriptor has per-group scales, on the 16-token window kernel (weights as

@@ -85,7 +85,8 @@ class sherry_gemm_desc(ctypes.Structure):
         ("y", ctypes.c_void_p), ("acc", ctypes.c_void_p), ("w_scales", ctypes.c_void_p),
         ("w_group_scales", ctypes.c_void_p),
         ("n", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32),
-        ("w_scale", ctypes.c_float), ("block_begin", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("w_scale", ctypes.c_float), ("block_begin", ctypes.c_int32),
+        ("block_count", ctypes.c_int32),
     ]
 
 
@@ -445,8 +446,8 @@ def sherry_gemv_f32_il_batched(descs_dev, count: int, total_blocks: int, stream=
 
 
 def sherry_gemm_batched_prepare(descs) -> tuple[int, int]:
-    """Fills block_begin of a ctypes array of sherry_gemm_desc; returns
-    (total blocks, largest m)."""
+    """Fills block_begin and block_count of a ctypes array of sherry_gemm_desc
+    (blocks numbered longest rows first); returns (total blocks, launch value)."""
     total = ctypes.c_int64(0)
     mm = ctypes.c_int32(0)
     _check(lib.sherry_gemm_batched_prepare(descs, len(descs), ctypes.byref(total),

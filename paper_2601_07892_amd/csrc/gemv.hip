@@ -784,16 +784,8 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_tok_il_batched_kernel(
   __shared__ __attribute__((aligned(16))) int8_t xq[kTokMaxBytes];
   fill_lut(lut);
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
-  const int lane = threadIdx.x & 63;
-  int lo = 0;
-  for (int base = 0; base < count; base += 64) {
-    const int i = base + lane;
-    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
-    const int len = __popcll(__ballot(ok));
-    lo = base + len - 1;
-    if (len < 64) break;
-  }
-  lo = __builtin_amdgcn_readfirstlane(lo);
+  const int lo = find_block_desc(descs, count, blk);
+  if (lo < 0) return;
   const sherry_gemm_desc& d = descs[lo];
   const int g = blk - d.block_begin;
   switch (d.m) {
@@ -815,16 +807,8 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_tok_batched_kernel(
   __shared__ __attribute__((aligned(16))) int8_t xq[kTokMaxBytes];
   fill_lut(lut);
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
-  const int lane = threadIdx.x & 63;
-  int lo = 0;
-  for (int base = 0; base < count; base += 64) {
-    const int i = base + lane;
-    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
-    const int len = __popcll(__ballot(ok));
-    lo = base + len - 1;
-    if (len < 64) break;
-  }
-  lo = __builtin_amdgcn_readfirstlane(lo);
+  const int lo = find_block_desc(descs, count, blk);
+  if (lo < 0) return;
   const sherry_gemm_desc& d = descs[lo];
   const int g = blk - d.block_begin;
   if (kGroups && d.w_group_scales) {

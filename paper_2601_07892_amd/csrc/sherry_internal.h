@@ -162,6 +162,28 @@ __device__ __forceinline__ SHERRY_GLOBAL T* as_global_mut(T* p) {
   return (SHERRY_GLOBAL T*)(p);
 }
 
+// Descriptor of a grouped launch whose block range [block_begin, block_begin
+// + block_count) holds block blk (the grouped prepares number the products'
+// blocks longest rows first, so the ranges follow no order of the array):
+// 64 descriptors per ballot round.  -1 if none does (a grid larger than the
+// prepared total): the workgroup then has no work.
+template <class Desc>
+__device__ __forceinline__ int find_block_desc(const Desc* descs, int count, int32_t blk) {
+  const int lane = threadIdx.x & 63;
+  for (int base = 0; base < count; base += 64) {
+    const int i = base + lane;
+    bool hit = false;
+    if (i < count) {
+      const int32_t b0 = as_global(descs)[i].block_begin;
+      const int32_t nb = as_global(descs)[i].block_count;
+      hit = b0 <= blk && blk - b0 < nb;
+    }
+    const uint64_t m = __ballot(hit);
+    if (m) return __builtin_amdgcn_readfirstlane(base + static_cast<int>(__builtin_ctzll(m)));
+  }
+  return -1;
+}
+
 // Weight scale of output row n: one per tensor, or, when rows is set, one
 // per output channel ([T alpha]_ij = T_ij alpha_j, the footnote to Eq. 2).
 // A wave's run of n consecutive weight units of B bytes each, from base.

@@ -547,19 +547,9 @@ __global__ __launch_bounds__(64 * kSkWavesGrouped) void skinny_batched_kernel(
   uint32_t* lut = reinterpret_cast<uint32_t*>(lds);
   if (threadIdx.x < 32) lut[threadIdx.x] = decode_word(threadIdx.x);
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
-  // last descriptor with block_begin <= blk (a prefix of the array), found
-  // 64 descriptors per round trip with a ballot
-  const int lane = threadIdx.x & 63;
-  int lo = 0;
-  for (int base = 0; base < count; base += 64) {
-    const int i = base + lane;
-    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
-    const uint64_t mk = __ballot(ok);
-    const int len = __popcll(mk);
-    lo = base + len - 1;
-    if (len < 64) break;
-  }
-  lo = __builtin_amdgcn_readfirstlane(lo);
+  // the descriptor whose block range holds blk
+  const int lo = find_block_desc(descs, count, blk);
+  if (lo < 0) return;
   const sherry_gemm_desc& d = descs[lo];
   // a product's blocks: its tile groups for token block 0, then for token
   // block 1, ... (blocks in flight together share their activations)

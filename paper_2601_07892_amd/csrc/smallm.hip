@@ -366,16 +366,8 @@ __global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(kGro
   __shared__ __attribute__((aligned(16))) int8_t zrow[kWinK];
   __shared__ float xs[kSmTok];
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
-  const int lane = threadIdx.x & 63;
-  int lo = 0;
-  for (int base = 0; base < count; base += 64) {
-    const int i = base + lane;
-    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
-    const int len = __popcll(__ballot(ok));
-    lo = base + len - 1;
-    if (len < 64) break;
-  }
-  lo = __builtin_amdgcn_readfirstlane(lo);
+  const int lo = find_block_desc(descs, count, blk);
+  if (lo < 0) return;
   const sherry_gemm_desc& d = descs[lo];
   const SmProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m,
                     WScale{d.w_scales, d.w_scale}, d.w_group_scales};
@@ -391,16 +383,8 @@ __global__ __launch_bounds__(kSmThreads) __attribute__((amdgpu_waves_per_eu(4)))
   __shared__ __attribute__((aligned(16))) int8_t zrow[kWinK];
   __shared__ float xs[kSmTok];
   const int32_t blk = static_cast<int32_t>(blockIdx.x);
-  const int lane = threadIdx.x & 63;
-  int lo = 0;
-  for (int base = 0; base < count; base += 64) {
-    const int i = base + lane;
-    const bool ok = i < count && as_global(descs)[i].block_begin <= blk;
-    const int len = __popcll(__ballot(ok));
-    lo = base + len - 1;
-    if (len < 64) break;
-  }
-  lo = __builtin_amdgcn_readfirstlane(lo);
+  const int lo = find_block_desc(descs, count, blk);
+  if (lo < 0) return;
   const sherry_gemm_desc& d = descs[lo];
   const SmProblem p{d.w, d.x, d.x_scale, d.y, d.acc, d.n, d.k, d.m,
                     WScale{d.w_scales, d.w_scale}, nullptr};

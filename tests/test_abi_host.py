@@ -181,6 +181,37 @@ def test_il_fused_prepare_rejects_group_scales():
     assert L.sherry_gemv_f32_il_batched(FAKE + 4, 1, 1, None) == sh.SHERRY_E_ALIGN
 
 
+def test_grouped_prepare_numbers_blocks_longest_rows_first():
+    # one LLaMA-3.2-3B layer in model order and reversed, on the three
+    # grouped kernels: each product's range [block_begin, block_begin +
+    # block_count) is the same in both orders, the ranges tile the launch, and
+    # the products with the longest rows (k = 8192) come first
+    spec = synth.LLAMA_3B
+    blk = synth.llama_block(spec["hidden"], spec["kv"], spec["inter"])
+    for m, prepare in ((4, sh.sherry_gemm_batched_prepare), (16, sh.sherry_gemm_batched_prepare),
+                       (64, sh.sherry_gemm_batched_prepare), (4, sh.sherry_gemm_il_batched_prepare),
+                       (16, sh.sherry_gemm_il_batched_prepare)):
+        got = []
+        for order in (list(range(len(blk))), list(reversed(range(len(blk))))):
+            descs = (sh.sherry_gemm_desc * len(blk))()
+            for j, i in enumerate(order):
+                d = descs[j]
+                d.w, d.x, d.x_scale, d.y = FAKE, FAKE, FAKE, FAKE
+                d.n, d.k, d.m, d.w_scale = blk[i].n, blk[i].k, m, 0.02
+            total, _ = prepare(descs)
+            r = {i: (descs[j].block_begin, descs[j].block_count) for j, i in enumerate(order)}
+            spans = sorted(r.values())
+            assert spans[0][0] == 0 and all(a[0] + a[1] == b[0] for a, b in zip(spans, spans[1:]))
+            assert spans[-1][0] + spans[-1][1] == total
+            assert all(c >= 1 for _, c in spans)
+            longest = max(lin.k for lin in blk)
+            first = [i for i in r if blk[i].k == longest]
+            assert sorted(r[i][0] for i in first) == [b for b, _ in spans[:len(first)]]
+            got.append((r, total))
+        assert got[0][0].keys() == got[1][0].keys() and got[0][1] == got[1][1]
+        assert all(got[0][0][i][1] == got[1][0][i][1] for i in got[0][0])
+
+
 def test_il_grouped_prepare_without_launch():
     def prep(cases, group=False):
         descs = (sh.sherry_gemm_desc * len(cases))()
@@ -193,7 +224,9 @@ def test_il_grouped_prepare_without_launch():
         total, max_m = sh.sherry_gemm_il_batched_prepare(descs)
         return [d.block_begin for d in descs], total, max_m
     # the same block counts and launch values as the tiled grouped launches
-    assert prep([(4, 3072, 3072), (2, 1024, 3072), (1, 3072, 8192)]) == ([0, 12, 16], 40, 4)
+    # (blocks numbered longest rows first: the k = 8192 product's 24, then the
+    # k = 3072 ones in array order)
+    assert prep([(4, 3072, 3072), (2, 1024, 3072), (1, 3072, 8192)]) == ([24, 36, 0], 40, 4)
     assert prep([(4, 3072, 8320), (1, 64, 128)]) == ([0, 12], 13, 5)
     assert prep([(16, 3072, 8192), (9, 1024, 3072)]) == ([0, 12], 16, 16)
     with pytest.raises(sh.SherryError) as e:
@@ -360,7 +393,9 @@ def test_gemm_batched_prepare_picks_the_token_gemv():
     # up to 4 tokens, activations fit 32 KB of LDS: the matrix-core GEMV
     # (the int8 GEMV's work split, 8-wave blocks, at most 16 units per wave:
     # 48 tiles x S=2 / 8, 16 x 2 / 8, 48 x 4 / 8)
-    assert prep([(4, 3072, 3072), (2, 1024, 3072), (1, 3072, 8192)]) == ([0, 12, 16], 40, 4)
+    # (blocks numbered longest rows first: the k = 8192 product's 24, then the
+    # k = 3072 ones in array order)
+    assert prep([(4, 3072, 3072), (2, 1024, 3072), (1, 3072, 8192)]) == ([24, 36, 0], 40, 4)
     assert prep([(1, 64, 128)]) == ([0], 1, 1)
     # too long for the staging, or 5-16 tokens: the 16-token window kernel
     # (launch value 5-16; four 64-row tiles per workgroup, whole K)
