@@ -112,6 +112,17 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
   const int part = __builtin_amdgcn_readfirstlane(tid / G::BN);
   const int wi = wrow % kTileRows;  // row within its unit (n0 is a multiple of 64)
 
+  // the scales of the tile's rows and columns, for the epilogue: loaded
+  // first and parked in LDS with the first stage, because one counter tracks
+  // a wave's loads and stores, so a load between the epilogue's stores would
+  // wait for every store before it
+  static_assert(G::THREADS >= G::BM && G::THREADS >= G::BN, "one scale per thread");
+  __shared__ float sxs[G::BM];
+  __shared__ float sws[G::BN];
+  float sxp = 0.0f, swp = 0.0f;
+  if (tid < G::BM && m0 + tid < M) sxp = x_scale[m0 + tid];
+  if (tid < G::BN && n0 + tid < N) swp = ws.at(n0 + tid);
+
   uint4 xr[G::XPT];
   uint32_t wd[5];
   const bool k16 = (K % 16) == 0;
@@ -284,6 +295,8 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
   load_step(0);
   __syncthreads();  // lut ready
   store_step(smem);
+  if (tid < G::BM) sxs[tid] = sxp;
+  if (tid < G::BN) sws[tid] = swp;
   if (C > 1) load_step(1);
   __syncthreads();
 
@@ -380,12 +393,12 @@ __global__ __launch_bounds__(G::THREADS) void gemm_kernel(
           }
           continue;
         }
-        const float sx = x_scale[gm];
+        const float sx = sxs[wr * G::WM + a * 32 + row];
         float o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if constexpr (GR) o[e] = __int_as_float(vv[e]) * sx;
-          else o[e] = static_cast<float>(vv[e]) * (sx * ws.at(gn + e));
+          else o[e] = static_cast<float>(vv[e]) * (sx * sws[wc * G::WN + 4 * c4 + e]);
         }
         if (vec) {
           *reinterpret_cast<float4*>(y + gm * N + gn) = make_float4(o[0], o[1], o[2], o[3]);

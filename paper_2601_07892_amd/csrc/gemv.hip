@@ -524,13 +524,21 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
   prelude.issue();
   float sx[M];
   prelude.finish(sx);
-  // a per-channel scale for this thread's first output is loaded now, so
-  // its latency hides behind the stream instead of ending the workgroup
-  float sw0 = ws.tensor;
-  if (ws.rows && static_cast<int>(threadIdx.x) < tpb * M * 64) {
-    const int r0 = g * tpb + static_cast<int>(threadIdx.x >> 6) / M;
-    const int64_t row0 = int64_t(r0) * kTileRows + (threadIdx.x & 63);
-    if (r0 < R && row0 < n) sw0 = as_global(ws.rows)[row0];
+  // the per-channel scales of this thread's outputs (output t = threadIdx.x
+  // + j * kGemvThreads: row 64 (g tpb + (t / 64) / M) + t % 64) are loaded
+  // now: their latency hides behind the stream instead of ending the
+  // workgroup, and no load sits between the epilogue's stores (one counter
+  // tracks a wave's loads and stores, so it would wait for every store
+  // before it)
+  constexpr int kOut = (kGemvWaves * M * 64 + kGemvThreads - 1) / kGemvThreads;
+  float swo[kOut];
+#pragma unroll
+  for (int j = 0; j < kOut; ++j) {
+    const int t = static_cast<int>(threadIdx.x) + j * kGemvThreads;
+    const int r0 = g * tpb + (t >> 6) / M;
+    const int64_t row0 = int64_t(r0) * kTileRows + (t & 63);
+    swo[j] = (ws.rows && t < tpb * M * 64 && r0 < R && row0 < n) ? as_global(ws.rows)[row0]
+                                                                  : ws.tensor;
   }
   __builtin_amdgcn_sched_barrier(0);
   float accf[M];
@@ -615,8 +623,15 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
     for (int m = 0; m < M; ++m) redf[(wave * M + m) * 64 + lane] = accf[m];
   }
   __syncthreads();
+  // the scales are waited for here, once, before the first store (a wait
+  // inside the loop would also wait for the stores issued before it)
+#pragma unroll
+  for (int j = 0; j < kOut; ++j) asm volatile("" ::"v"(swo[j]));
   // thread t -> (tile lt2, token m, row i); the S waves of a tile are adjacent
-  for (int t = threadIdx.x; t < tpb * M * 64; t += kGemvThreads) {
+#pragma unroll
+  for (int j = 0; j < kOut; ++j) {
+    const int t = static_cast<int>(threadIdx.x) + j * kGemvThreads;
+    if (t >= tpb * M * 64) break;
     const int i = t & 63;
     const int m = (t >> 6) % M;
     const int lt2 = (t >> 6) / M;
@@ -630,7 +645,7 @@ __device__ __forceinline__ void gemv_block(const uint8_t* w_, const X& xsrc, Pre
       for (int p = 0; p < S; ++p) f += redf[((lt2 * S + p) * M + m) * 64 + i];
       as_global_mut(y)[m * n + row] = f * sx[m];
     } else {
-      const float s = sx[m] * (t == static_cast<int>(threadIdx.x) ? sw0 : ws.at(row));
+      const float s = sx[m] * swo[j];
       as_global_mut(y)[m * n + row] = static_cast<float>(a) * s;
     }
     if (acc_out) as_global_mut(acc_out)[m * n + row] = a;

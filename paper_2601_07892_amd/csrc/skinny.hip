@@ -238,6 +238,25 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
   const int r = g * T + wave / S;
   const int sp = wave % S;
   const int u0 = sp * U, u1 = (u0 + U < C) ? u0 + U : C;
+  // the scales of this lane's epilogue stores (tokens (lane >> 3) + 8i of
+  // each 32-token block, rows 32h + 4(lane & 7) + u of the tile), loaded
+  // before any other load: one counter tracks a wave's loads and stores, so a
+  // load issued between the stores would wait for every store before it
+  float sxl[MT][4], swl[2][4];
+#pragma unroll
+  for (int tb = 0; tb < MT; ++tb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tok = 32 * tb + (lane >> 3) + 8 * i;
+      sxl[tb][i] = tok < p.m ? as_global(p.x_scale)[tok] : 0.0f;
+    }
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int row = r * kTileRows + 32 * h + 4 * (lane & 7) + u;
+      swl[h][u] = (!GR && row < p.n) ? p.ws.at(row) : 0.0f;
+    }
   const bool live = r < R && u0 < u1;
   const UnitRun rs{p.w + (int64_t(r < R ? r : 0) * C + (live ? u0 : 0)) * kUnitBytes,
                    live ? u1 - u0 : 0};
@@ -487,13 +506,13 @@ __device__ __forceinline__ void sk_block(const SkProblem& p, int g, const uint32
         const int tok = 32 * tb + tl;
         const int row = r * kTileRows + 32 * h + 4 * c4;
         if (tok >= p.m || row >= p.n) continue;
-        const float sx = as_global(p.x_scale)[tok];
+        const float sx = sxl[tb][i];
         const int32_t vv[4] = {v.x, v.y, v.z, v.w};
         float o[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           if constexpr (GR) o[u] = __int_as_float(vv[u]) * sx;
-          else o[u] = static_cast<float>(vv[u]) * (sx * p.ws.at(row + u));
+          else o[u] = static_cast<float>(vv[u]) * (sx * swl[h][u]);
         }
         float* yrow = as_global_mut(p.y) + int64_t(tok) * p.n + row;
         if (vec) {
