@@ -933,7 +933,8 @@ def _channel_scales(n, seed):
 # every kernel (GEMV up to 4 tokens, register-decoded, LDS-tiled) with ragged
 # n and k: int32 acc as the per-tensor path, y scaled per output channel
 CHANNEL_CASES = [(1, 70, 132, "GEMV"), (4, 600, 2048, "GEMV"), (9, 130, 1028, "SKINNY"),
-                 (100, 257, 388, "SKINNY"), (33, 300, 1032, "MFMA"), (300, 520, 2052, "MFMA")]
+                 (100, 257, 388, "SKINNY"), (33, 300, 1032, "MFMA"), (300, 520, 2052, "MFMA"),
+                 (40, 258, 1028, "MFMA"), (130, 1027, 640, "MFMA")]
 
 
 @pytest.mark.parametrize("m,n,k,kernel", CHANNEL_CASES)
