@@ -12,8 +12,8 @@
 // 32 codes are then packed by one lane into its 16-byte head and 4-byte tail,
 // while the next 8 units' loads are in flight.
 // Rows past n, blocks past k and units past the padded row read as zeros
-// (buffer loads past the row return zero) and so become code 0, the padding
-// code.  The alpha of a row (Eq. 5) adds its 32 lanes' partial sums in a
+// (their offsets fall outside the range of the wave's buffer resource) and so
+// become code 0, the padding code.  The alpha of a row (Eq. 5) adds its 32 lanes' partial sums in a
 // fixed order.
 #include "sherry_internal.h"
 
@@ -24,23 +24,24 @@ constexpr int kTpRound = 8;  // units in flight per round
 
 // Code of one block (Eq. 4): the smallest |w| is dropped (ties to the lowest
 // position); the other three keep their sign, +1 for a kept zero.  Adds the
-// kept magnitudes to kept.
+// kept magnitudes to kept, in ascending position (the dropped one adds +0,
+// which leaves the fp64 sum unchanged).  Branch-free: the sign bits of the
+// four weights are gathered and the dropped position's bit is cut out.
 __device__ __forceinline__ uint32_t tp_block(const float4 v, double& kept) {
-  const float w[4] = {v.x, v.y, v.z, v.w};
-  const float a[4] = {fabsf(v.x), fabsf(v.y), fabsf(v.z), fabsf(v.w)};
-  int z = 0;
-#pragma unroll
-  for (int p = 1; p < 4; ++p) z = (a[p] < a[z]) ? p : z;
-  uint32_t neg = 0;  // sign bit of the i-th kept weight, ascending position
-  int i = 0;
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    if (p == z) continue;
-    neg |= (w[p] < 0.0f ? 1u : 0u) << i;
-    kept += static_cast<double>(a[p]);
-    ++i;
-  }
-  return static_cast<uint32_t>(z) | (neg << 2);
+  const float a0 = fabsf(v.x), a1 = fabsf(v.y), a2 = fabsf(v.z), a3 = fabsf(v.w);
+  uint32_t z = 0;
+  float lo = a0;
+  if (a1 < lo) { z = 1; lo = a1; }
+  if (a2 < lo) { z = 2; lo = a2; }
+  if (a3 < lo) z = 3;
+  const uint32_t s = (v.x < 0.0f ? 1u : 0u) | (v.y < 0.0f ? 2u : 0u) | (v.z < 0.0f ? 4u : 0u) |
+                     (v.w < 0.0f ? 8u : 0u);
+  const uint32_t neg = (s & ((1u << z) - 1u)) | ((s >> (z + 1u)) << z);
+  kept += static_cast<double>(z == 0 ? 0.0f : a0);
+  kept += static_cast<double>(z == 1 ? 0.0f : a1);
+  kept += static_cast<double>(z == 2 ? 0.0f : a2);
+  kept += static_cast<double>(z == 3 ? 0.0f : a3);
+  return z | (neg << 2);
 }
 
 // Code j of a unit row sits at bits [5j, 5j + 5) of the 160-bit row
@@ -72,17 +73,26 @@ __global__ __launch_bounds__(32 * ROWS) void ternarize_pack_kernel(
   const int r0 = (blockIdx.x % QUARTERS) * ROWS;  // first row within the tile
   const int64_t row = tile * kTileRows + r0 + rl;
   const int64_t C = (k + kTileK - 1) / kTileK, nb = k / 4;
-  const bool in = row < n;
+  // one buffer resource per wave (it must be wave-uniform): the wave's two
+  // rows, rows past n left out of its range; a lane's block past the end of
+  // its row gets an offset past the range, so both read as zeros (k % 4 == 0,
+  // so no block straddles two rows)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t wrow0 = tile * kTileRows + r0 + 2 * wave;  // rows rl & ~1 and rl | 1
+  const int64_t wrows = n - wrow0 < 0 ? 0 : (n - wrow0 < 2 ? n - wrow0 : 2);
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(w) + (in ? row : 0) * k, 0, in ? static_cast<int>(k * 4) : 0,
+      const_cast<float*>(w) + (wrows > 0 ? wrow0 : 0) * k, 0, static_cast<int>(wrows * k * 4),
       kBufferWord3);
+  const int rowoff = static_cast<int>((rl & 1) * k * 4);
+  constexpr int kPastRange = 0x7ffffff0;
   double kept = 0.0;
   float4 v[kTpRound];
   auto load_round = [&](int64_t c0) {
 #pragma unroll
     for (int u = 0; u < kTpRound; ++u) {
-      const u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(
-          rs, static_cast<int>(((c0 + u) * 32 + j) * 16), 0, kLoadStream);
+      const int64_t blk = (c0 + u) * 32 + j;
+      const int off = blk < nb ? rowoff + static_cast<int>(blk * 16) : kPastRange;
+      const u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kLoadStream);
       v[u] = make_float4(__uint_as_float(raw.x), __uint_as_float(raw.y), __uint_as_float(raw.z),
                          __uint_as_float(raw.w));
     }
@@ -95,8 +105,8 @@ __global__ __launch_bounds__(32 * ROWS) void ternarize_pack_kernel(
     if (c0 + kTpRound < C) load_round(c0 + kTpRound);
     __syncthreads();
     // unit c0 + u, row lane: one lane per unit row packs its 32 codes
-    const int wv = tid >> 6, lane = tid & 63;
-    for (int u = wv; u < kTpRound; u += WAVES) {
+    const int lane = tid & 63;
+    for (int u = wave; u < kTpRound; u += WAVES) {
       if (lane < ROWS && c0 + u < C) {
         uint32_t d[5] = {0, 0, 0, 0, 0};
         tp_pack(codes[u][lane], d, std::make_integer_sequence<int, 32>{});

@@ -1007,7 +1007,7 @@ def _ulp_close(a, b):
 
 
 @pytest.mark.parametrize("n,k", [(1, 4), (63, 128), (64, 132), (70, 1028), (130, 260),
-                                 (512, 4096), (8192, 3072)])
+                                 (1031, 516), (4097, 256), (512, 4096), (8192, 3072)])
 def test_ternarize_pack_parity(dev, n, k):
     # packed bytes identical to packing the oracle's ternary matrix (padding
     # included); per-channel alpha within one fp32 unit of the oracle's fp64
