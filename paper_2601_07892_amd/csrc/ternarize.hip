@@ -13,8 +13,8 @@
 // while the next 8 units' loads are in flight.
 // Rows past n, blocks past k and units past the padded row read as zeros
 // (their offsets fall outside the range of the wave's buffer resource) and so
-// become code 0, the padding code.  The alpha of a row (Eq. 5) adds its 32 lanes' partial sums in a
-// fixed order.
+// become code 0, the padding code.  The alpha of a row (Eq. 5) adds its 32
+// lanes' partial sums in a fixed order.
 #include "sherry_internal.h"
 
 namespace sherry {
